@@ -1,0 +1,140 @@
+/*
+ * ROCKET transform oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Only tests/, the smoke check and the benchmark's CPU-baseline leg may load
+ * this file's library.  The product path (the HIP library and its Python
+ * binding) never calls it, and this file shares no code, header or table
+ * with that path.
+ *
+ * What it computes (CUROCKET paper, Sec. 2.1 "ROCKET" and Sec. 3.2
+ * "Implementing CUROCKET"):
+ *   every kernel k has a length l, weights w[0..l-1], a bias b, a dilation d
+ *   and a zero padding p.  Convolving it with a series x of length L is a
+ *   run of dot products, one per output position t = 0 .. O-1 with
+ *       O   = L + 2p - (l-1) d                (number of dot products)
+ *       y_t = b + sum_j w[j] * xz[t - p + j d]
+ *   where xz is x with zeros outside [0, L) (the zero padding of Sec. 2.1).
+ *   Two features come out of the run of y_t:
+ *       PPV = |{t : y_t > 0}| / O   (proportion of positive values, divided by
+ *                                    the number of dot products as Sec. 3.2 says)
+ *       MAX = max_t y_t.
+ *   Feature layout: F[i, 2k] = PPV, F[i, 2k+1] = MAX, in kernel order.
+ *
+ * Readings where the paper is silent (listed with reasons in the design notes):
+ *   - cross-correlation orientation: tap j multiplies xz[t - p + j d];
+ *   - "positive" is strict (y > 0);
+ *   - evaluation in fp64 on the fp32 inputs (the paper notes that rounding
+ *     near zero moves PPV slightly between devices, Sec. 5).
+ *
+ * Besides F it returns, per (row, kernel), the integer positive count and a
+ * certified interval for the count that any fp32 evaluation of the same sums
+ * can produce, in any summation order, with or without fused multiply-add:
+ *       beta_t = gamma_{l+1} * (|b| + sum_j |w[j] xz[..]|) + (l+1) * 2^-126
+ *       cnt_lo = |{t : y_t >  beta_t}|,  cnt_hi = |{t : y_t > -beta_t}|
+ * with gamma_m = m u / (1 - m u), u = 2^-24 (the standard error bound of a
+ * floating-point dot product of m terms; the 2^-126 term covers flushing of
+ * subnormal intermediates).  beta_max = max_t beta_t bounds the error of MAX.
+ *
+ * Plain loops: rows -> kernels -> t -> j.  No SIMD intrinsics, no fast-math.
+ * OpenMP only splits rows across threads (for timing the CPU baseline).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORACLE_OK = 0, ORACLE_ERR_ARG = -1, ORACLE_ERR_LENGTH = -2 };
+
+static double gamma_m(int m) {
+    const double u = ldexp(1.0, -24);
+    return (m * u) / (1.0 - m * u);
+}
+
+/* Number of dot products of one kernel on a series of length L (Sec. 2.1). */
+int64_t oracle_output_length(int32_t L, int32_t length, int32_t dilation, int32_t padding) {
+    return (int64_t)L + 2 * (int64_t)padding - (int64_t)(length - 1) * (int64_t)dilation;
+}
+
+/*
+ * X        : fp32 [n_rows_total, L] row-major.
+ * rows     : optional list of n_out row indices into X (NULL: rows 0..n_out-1).
+ * kernels  : SoA arrays of K kernels; weights row stride wstride (>= length).
+ * F        : fp64 [n_out, 2K]  (PPV, MAX interleaved per kernel).
+ * cnt, cnt_lo, cnt_hi : int64 [n_out, K] (may be NULL).
+ * beta_max : fp64 [n_out, K] (may be NULL).
+ * nthreads : OpenMP threads (<= 0: runtime default).
+ */
+int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, int64_t n_out,
+                     int32_t L, int32_t K, const int32_t *length, const int32_t *dilation,
+                     const int32_t *padding, const float *bias, const float *weights,
+                     int32_t wstride, double *F, int64_t *cnt, int64_t *cnt_lo,
+                     int64_t *cnt_hi, double *beta_max, int nthreads) {
+    if (!X || !length || !dilation || !padding || !bias || !weights || !F) return ORACLE_ERR_ARG;
+    if (L < 1 || K < 1 || n_out < 0 || wstride < 1) return ORACLE_ERR_ARG;
+    for (int32_t k = 0; k < K; ++k) {
+        if (length[k] < 1 || length[k] > wstride || dilation[k] < 1 || padding[k] < 0)
+            return ORACLE_ERR_ARG;
+        if (oracle_output_length(L, length[k], dilation[k], padding[k]) < 1) return ORACLE_ERR_LENGTH;
+    }
+    if (rows) {
+        for (int64_t r = 0; r < n_out; ++r)
+            if (rows[r] < 0 || rows[r] >= n_rows_total) return ORACLE_ERR_ARG;
+    } else if (n_out > n_rows_total) {
+        return ORACLE_ERR_ARG;
+    }
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n_out; ++r) {
+        const int64_t row = rows ? rows[r] : r;
+        const float *x = X + row * (int64_t)L;
+        for (int32_t k = 0; k < K; ++k) {
+            const int32_t len = length[k], d = dilation[k], p = padding[k];
+            const float *w = weights + (int64_t)k * wstride;
+            const double b = (double)bias[k];
+            const int64_t O = oracle_output_length(L, len, d, p);
+            const double g = gamma_m(len + 1);
+            const double tiny = (len + 1) * ldexp(1.0, -126);
+            int64_t positive = 0, lo = 0, hi = 0;
+            double mx = -INFINITY, bmax = 0.0;
+            for (int64_t t = 0; t < O; ++t) {
+                double y = b;
+                double mag = fabs(b);
+                for (int32_t j = 0; j < len; ++j) {
+                    const int64_t m = t - p + (int64_t)j * d;
+                    const double xv = (m >= 0 && m < L) ? (double)x[m] : 0.0;
+                    y += (double)w[j] * xv;
+                    mag += fabs((double)w[j] * xv);
+                }
+                const double beta = g * mag + tiny;
+                if (y > 0.0) ++positive;
+                if (y > beta) ++lo;
+                if (y > -beta) ++hi;
+                if (y > mx) mx = y;
+                if (beta > bmax) bmax = beta;
+            }
+            F[r * 2 * (int64_t)K + 2 * k] = (double)positive / (double)O;
+            F[r * 2 * (int64_t)K + 2 * k + 1] = mx;
+            if (cnt) cnt[r * (int64_t)K + k] = positive;
+            if (cnt_lo) cnt_lo[r * (int64_t)K + k] = lo;
+            if (cnt_hi) cnt_hi[r * (int64_t)K + k] = hi;
+            if (beta_max) beta_max[r * (int64_t)K + k] = bmax;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* Threads the OpenMP runtime would use (reported with the CPU baseline). */
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,131 @@
+"""Shared helpers for the tests (fixture parsing, brute force, kernel sets)."""
+import glob
+import math
+import os
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+MAX_LEN = 11
+
+
+def load_golden():
+    """Parse every worked-example fixture under tests/golden/."""
+    out = []
+    for path in sorted(glob.glob(os.path.join(GOLDEN, "w*.txt"))):
+        rec = {"name": os.path.basename(path)}
+        with open(path) as f:
+            for line in f:
+                line = line.split("#", 1)[0].strip()
+                if not line:
+                    continue
+                key, val = line.split(":", 1)
+                vals = [float(v) for v in val.split()]
+                rec[key.strip()] = vals if len(vals) > 1 or key.strip() in ("x", "w", "y") else vals[0]
+        out.append(rec)
+    return out
+
+
+def kernel_set(lengths, dilations, paddings, biases, weights):
+    """Kernel arrays in the shared SoA layout (weights row stride 11, zero tail)."""
+    K = len(lengths)
+    W = np.zeros((K, MAX_LEN), dtype=np.float32)
+    for k, w in enumerate(weights):
+        W[k, :len(w)] = np.asarray(w, dtype=np.float32)
+    return dict(length=np.asarray(lengths, dtype=np.int32),
+                dilation=np.asarray(dilations, dtype=np.int32),
+                padding=np.asarray(paddings, dtype=np.int32),
+                bias=np.asarray(biases, dtype=np.float32), weights=W)
+
+
+def brute_force(X, kernels):
+    """Literal transcription of the definitions with Python floats (fp64).
+
+    For every row and kernel: the dot products y_t, t < O, then PPV (strictly
+    positive share) and MAX.  Independent of the C oracle; small inputs only.
+    """
+    n, L = X.shape
+    K = len(kernels["length"])
+    F = np.zeros((n, 2 * K))
+    for i in range(n):
+        x = [float(v) for v in X[i]]
+        for k in range(K):
+            ln = int(kernels["length"][k])
+            d = int(kernels["dilation"][k])
+            p = int(kernels["padding"][k])
+            b = float(kernels["bias"][k])
+            w = [float(v) for v in kernels["weights"][k][:ln]]
+            O = L + 2 * p - (ln - 1) * d
+            ys = []
+            for t in range(O):
+                acc = b
+                for j in range(ln):
+                    m = t - p + j * d
+                    if 0 <= m < L:
+                        acc += w[j] * x[m]
+                ys.append(acc)
+            F[i, 2 * k] = sum(1 for y in ys if y > 0) / O
+            F[i, 2 * k + 1] = max(ys)
+    return F
+
+
+def random_kernels(rng, K, L, max_len=MAX_LEN):
+    """Random valid kernels (any length 1..11, any admissible dilation, either
+    padding choice) for brute-force cross-checks."""
+    lengths, dil, pad, bias, weights = [], [], [], [], []
+    for _ in range(K):
+        ln = int(rng.choice([1, 2, 3, 5, 7, 9, 11])) if max_len >= 11 else int(rng.integers(1, max_len + 1))
+        ln = min(ln, L)
+        dmax = max(1, (L - 1) // max(1, ln - 1)) if ln > 1 else int(rng.integers(1, 5))
+        d = int(rng.integers(1, dmax + 1))
+        p = ((ln - 1) * d) // 2 if rng.integers(2) else 0
+        if L + 2 * p - (ln - 1) * d < 1:
+            p = ((ln - 1) * d) // 2
+        lengths.append(ln)
+        dil.append(d)
+        pad.append(p)
+        bias.append(float(rng.uniform(-1, 1)))
+        weights.append(rng.standard_normal(ln).astype(np.float32))
+    return kernel_set(lengths, dil, pad, bias, weights)
+
+
+def fp32_features(X, kernels, order="ascending"):
+    """fp32 evaluation in numpy with a chosen summation order, used to check
+    that the oracle's certified intervals contain real fp32 results."""
+    n, L = X.shape
+    K = len(kernels["length"])
+    cnt = np.zeros((n, K), dtype=np.int64)
+    mx = np.zeros((n, K), dtype=np.float64)
+    for k in range(K):
+        ln = int(kernels["length"][k])
+        d = int(kernels["dilation"][k])
+        p = int(kernels["padding"][k])
+        b = np.float32(kernels["bias"][k])
+        w = kernels["weights"][k][:ln].astype(np.float32)
+        O = L + 2 * p - (ln - 1) * d
+        xz = np.zeros((n, L + 2 * p + 1), dtype=np.float32)
+        xz[:, p:p + L] = X
+        taps = range(ln) if order == "ascending" else range(ln - 1, -1, -1)
+        y = np.full((n, O), b, dtype=np.float32) if order == "ascending" else np.zeros((n, O), np.float32)
+        for j in taps:
+            y = (y + w[j] * xz[:, j * d:j * d + O]).astype(np.float32)
+        if order != "ascending":
+            y = (y + b).astype(np.float32)
+        cnt[:, k] = (y > 0).sum(axis=1)
+        mx[:, k] = y.max(axis=1)
+    return cnt, mx
+
+
+def ceil_div(a, b):
+    return -(-a // b)
+
+
+def z_norm(x):
+    x = np.asarray(x, dtype=np.float64)
+    sd = x.std(axis=1, keepdims=True)
+    sd[sd == 0] = 1
+    return ((x - x.mean(axis=1, keepdims=True)) / sd).astype(np.float32)
+
+
+__all__ = ["load_golden", "kernel_set", "brute_force", "random_kernels", "fp32_features",
+           "ceil_div", "z_norm", "math"]
