@@ -1,0 +1,248 @@
+#!/usr/bin/env python3
+"""ROCKET transform throughput on one MI355X.
+
+One step = one full transform pass over the workload's series (every row,
+every kernel: X[n, L] -> F[n, 2K]) with X already resident in HBM.  Prints
+one JSON line: series x kernels per second, the roofline position of the
+fused kernel (fp32 MFMA bound, 157.3 TFLOP/s peak) and, on the side, the
+fp64 oracle timed on this host's cores over a bounded row sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload manufacturing]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 (matrix and vector, published)
+PEAK_FP32_FMA_NOPACK = 78.6   # fp32 vector FMA without packed instructions
+F_RESIDENT_LIMIT = 16 << 30   # above this the feature matrix is streamed in row batches
+DEFAULT_BATCH_ROWS = 100000
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def valid_taps(kernels, L):
+    """Products whose series index lands inside [0, L) (padding zeros excluded),
+    summed over kernels: the algorithmic FMA count of one series."""
+    ln = kernels["length"].astype(np.int64)
+    d = kernels["dilation"].astype(np.int64)
+    p = kernels["padding"].astype(np.int64)
+    O = L + 2 * p - (ln - 1) * d
+    total = 0
+    for j in range(11):
+        on = j < ln
+        lo = np.maximum(0, p - j * d)
+        hi = np.minimum(O, p - j * d + L)
+        total += int(np.where(on, np.maximum(0, hi - lo), 0).sum())
+    nominal = int((ln * O).sum())
+    return total, nominal
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for name in ("transform.hip", "plan.cpp", "rocket_internal.h"):
+        with open(os.path.join(ROOT, "paper_2601_17091_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(workload, digest):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "rocket_fused_kernel_%s_pmc.json" % workload)
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_digest") != digest:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="manufacturing")
+    ap.add_argument("--batch-rows", type=int, default=0,
+                    help="rows per F batch (0: whole F if it fits %d GiB)" % (F_RESIDENT_LIMIT >> 30))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--direct", action="store_true", help="time the plain kernel instead")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs the transform on a single "
+              "MI355X (rows shard across GPUs with no exchange; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2601_17091_amd as rk
+    from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
+
+    if not os.path.exists(rk.rocket.LIB_PATH):
+        from paper_2601_17091_amd import build_lib
+        build_lib.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(dev)
+
+    log("workload %s: n=%d L=%d K=%d" % (w.name, w.n, w.L, w.n_kernels))
+    ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
+    t0 = time.perf_counter()
+    X_np = workload_series(w.name)
+    log("series generated in %.1f s" % (time.perf_counter() - t0))
+    X = torch.from_numpy(X_np).to(dev)
+
+    t0 = time.perf_counter()
+    plan = rk.Plan(ks, w.L, direct=args.direct)
+    torch.cuda.synchronize()
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    info = plan.info()
+    log("plan: %s (%.1f ms)" % (info, plan_ms))
+
+    K2 = 2 * w.n_kernels
+    batch = args.batch_rows or (w.n if w.n * K2 * 4 <= F_RESIDENT_LIMIT else DEFAULT_BATCH_ROWS)
+    batch = min(batch, w.n)
+    F = torch.empty((batch, K2), dtype=torch.float32, device=dev)
+    n_batches = (w.n + batch - 1) // batch
+    stream = torch.cuda.current_stream()
+
+    def one_pass():
+        for r0 in range(0, w.n, batch):
+            nb = min(batch, w.n - r0)
+            plan.transform_into(X[r0:r0 + nb], F[:nb], stream)
+
+    for i in range(args.warmup):
+        one_pass()
+        torch.cuda.synchronize()
+        log("warmup %d/%d done" % (i + 1, args.warmup))
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        one_pass()
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    log("timed %d passes: %.3f ms per pass" % (args.steps, ms_per_step))
+
+    valid_per_row, nominal_per_row = valid_taps(ks, w.L)
+    flops_per_pass = 2.0 * w.n * valid_per_row
+    launches = n_batches
+    per_launch_ms = ms_per_step / launches
+    achieved = (flops_per_pass / launches) / (per_launch_ms * 1e-3) / 1e12
+    mfma_fma_per_pass = 256.0 * info["mfma_per_row"] * w.n
+    pairs_per_s = w.n * w.n_kernels / (ms_per_step * 1e-3)
+    digest = source_digest()
+    traffic = None if args.direct else traffic_from_profile(w.name, digest)
+
+    # parity of sampled rows and the CPU baseline on the same rows
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        from oracle import rocket_oracle
+        rocket_oracle.build()
+        threads = rocket_oracle.max_threads()
+        rng_rows = sample_rows(w.n, batch, 4096)
+        t0 = time.perf_counter()
+        rocket_oracle.transform(X_np, ks, rows=rng_rows[:2], threads=threads)
+        per_row = max((time.perf_counter() - t0) / 2.0, 1e-6)
+        m = int(max(2, min(rng_rows.shape[0], args.cpu_seconds / per_row * threads)))
+        rows = np.unique(np.concatenate([rng_rows[:2], rng_rows[-2:],
+                                         np.random.default_rng(3).choice(rng_rows, m, replace=False)]))
+        log("oracle on %d rows (%d threads)" % (rows.shape[0], threads))
+        t0 = time.perf_counter()
+        ref = rocket_oracle.transform(X_np, ks, rows=rows, threads=threads)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": rows.shape[0] * w.n_kernels / cpu_s, "unit": "series*kernels/s",
+               "cores": threads, "kind": "oracle",
+               "sample": "%d of %d %s rows (first/last row, first/last of each batch, seeded "
+                         "random), all %d kernels, fp64, %.1f s" % (rows.shape[0], w.n, w.name,
+                                                                     w.n_kernels, cpu_s)}
+        # GPU features of the same rows
+        got = np.zeros((rows.shape[0], K2), np.float32)
+        for r0 in range(0, w.n, batch):
+            nb = min(batch, w.n - r0)
+            sel = rows[(rows >= r0) & (rows < r0 + nb)]
+            if sel.size == 0:
+                continue
+            plan.transform_into(X[r0:r0 + nb], F[:nb], stream)
+            torch.cuda.synchronize()
+            got[np.searchsorted(rows, sel)] = F[torch.from_numpy(sel - r0).to(dev)].cpu().numpy()
+        O = ref["O"][None, :]
+        cnt = np.rint(got[:, 0::2].astype(np.float64) * O)
+        parity = {
+            "rows": int(rows.shape[0]),
+            "max_abs_err_max": float(np.abs(got[:, 1::2] - ref["F"][:, 1::2]).max()),
+            "max_count_err": int(np.abs(cnt - ref["cnt"]).max()),
+            "outside_certified": int(((cnt < ref["cnt_lo"]) | (cnt > ref["cnt_hi"])).sum()
+                                     + (np.abs(got[:, 1::2] - ref["F"][:, 1::2]) > ref["beta"]).sum()),
+        }
+        log("parity %s" % parity)
+
+    out = {
+        "metric": "series*kernels/s (ROCKET transform, fp32, 1 MI355X)",
+        "value": pairs_per_s,
+        "unit": "series*kernels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic (seeded %s series, z-normalised; seeded ROCKET kernels)" % w.kind,
+        "config": {"workload": w.name, "n_series": w.n, "series_length": w.L,
+                   "n_kernels": w.n_kernels, "features": K2, "f_batch_rows": batch,
+                   "kernel_seed": w.kernel_seed, "data_seed": w.data_seed,
+                   "path": "direct" if info["direct"] else "fused-mfma"},
+        "pct_fp32_peak": 100.0 * achieved / PEAK_FP32_TFLOPS,
+        "pct_fp32_fma_nopack_peak": 100.0 * achieved / PEAK_FP32_FMA_NOPACK,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS, "traffic": traffic,
+                     "kernel": "rocket_direct_kernel" if info["direct"] else "rocket_fused_kernel",
+                     "launches_per_step": launches, "launch_ms": per_launch_ms,
+                     "algorithmic_flops_per_launch": flops_per_pass / launches,
+                     "valid_fma_per_series": valid_per_row,
+                     "nominal_fma_per_series": nominal_per_row,
+                     "mfma_fma_issued_per_series": 256 * info["mfma_per_row"],
+                     "mfma_pipe_frac": mfma_fma_issued_frac(mfma_fma_per_pass, ms_per_step)},
+        "plan": dict(info, create_ms=plan_ms),
+        "device": {"name": props.name, "cu": props.multi_processor_count},
+        "source_digest": digest,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def mfma_fma_issued_frac(fma_per_pass, ms_per_step):
+    """Share of the fp32 MFMA peak the issued MFMA work (incl. padding and
+    empty slots) represents."""
+    return 2.0 * fma_per_pass / (ms_per_step * 1e-3) / 1e12 / PEAK_FP32_TFLOPS
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,225 @@
+/*
+ * rocket.h -- C ABI of the MI355X (gfx950) ROCKET transform library.
+ *
+ * ROCKET (CUROCKET paper, Sec. 2.1): n_kernels random convolution kernels,
+ * each with its own length, weights, bias, dilation and zero padding, are
+ * slid over every series; every (series, kernel) pair yields two features,
+ * the proportion of positive values (PPV) and the maximum (MAX) of the run
+ * of dot products.  Sec. 3.2 normalises the positive count by the number of
+ * dot products.
+ *
+ * Definitions used throughout (Sec. 2.1):
+ *   O_k   = L + 2 p_k - (l_k - 1) d_k                  number of dot products
+ *   y_t   = b_k + sum_{j<l_k} w_k[j] * xz[t - p_k + j d_k],  t = 0 .. O_k-1,
+ *           xz = the series with zeros outside [0, L)
+ *   F[i, 2k]   = |{t : y_t > 0}| / O_k   (PPV, computed as (float)count/(float)O_k)
+ *   F[i, 2k+1] = max_t y_t                (MAX)
+ *
+ * Memory and threading rules for every entry point:
+ *   - X (n x L fp32, row-major, contiguous) and F (n x 2 n_kernels fp32,
+ *     row-major) are caller-owned DEVICE memory on the current HIP device.
+ *     The library never frees them.  F is fully overwritten.
+ *   - Kernel sets (rocket_kernels) live in HOST memory.
+ *   - Every argument is validated on the host before any device work; an
+ *     invalid call returns an error and touches nothing.
+ *   - No C++ exception crosses this boundary.
+ *   - Device work is asynchronous on the given HIP stream (NULL = the null
+ *     stream) unless a function says otherwise.
+ */
+#ifndef ROCKET_MI355X_H
+#define ROCKET_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ROCKET_OK = 0,
+    ROCKET_ERR_INVALID_ARG = -1, /* null pointer, non-positive size, bad kernel field */
+    ROCKET_ERR_LENGTH = -2,      /* a kernel has O_k < 1 (or O_k >= 2^24) for this L */
+    ROCKET_ERR_OOM = -3,         /* host or device allocation failed */
+    ROCKET_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed */
+    ROCKET_ERR_INTERNAL = -5     /* should not happen; a bug */
+} rocket_status;
+
+#define ROCKET_MAX_KERNEL_LENGTH 11 /* longest kernel; weights row stride */
+
+/*
+ * A kernel set in structure-of-arrays form (Sec. 2.1 kernel parameters).
+ *   length[k]   in [1, 11]       (generated kernels use 7, 9, 11)
+ *   dilation[k] >= 1
+ *   padding[k]  >= 0             (generated: 0 or (length-1)*dilation/2)
+ *   bias[k]     fp32
+ *   weights[k*max_len + j], j < length[k]; entries beyond length[k] are
+ *               ignored (the generator writes zeros there)
+ *   max_len     weights row stride, in [length max, 11]; generated sets use 11
+ *   input_length the series length the set was generated for (informational
+ *               for hand-built sets; the transform takes L explicitly)
+ */
+typedef struct {
+    int32_t n_kernels;
+    int32_t input_length;
+    int32_t max_len;
+    int32_t *length;
+    int32_t *dilation;
+    int32_t *padding;
+    float *bias;
+    float *weights;
+} rocket_kernels;
+
+/*
+ * Generate n_kernels ROCKET kernels for series of length input_length
+ * (Sec. 2.1): length uniform on {7, 9, 11}; weights standard normal, then
+ * the kernel's mean subtracted (fp64, stored fp32); bias uniform on [-1, 1);
+ * dilation floor(2^x), x uniform on [0, A), A = log2((L-1)/(length-1)),
+ * capped at (L-1)/(length-1); padding (length-1)*dilation/2 with
+ * probability 1/2, else 0.
+ * Random numbers: kernel k, draw slot s in 0..15, is element k*16 + s of the
+ * SplitMix64 sequence started at `seed` (Steele, Lea, Flood 2014); uniforms
+ * take the top 53 bits; normals come from the Box-Muller transform
+ * (slots 1..12, six pairs).  Slot 0: length, 13: bias, 14: dilation,
+ * 15: padding (top bit).  The result depends only on (seed, k, input_length),
+ * so a set of K kernels is a prefix of the set of K' > K kernels.
+ * Host only; never touches a GPU.
+ *
+ * out: filled with library-owned host arrays (max_len = 11); release them
+ *      with rocket_free_kernels.  On error *out is zeroed.
+ * Errors: ROCKET_ERR_INVALID_ARG for out == NULL, n_kernels < 1 or
+ *         input_length < 11 (some length would have no admissible dilation);
+ *         ROCKET_ERR_OOM.
+ */
+rocket_status rocket_generate_kernels(uint64_t seed, int32_t n_kernels, int32_t input_length,
+                                      rocket_kernels *out);
+
+/* Release arrays allocated by rocket_generate_kernels and zero *k.
+ * NULL-safe and idempotent.  Do not call on caller-built sets. */
+void rocket_free_kernels(rocket_kernels *k);
+
+/*
+ * Opaque execution plan for one kernel set and one series length L, on the
+ * HIP device that is current when it is created.  Creating a plan validates
+ * the set, groups the kernels by (length, dilation, padding), builds the
+ * device work tables and uploads them (synchronously).  A plan is immutable
+ * afterwards: transforms on different streams may share it.
+ */
+typedef struct rocket_plan rocket_plan;
+
+/*
+ * Errors: ROCKET_ERR_INVALID_ARG (null pointers, n_kernels < 1, L < 1,
+ *         max_len outside [1, 11], a length outside [1, max_len], dilation < 1,
+ *         padding < 0); ROCKET_ERR_LENGTH (some O_k < 1, or some O_k above
+ *         2^24 - 1); ROCKET_ERR_OOM; ROCKET_ERR_HIP.
+ * On error *out is NULL.
+ */
+rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan **out);
+
+/* Plan flags for rocket_plan_create_ex. */
+#define ROCKET_PLAN_DEFAULT 0u
+#define ROCKET_PLAN_DIRECT 1u /* use the plain one-wavefront-per-pair kernel */
+
+/*
+ * rocket_plan_create with flags.  ROCKET_PLAN_DIRECT selects the plain
+ * kernel: one wavefront per (series, kernel) pair reading the series from
+ * global memory.  It is slower and serves as a second GPU reference; the
+ * default plan also falls back to it when a series (plus the zero margins
+ * the kernels need) does not fit one workgroup's LDS.  Unknown flag bits
+ * give ROCKET_ERR_INVALID_ARG.  Same errors as rocket_plan_create otherwise.
+ */
+rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t flags,
+                                    rocket_plan **out);
+
+/* Free a plan's host and device memory.  NULL-safe.  The caller must make
+ * sure no transform using the plan is still running. */
+void rocket_plan_destroy(rocket_plan *p);
+
+/*
+ * Transform n series with a plan: X_dev [n, L] -> F_dev [n, 2 n_kernels],
+ * features in the ORIGINAL kernel order, interleaved (PPV, MAX) per kernel.
+ * Asynchronous on hip_stream (a hipStream_t; NULL = null stream).
+ * n == 0 is a no-op.  Rows are independent; any row range of X may be
+ * passed (row batching is the caller's loop over pointer offsets).
+ * Errors: ROCKET_ERR_INVALID_ARG (p, X_dev or F_dev NULL with n > 0, n < 0);
+ *         ROCKET_ERR_HIP (launch failure).
+ */
+rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
+                                    float *F_dev, void *hip_stream);
+
+/*
+ * One-shot transform: plan create + transform + plan destroy.  Returns after
+ * the work on hip_stream has completed (it synchronises the stream before
+ * freeing the plan).  Same errors as rocket_plan_create and
+ * rocket_transform_plan.
+ */
+rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const rocket_kernels *k,
+                               float *F_dev, void *hip_stream);
+
+/*
+ * Plan facts for benchmarks and tests (host only).  Any output pointer may
+ * be NULL.
+ *   n_items      number of work items (groups of kernels sharing one bucket)
+ *   n_buckets    number of distinct (length, dilation, padding) buckets
+ *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks)
+ *   lds_bytes    LDS one workgroup uses (0 for the direct kernel)
+ *   direct       1 if the plan runs the direct kernel, else 0
+ * Errors: ROCKET_ERR_INVALID_ARG if p is NULL.
+ */
+rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
+                               int64_t *mfma_per_row, int64_t *lds_bytes, int32_t *direct);
+
+/*
+ * Host-side work tables of the fused kernel, for tests and tools (no GPU is
+ * touched).  rocket_plan_tables_build validates like rocket_plan_create and
+ * fills *out with library-owned arrays; free them with
+ * rocket_plan_tables_free (NULL-safe, idempotent).
+ *   items        n_items x 16 int32, one row per work item:
+ *                [variant, dilation, padding, outputs O, steps S, rounds,
+ *                 lane_off, w_off, k_off, cost, 0 x 6];
+ *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
+ *                7/9/11 taps, G kernel groups of 4 slots
+ *   lanes        lane table: per item and round, 64 entries; bits 0..23 the
+ *                output position of the lane's first step, bit 30 "the
+ *                round's last step is inside the lane's chunk", bit 31 "the
+ *                lane's outputs are counted" (else it duplicates another lane)
+ *   wpk          packed weights, per item [G][taps][4 slots]
+ *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
+ *   order, split_begin, layout_off  item orders for the split counts in
+ *                split_counts[n_layouts]: split s of layout i is
+ *                order[split_begin[layout_off[i] + s] .. split_begin[layout_off[i] + s + 1])
+ *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
+ */
+typedef struct {
+    int64_t n_items;
+    const int32_t *items;
+    int64_t n_lanes;
+    const uint32_t *lanes;
+    int64_t n_wpk;
+    const float *wpk;
+    int64_t n_slots;
+    const float *slot_bias;
+    const int32_t *slot_kernel;
+    int64_t n_order;
+    const int32_t *order;
+    int64_t n_split_begin;
+    const int32_t *split_begin;
+    int32_t n_layouts;
+    const int32_t *layout_off;
+    const int32_t *split_counts;
+    int32_t halo_lo;
+    int32_t halo_hi;
+    int32_t row_stride;
+    void *internal;
+} rocket_plan_tables;
+
+rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32_t L, rocket_plan_tables *out);
+void rocket_plan_tables_free(rocket_plan_tables *t);
+
+/* Static, human-readable name of a status code ("unknown status" otherwise). */
+const char *rocket_status_string(rocket_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROCKET_MI355X_H */

@@ -1,0 +1,254 @@
+// Host-side planning: validation, bucketing of kernels by (length, dilation,
+// padding), work items, lane tables and packed weights for the fused MFMA
+// kernel.  Pure host code; no HIP calls.
+#include <algorithm>
+#include <cstring>
+#include <map>
+#include <new>
+#include <tuple>
+
+#include "rocket_internal.h"
+
+namespace rocket {
+
+static int64_t output_length(int64_t L, int64_t len, int64_t dil, int64_t pad) {
+    return L + 2 * pad - (len - 1) * dil;
+}
+
+rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
+    if (!k || L < 1 || k->n_kernels < 1) return ROCKET_ERR_INVALID_ARG;
+    if (!k->length || !k->dilation || !k->padding || !k->bias || !k->weights)
+        return ROCKET_ERR_INVALID_ARG;
+    if (k->max_len < 1 || k->max_len > ROCKET_MAX_KERNEL_LENGTH) return ROCKET_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < k->n_kernels; ++i) {
+        const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
+        if (len < 1 || len > k->max_len || d < 1 || p < 0) return ROCKET_ERR_INVALID_ARG;
+    }
+    for (int32_t i = 0; i < k->n_kernels; ++i) {
+        const int64_t O = output_length(L, k->length[i], k->dilation[i], k->padding[i]);
+        if (O < 1 || O > kMaxOutputs) return ROCKET_ERR_LENGTH;
+    }
+    return ROCKET_OK;
+}
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+void choose_chunking(int64_t O, int64_t d, int32_t *S_out, int32_t *nc_out, int32_t *rounds_out) {
+    const int64_t C = ceil_div(O, d);  // longest residue class
+    int64_t best_cost = -1, best_nc = 1, best_S = C, best_rounds = ceil_div(d, kWave);
+    const int64_t nc_max = std::min<int64_t>(C, 4096);
+    for (int64_t nc = 1; nc <= nc_max; ++nc) {
+        const int64_t S = ceil_div(C, nc);
+        const int64_t rounds = ceil_div(d * nc, kWave);
+        // steps are what costs; a small per-round charge favours fewer rounds
+        const int64_t cost = 4 * rounds * S + rounds;
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best_nc = nc;
+            best_S = S;
+            best_rounds = rounds;
+        }
+    }
+    *S_out = (int32_t)best_S;
+    *nc_out = (int32_t)best_nc;
+    *rounds_out = (int32_t)best_rounds;
+}
+
+// Lane table of one bucket: chunk c of residue r covers residue positions
+// [floor(c*C_r/nc), floor((c+1)*C_r/nc)), so chunk lengths are S or S-1 and
+// only step S-1 can fall outside a chunk.  Tasks are numbered residue-fastest
+// (task = c*d + r), which keeps neighbouring lanes on neighbouring positions.
+static void build_lane_table(int64_t O, int64_t d, int32_t S, int32_t nc, int32_t rounds,
+                             std::vector<uint32_t> &lanes) {
+    const int64_t ntasks = d * nc;
+    const int64_t nslots = (int64_t)rounds * kWave;
+    // a full-length chunk of residue 0 to duplicate into idle lanes
+    uint32_t dup = 0;
+    {
+        const int64_t C0 = ceil_div(O, d);
+        for (int64_t c = 0; c < nc; ++c) {
+            const int64_t st = c * C0 / nc, en = (c + 1) * C0 / nc;
+            if (en - st == S) {
+                dup = (uint32_t)(st * d) | kLaneLastValid;
+                break;
+            }
+        }
+    }
+    for (int64_t t = 0; t < nslots; ++t) {
+        uint32_t e = dup;  // idle lane: exact duplicate, not counted
+        if (t < ntasks) {
+            const int64_t r = t % d, c = t / d;
+            const int64_t Cr = r < O ? ceil_div(O - r, d) : 0;
+            const int64_t st = c * Cr / nc, en = (c + 1) * Cr / nc;
+            const int64_t len = en - st;
+            if (len >= 1) {
+                e = (uint32_t)(r + st * d) | kLaneCounted | (len == S ? kLaneLastValid : 0u);
+            }
+        }
+        lanes.push_back(e);
+    }
+}
+
+rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
+    try {
+        HostPlan P;
+        P.n_kernels = k->n_kernels;
+        P.L = L;
+        // bucket kernels by (length, dilation, padding); kernels keep their
+        // original order inside a bucket
+        std::map<std::tuple<int32_t, int32_t, int32_t>, std::vector<int32_t>> buckets;
+        int64_t halo_lo = 0, halo_hi = 0;
+        for (int32_t i = 0; i < k->n_kernels; ++i) {
+            const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
+            buckets[std::make_tuple(len, d, p)].push_back(i);
+            const int64_t ell_eff = kEllValues[ell_index_for(len)];
+            halo_lo = std::max<int64_t>(halo_lo, p);
+            halo_hi = std::max<int64_t>(halo_hi, (int64_t)p + d + (ell_eff - len) * (int64_t)d);
+        }
+        P.n_buckets = (int64_t)buckets.size();
+        const int64_t stride = halo_lo + L + halo_hi;
+        if (stride > (int64_t)1 << 30) {
+            // cannot be staged; the plan will use the direct kernel
+            P.halo_lo = P.halo_hi = P.row_stride = 0;
+        } else {
+            P.halo_lo = (int32_t)halo_lo;
+            P.halo_hi = (int32_t)halo_hi;
+            P.row_stride = (int32_t)stride;
+        }
+
+        for (auto &kv : buckets) {
+            const int32_t len = std::get<0>(kv.first), d = std::get<1>(kv.first),
+                          p = std::get<2>(kv.first);
+            const std::vector<int32_t> &ids = kv.second;
+            const int eidx = ell_index_for(len);
+            const int ell = kEllValues[eidx];
+            const int64_t O = output_length(L, len, d, p);
+            int32_t S, nc, rounds;
+            choose_chunking(O, d, &S, &nc, &rounds);
+            size_t pos = 0;
+            bool table_built = false;
+            int32_t lane_off = 0;
+            while (pos < ids.size()) {
+                const size_t rem = ids.size() - pos;
+                const int G = rem > 4 ? 2 : 1;
+                const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
+                if (!table_built) {
+                    lane_off = (int32_t)P.lanes.size();
+                    build_lane_table(O, d, S, nc, rounds, P.lanes);
+                    table_built = true;
+                }
+                ItemDesc it;
+                std::memset(&it, 0, sizeof(it));
+                it.variant = eidx * 2 + (G - 1);
+                it.d = d;
+                it.p = p;
+                it.O = (int32_t)O;
+                it.S = S;
+                it.rounds = rounds;
+                it.lane_off = lane_off;
+                it.w_off = (int32_t)P.wpk.size();
+                it.k_off = (int32_t)P.kid.size();
+                it.cost = rounds * S * ell * G;
+                // A-operand weights: [g][j][slot i]; zeros for empty slots and
+                // for taps past the kernel's own length
+                for (int g = 0; g < G; ++g)
+                    for (int j = 0; j < ell; ++j)
+                        for (int i = 0; i < 4; ++i) {
+                            const size_t s = (size_t)(4 * g + i);
+                            float w = 0.0f;
+                            if (s < take && j < len)
+                                w = k->weights[(int64_t)ids[pos + s] * k->max_len + j];
+                            P.wpk.push_back(w);
+                        }
+                for (int s = 0; s < 4 * G; ++s) {
+                    if ((size_t)s < take) {
+                        P.kid.push_back(ids[pos + s]);
+                        P.bias.push_back(k->bias[ids[pos + s]]);
+                    } else {
+                        P.kid.push_back(-1);
+                        P.bias.push_back(0.0f);
+                    }
+                }
+                P.items.push_back(it);
+                P.mfma_per_row += it.cost;
+                pos += take;
+            }
+        }
+
+        // item orders: largest cost first (longest-processing-time first),
+        // dealt to splits greedily by accumulated cost
+        std::vector<int32_t> by_cost(P.items.size());
+        for (size_t i = 0; i < by_cost.size(); ++i) by_cost[i] = (int32_t)i;
+        std::stable_sort(by_cost.begin(), by_cost.end(), [&](int32_t a, int32_t b) {
+            return P.items[a].cost > P.items[b].cost;
+        });
+        for (int li = 0; li < kNumSplitLayouts; ++li) {
+            const int ns = kSplitCounts[li];
+            std::vector<std::vector<int32_t>> lists(ns);
+            std::vector<int64_t> load(ns, 0);
+            for (int32_t it : by_cost) {
+                int best = 0;
+                for (int s = 1; s < ns; ++s)
+                    if (load[s] < load[best]) best = s;
+                lists[best].push_back(it);
+                load[best] += P.items[it].cost;
+            }
+            P.layout_off.push_back((int32_t)P.split_begin.size());
+            for (int s = 0; s < ns; ++s) {
+                P.split_begin.push_back((int32_t)P.order.size());
+                P.order.insert(P.order.end(), lists[s].begin(), lists[s].end());
+            }
+            P.split_begin.push_back((int32_t)P.order.size());
+        }
+        *out = std::move(P);
+        return ROCKET_OK;
+    } catch (const std::bad_alloc &) {
+        return ROCKET_ERR_OOM;
+    } catch (...) {
+        return ROCKET_ERR_INTERNAL;
+    }
+}
+
+}  // namespace rocket
+
+extern "C" rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32_t L,
+                                                  rocket_plan_tables *out) {
+    if (!out) return ROCKET_ERR_INVALID_ARG;
+    std::memset(out, 0, sizeof(*out));
+    rocket_status st = rocket::validate_kernels(k, L);
+    if (st != ROCKET_OK) return st;
+    rocket::HostPlan *P = new (std::nothrow) rocket::HostPlan();
+    if (!P) return ROCKET_ERR_OOM;
+    st = rocket::build_host_plan(k, L, P);
+    if (st != ROCKET_OK) {
+        delete P;
+        return st;
+    }
+    out->n_items = (int64_t)P->items.size();
+    out->items = reinterpret_cast<const int32_t *>(P->items.data());
+    out->n_lanes = (int64_t)P->lanes.size();
+    out->lanes = P->lanes.data();
+    out->n_wpk = (int64_t)P->wpk.size();
+    out->wpk = P->wpk.data();
+    out->n_slots = (int64_t)P->kid.size();
+    out->slot_bias = P->bias.data();
+    out->slot_kernel = P->kid.data();
+    out->n_order = (int64_t)P->order.size();
+    out->order = P->order.data();
+    out->n_split_begin = (int64_t)P->split_begin.size();
+    out->split_begin = P->split_begin.data();
+    out->n_layouts = rocket::kNumSplitLayouts;
+    out->layout_off = P->layout_off.data();
+    out->split_counts = rocket::kSplitCounts;
+    out->halo_lo = P->halo_lo;
+    out->halo_hi = P->halo_hi;
+    out->row_stride = P->row_stride;
+    out->internal = P;
+    return ROCKET_OK;
+}
+
+extern "C" void rocket_plan_tables_free(rocket_plan_tables *t) {
+    if (!t) return;
+    delete static_cast<rocket::HostPlan *>(t->internal);
+    std::memset(t, 0, sizeof(*t));
+}

@@ -1,0 +1,89 @@
+// Internal layout shared by the host planner (plan.cpp) and the gfx950
+// kernels (transform.hip).  Not part of the public ABI.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "../../include/rocket.h"
+
+namespace rocket {
+
+// The fused MFMA path keeps the three kernel lengths ROCKET draws
+// (Sec. 2.1: 7, 9, 11).  A hand-built kernel of another length is run as the
+// next supported length with zero weights on the extra taps.
+constexpr int kNumEll = 3;
+constexpr int kEllValues[kNumEll] = {7, 9, 11};
+
+inline int ell_index_for(int length) { return length <= 7 ? 0 : (length <= 9 ? 1 : 2); }
+
+// Wavefront size on CDNA4 and the number of kernel slots one
+// v_mfma_f32_4x4x1_16b_f32 block holds (its 4 A-matrix rows).
+constexpr int kWave = 64;
+constexpr int kSlotsPerGroup = 4;
+constexpr int kMaxGroups = 2;  // a work item holds 4 or 8 kernels of one bucket
+
+// One work item: up to 4*G kernels that share (length, dilation, padding).
+// The 64 lanes of a wavefront each own a chunk of consecutive outputs along
+// one dilation residue class (positions q, q+d, q+2d, ...).  A "round" is one
+// pass of 64 such chunks; every chunk has S steps except that step S-1 may be
+// past the end of its chunk (flagged per lane).
+struct alignas(16) ItemDesc {
+    int32_t variant;   // ell_index * 2 + (G - 1)
+    int32_t d;         // dilation
+    int32_t p;         // padding
+    int32_t O;         // number of dot products (outputs)
+    int32_t S;         // steps per chunk
+    int32_t rounds;    // rounds per series
+    int32_t lane_off;  // first lane-table entry (rounds * 64 entries)
+    int32_t w_off;     // first packed weight: [G][ell][4] floats
+    int32_t k_off;     // first slot entry: kernel ids and biases, [4G]
+    int32_t cost;      // MFMA instructions per series (scheduling weight)
+    int32_t reserved[6];
+};
+static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
+
+// Lane-table entry: bits 0..23 hold q0, the output position of the lane's
+// step 0; bit 30 says step S-1 is a valid output of this lane; bit 31 says
+// the lane's outputs are counted (a lane without it duplicates another
+// lane's chunk exactly, so its values are safe for MAX but must not be
+// counted twice).
+constexpr uint32_t kLaneQMask = 0x00FFFFFFu;
+constexpr uint32_t kLaneLastValid = 1u << 30;
+constexpr uint32_t kLaneCounted = 1u << 31;
+constexpr int64_t kMaxOutputs = (int64_t)kLaneQMask;  // O must fit in 24 bits
+
+// Item orders for a few split counts: split s of a layout with `nsplit`
+// splits is order[split_begin[s] .. split_begin[s+1]).
+constexpr int kNumSplitLayouts = 6;  // 1, 2, 4, 8, 16, 32 splits
+constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
+
+struct HostPlan {
+    int32_t n_kernels = 0;
+    int32_t L = 0;
+    int32_t halo_lo = 0;   // zeros staged before the series in LDS
+    int32_t halo_hi = 0;   // zeros staged after the series in LDS
+    int32_t row_stride = 0;  // floats per staged row
+    int64_t n_buckets = 0;
+    int64_t mfma_per_row = 0;
+    std::vector<ItemDesc> items;
+    std::vector<uint32_t> lanes;
+    std::vector<float> wpk;       // packed A-operand weights
+    std::vector<float> bias;      // per slot
+    std::vector<int32_t> kid;     // per slot, -1 = empty
+    std::vector<int32_t> order;   // kNumSplitLayouts concatenated item orders
+    std::vector<int32_t> split_begin;  // per layout: nsplit + 1 offsets into order
+    std::vector<int32_t> layout_off;   // per layout: offset into split_begin
+};
+
+// Validate a kernel set for series length L (host only, no device calls).
+rocket_status validate_kernels(const rocket_kernels *k, int32_t L);
+
+// Build the host-side tables of a plan.  Assumes validate_kernels passed.
+rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out);
+
+// Choose the chunking of one bucket: number of chunks per residue nc, steps
+// S and rounds, minimising rounds * S (the MFMA steps one series costs).
+void choose_chunking(int64_t O, int64_t d, int32_t *S, int32_t *nc, int32_t *rounds);
+
+}  // namespace rocket

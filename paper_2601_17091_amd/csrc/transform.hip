@@ -1,0 +1,517 @@
+// ROCKET transform on CDNA4 (gfx950): fused MFMA kernel, plain direct
+// kernel, and the HIP-facing half of the C ABI.
+//
+// Fused kernel (one workgroup = one series x one split of the work items):
+//   1. the series is staged HBM -> LDS with coalesced loads, with zero
+//      margins on both sides that stand in for the zero padding (Sec. 2.1);
+//   2. each wavefront takes work items from an LDS counter; an item holds 4
+//      or 8 kernels of one (length, dilation, padding) bucket;
+//   3. the dot products of a bucket are an outer-product contraction over the
+//      taps: v_mfma_f32_4x4x1_16b_f32 multiplies the 4 kernels' weights (A,
+//      one kernel per block row) by 64 series values (B, one output position
+//      per lane), one tap per instruction, accumulating onto the bias;
+//   4. every lane walks a chunk of outputs along one dilation residue class,
+//      so successive outputs share all but one series value: a register
+//      window slides along the decimated series and each step loads one new
+//      value from LDS;
+//   5. MAX is a per-lane running max reduced across the wavefront at the end;
+//      the positive count is a ballot of y > 0 popcounted on the scalar unit;
+//      no dot product is written to memory (Sec. 3.2 keeps only the two
+//      counters per pair as well);
+//   6. PPV = count / O and MAX are written to F in the original kernel order.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "rocket_internal.h"
+
+using rocket::ItemDesc;
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+namespace {
+
+constexpr int kBlock = 256;       // 4 wavefronts per workgroup
+constexpr int kBigBlock = 1024;   // 16 wavefronts share one large staged row
+constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
+
+struct FusedArgs {
+    const float *X;
+    float *F;
+    int64_t row0;      // first row of this launch (rows are independent)
+    int64_t n_rows;    // rows in this launch
+    int32_t L;
+    int32_t K;
+    const ItemDesc *items;
+    const uint32_t *lanes;
+    const float *wpk;
+    const float *bias;
+    const int32_t *kid;
+    const int32_t *order;
+    const int32_t *split_begin;  // nsplit + 1 offsets into order
+    int32_t nsplit;
+    int32_t halo_lo;
+    int32_t row_stride;
+};
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// One output step of a work item: load the next series value into the
+// register window, run the G x ELL MFMA taps, and fold the 4G results into
+// the running MAX and positive counts.  U is the step's position in the
+// window ring, so every register index is a compile-time constant.
+//
+// Lanes that only duplicate another lane's chunk start from a -inf
+// accumulator (binit), so their results are never positive and never raise
+// MAX; no mask is needed for them.  The last step of a round (LAST) can lie
+// past the end of a lane's chunk; there the count uses the mask m_last and
+// MAX skips the lane.
+template <int ELL, int G, int U, bool LAST>
+__device__ __forceinline__ void item_step(int d, const float *&xn, float (&xw)[ELL],
+                                          const float (&wa)[G][ELL], const v4f (&binit)[G],
+                                          v4f (&mx)[G], uint32_t (&cnt)[G][4], uint64_t m_last,
+                                          bool last_ok) {
+    xw[(U + ELL - 1) % ELL] = *xn;
+    xn += d;
+    v4f acc[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) acc[g] = binit[g];
+#pragma unroll
+    for (int j = 0; j < ELL; ++j)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            acc[g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[(U + j) % ELL], acc[g], 0, 0, 0);
+    if (!LAST) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[g][v] > 0.0f));
+                mx[g][v] = fmaxf(mx[g][v], acc[g][v]);
+            }
+    } else {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                cnt[g][v] +=
+                    (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[g][v] > 0.0f) & m_last);
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) mx[g][v] = last_ok ? fmaxf(mx[g][v], acc[g][v]) : mx[g][v];
+    }
+}
+
+// Steps with ring positions U .. UEND-1 of one block, each run if U >= ustart.
+template <int ELL, int G, int U, int UEND>
+struct StepRange {
+    __device__ __forceinline__ static void run(int ustart, int d, const float *&xn, float (&xw)[ELL],
+                                               const float (&wa)[G][ELL], const v4f (&binit)[G],
+                                               v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+        if (U >= ustart) item_step<ELL, G, U, false>(d, xn, xw, wa, binit, mx, cnt, 0, true);
+        StepRange<ELL, G, U + 1, UEND>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+    }
+};
+
+template <int ELL, int G, int UEND>
+struct StepRange<ELL, G, UEND, UEND> {
+    __device__ __forceinline__ static void run(int, int, const float *&, float (&)[ELL],
+                                               const float (&)[G][ELL], const v4f (&)[G],
+                                               v4f (&)[G], uint32_t (&)[G][4]) {}
+};
+
+template <int ELL, int G>
+__device__ __forceinline__ void run_item(const ItemDesc &it, const float *xrow, const FusedArgs &a,
+                                         float *Frow, int lane) {
+    const int d = it.d;
+    const int S = it.S;
+    // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
+    float wa[G][ELL];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
+    // biases of block rows v (kernel slots v)
+    float bias[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) bias[g][v] = a.bias[it.k_off + 4 * g + v];
+    v4f mx[G];
+    uint32_t cnt[G][4];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
+    }
+    // Step s of a round sits at ring position (s + U0) mod ELL, with U0
+    // chosen so that the last step S-1 sits at position ELL-1.
+    const int U0 = (ELL - S % ELL) % ELL;
+    const int nblocks = (S + U0) / ELL;
+    // xb[q + m*d] is the zero-padded series value under tap m of output q
+    const float *xb = xrow - it.p;
+    for (int rd = 0; rd < it.rounds; ++rd) {
+        const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
+        const int q0 = (int)(e & rocket::kLaneQMask);
+        const bool counted = (e & rocket::kLaneCounted) != 0;
+        const bool last_ok = counted && (e & rocket::kLaneLastValid) != 0;
+        const uint64_t m_last = __builtin_amdgcn_ballot_w64(last_ok);
+        // C operand of the first tap: the slot's bias, or -inf on lanes that
+        // duplicate another lane's chunk
+        v4f binit[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) binit[g][v] = counted ? bias[g][v] : -INFINITY;
+        // window element m (series value under output q0 + m*d) goes to ring
+        // slot (m + U0) mod ELL; element ELL-1 is loaded by the first step
+        const float *xq = xb + q0;
+        float xw[ELL];
+#pragma unroll
+        for (int i = 0; i < ELL; ++i) {
+            const int m = (i - U0 + ELL) % ELL;
+            xw[i] = (m < ELL - 1) ? xq[m * d] : 0.0f;
+        }
+        const float *xn = xq + (ELL - 1) * d;
+        int ustart = U0;
+        for (int blk = 0; blk + 1 < nblocks; ++blk) {
+            StepRange<ELL, G, 0, ELL>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+            ustart = 0;
+        }
+        StepRange<ELL, G, 0, ELL - 1>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+        item_step<ELL, G, ELL - 1, true>(d, xn, xw, wa, binit, mx, cnt, m_last, last_ok);
+    }
+    // reduce MAX across the wavefront; lane s writes kernel slot s
+    float out_max = 0.0f;
+    uint32_t out_cnt = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float m = wave_max(mx[g][v]);
+            if (lane == 4 * g + v) {
+                out_max = m;
+                out_cnt = cnt[g][v];
+            }
+        }
+    if (lane < 4 * G) {
+        const int k = a.kid[it.k_off + lane];
+        if (k >= 0) {
+            float2 r;
+            r.x = (float)out_cnt / (float)it.O;
+            r.y = out_max;
+            *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)k) = r;
+        }
+    }
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
+    extern __shared__ float smem[];
+    __shared__ int next_item;
+    // Consecutive workgroup ids land on different XCDs; renumber so that the
+    // splits of one series (which write the same F row) share an XCD's L2.
+    const int64_t nb = gridDim.x;
+    int64_t b = blockIdx.x;
+    if (nb % 8 == 0) b = (b % 8) * (nb / 8) + b / 8;
+    const int64_t row = b / a.nsplit;
+    const int split = (int)(b % a.nsplit);
+    if (row >= a.n_rows) return;
+    const int64_t grow = a.row0 + row;
+
+    const float *x = a.X + grow * (int64_t)a.L;
+    for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
+        const int m = e - a.halo_lo;
+        smem[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
+    }
+    if (threadIdx.x == 0) next_item = 0;
+    __syncthreads();
+
+    const int lane = threadIdx.x & (rocket::kWave - 1);
+    const int beg = a.split_begin[split];
+    const int cnt_items = a.split_begin[split + 1] - beg;
+    float *Frow = a.F + grow * 2 * (int64_t)a.K;
+    const float *xrow = smem + a.halo_lo;
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(&next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = a.items[a.order[beg + idx]];
+        switch (it.variant) {
+            case 0: run_item<7, 1>(it, xrow, a, Frow, lane); break;
+            case 1: run_item<7, 2>(it, xrow, a, Frow, lane); break;
+            case 2: run_item<9, 1>(it, xrow, a, Frow, lane); break;
+            case 3: run_item<9, 2>(it, xrow, a, Frow, lane); break;
+            case 4: run_item<11, 1>(it, xrow, a, Frow, lane); break;
+            default: run_item<11, 2>(it, xrow, a, Frow, lane); break;
+        }
+    }
+}
+
+// Plain kernel: one wavefront per (series, kernel) pair, lanes over output
+// positions, taps read straight from global memory with the zero padding
+// applied by bounds checks.
+__global__ __launch_bounds__(kBlock) void rocket_direct_kernel(
+    const float *__restrict__ X, int64_t row0, int32_t L, int32_t K, int32_t k0,
+    const int32_t *__restrict__ len, const int32_t *__restrict__ dil,
+    const int32_t *__restrict__ pad, const float *__restrict__ bias,
+    const float *__restrict__ w, int32_t max_len, float *__restrict__ F) {
+    const int64_t row = row0 + blockIdx.x;
+    const int k = k0 + (int)blockIdx.y * (kBlock / 64) + (int)(threadIdx.x >> 6);
+    if (k >= K) return;
+    const int lane = threadIdx.x & 63;
+    const int ell = len[k], d = dil[k], p = pad[k];
+    const float b = bias[k];
+    const float *wk = w + (int64_t)k * max_len;
+    const int64_t O = (int64_t)L + 2 * (int64_t)p - (int64_t)(ell - 1) * d;
+    const float *x = X + row * (int64_t)L;
+    float mx = -INFINITY;
+    uint32_t c = 0;
+    for (int64_t t = lane; t < O; t += 64) {
+        float acc = b;
+        for (int j = 0; j < ell; ++j) {
+            const int64_t m = t - p + (int64_t)j * d;
+            const float xv = (m >= 0 && m < L) ? x[m] : 0.0f;
+            acc = fmaf(wk[j], xv, acc);
+        }
+        c += acc > 0.0f ? 1u : 0u;
+        mx = fmaxf(mx, acc);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        c += __shfl_xor(c, off, 64);
+    }
+    if (lane == 0) {
+        float2 r;
+        r.x = (float)c / (float)O;
+        r.y = mx;
+        *reinterpret_cast<float2 *>(F + row * 2 * (int64_t)K + 2 * (int64_t)k) = r;
+    }
+}
+
+template <typename T>
+hipError_t upload(const std::vector<T> &h, T **d) {
+    *d = nullptr;
+    if (h.empty()) return hipSuccess;
+    hipError_t e = hipMalloc((void **)d, h.size() * sizeof(T));
+    if (e != hipSuccess) return e;
+    return hipMemcpy(*d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice);
+}
+
+template <typename T>
+hipError_t upload_raw(const T *h, size_t n, T **d) {
+    *d = nullptr;
+    hipError_t e = hipMalloc((void **)d, n * sizeof(T));
+    if (e != hipSuccess) return e;
+    return hipMemcpy(*d, h, n * sizeof(T), hipMemcpyHostToDevice);
+}
+
+}  // namespace
+
+struct rocket_plan {
+    rocket::HostPlan host;
+    int device = 0;
+    int n_cu = 0;
+    bool direct = false;
+    int64_t lds_bytes = 0;
+    ItemDesc *d_items = nullptr;
+    uint32_t *d_lanes = nullptr;
+    float *d_wpk = nullptr;
+    float *d_bias = nullptr;
+    int32_t *d_kid = nullptr;
+    int32_t *d_order = nullptr;
+    int32_t *d_split_begin = nullptr;
+    // the kernel set as given, for the direct kernel
+    int32_t max_len = 0;
+    int32_t *d_len = nullptr;
+    int32_t *d_dil = nullptr;
+    int32_t *d_pad = nullptr;
+    float *d_b = nullptr;
+    float *d_w = nullptr;
+};
+
+static void plan_free_device(rocket_plan *p) {
+    void *ptrs[] = {p->d_items, p->d_lanes, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
+                    p->d_split_begin, p->d_len, p->d_dil, p->d_pad, p->d_b, p->d_w};
+    for (void *q : ptrs)
+        if (q) (void)hipFree(q);
+}
+
+static rocket_status map_hip(hipError_t e) {
+    if (e == hipSuccess) return ROCKET_OK;
+    if (e == hipErrorOutOfMemory) return ROCKET_ERR_OOM;
+    return ROCKET_ERR_HIP;
+}
+
+extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t flags,
+                                               rocket_plan **out) {
+    if (!out) return ROCKET_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (flags & ~ROCKET_PLAN_DIRECT) return ROCKET_ERR_INVALID_ARG;
+    rocket_status st = rocket::validate_kernels(k, L);
+    if (st != ROCKET_OK) return st;
+    rocket_plan *p = new (std::nothrow) rocket_plan();
+    if (!p) return ROCKET_ERR_OOM;
+    st = rocket::build_host_plan(k, L, &p->host);
+    if (st != ROCKET_OK) {
+        delete p;
+        return st;
+    }
+    hipError_t e = hipGetDevice(&p->device);
+    hipDeviceProp_t prop;
+    if (e == hipSuccess) e = hipGetDeviceProperties(&prop, p->device);
+    if (e != hipSuccess) {
+        delete p;
+        return ROCKET_ERR_HIP;
+    }
+    p->n_cu = prop.multiProcessorCount;
+    const int64_t lds = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
+    p->direct = (flags & ROCKET_PLAN_DIRECT) || p->host.row_stride == 0 ||
+                lds > (int64_t)prop.sharedMemPerBlock;
+    p->lds_bytes = p->direct ? 0 : lds;
+    const int32_t K = k->n_kernels;
+    p->max_len = k->max_len;
+    if (e == hipSuccess) e = upload_raw(k->length, (size_t)K, &p->d_len);
+    if (e == hipSuccess) e = upload_raw(k->dilation, (size_t)K, &p->d_dil);
+    if (e == hipSuccess) e = upload_raw(k->padding, (size_t)K, &p->d_pad);
+    if (e == hipSuccess) e = upload_raw(k->bias, (size_t)K, &p->d_b);
+    if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * k->max_len, &p->d_w);
+    if (!p->direct) {
+        if (e == hipSuccess) e = upload(p->host.items, &p->d_items);
+        if (e == hipSuccess) e = upload(p->host.lanes, &p->d_lanes);
+        if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
+        if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
+        if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
+        if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
+        if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
+        if (e == hipSuccess && lds > 64 * 1024)
+            e = hipFuncSetAttribute((const void *)rocket_fused_kernel<kBigBlock>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    }
+    if (e != hipSuccess) {
+        plan_free_device(p);
+        delete p;
+        return map_hip(e);
+    }
+    *out = p;
+    return ROCKET_OK;
+}
+
+extern "C" rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan **out) {
+    return rocket_plan_create_ex(k, L, ROCKET_PLAN_DEFAULT, out);
+}
+
+extern "C" void rocket_plan_destroy(rocket_plan *p) {
+    if (!p) return;
+    plan_free_device(p);
+    delete p;
+}
+
+extern "C" rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
+                                          int64_t *mfma_per_row, int64_t *lds_bytes,
+                                          int32_t *direct) {
+    if (!p) return ROCKET_ERR_INVALID_ARG;
+    if (n_items) *n_items = (int64_t)p->host.items.size();
+    if (n_buckets) *n_buckets = p->host.n_buckets;
+    if (mfma_per_row) *mfma_per_row = p->host.mfma_per_row;
+    if (lds_bytes) *lds_bytes = p->lds_bytes;
+    if (direct) *direct = p->direct ? 1 : 0;
+    return ROCKET_OK;
+}
+
+static rocket_status launch_direct(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                   hipStream_t s) {
+    const int32_t K = p->host.n_kernels;
+    const int per_block = kBlock / 64;
+    const int64_t max_y = 65535;
+    const int64_t max_x = INT_MAX;
+    for (int64_t r0 = 0; r0 < n; r0 += max_x) {
+        const int64_t nr = std::min<int64_t>(max_x, n - r0);
+        for (int64_t k0 = 0; k0 < K; k0 += max_y * per_block) {
+            const int64_t nk = std::min<int64_t>(max_y * per_block, K - k0);
+            dim3 grid((unsigned)nr, (unsigned)((nk + per_block - 1) / per_block));
+            hipLaunchKernelGGL(rocket_direct_kernel, grid, dim3(kBlock), 0, s, X, r0, p->host.L, K,
+                               (int32_t)k0, p->d_len, p->d_dil, p->d_pad, p->d_b, p->d_w,
+                               p->max_len, F);
+            if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+        }
+    }
+    return ROCKET_OK;
+}
+
+static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                  hipStream_t s) {
+    // enough workgroups to fill the chip several times over: split the work
+    // items of a series across workgroups when there are few series
+    const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
+    int li = 0;
+    while (li + 1 < rocket::kNumSplitLayouts && n * rocket::kSplitCounts[li] < target) ++li;
+    const int nsplit = rocket::kSplitCounts[li];
+    FusedArgs a;
+    a.X = X;
+    a.F = F;
+    a.L = p->host.L;
+    a.K = p->host.n_kernels;
+    a.items = p->d_items;
+    a.lanes = p->d_lanes;
+    a.wpk = p->d_wpk;
+    a.bias = p->d_bias;
+    a.kid = p->d_kid;
+    a.order = p->d_order;
+    a.split_begin = p->d_split_begin + p->host.layout_off[li];
+    a.nsplit = nsplit;
+    a.halo_lo = p->host.halo_lo;
+    a.row_stride = p->host.row_stride;
+    const int64_t max_rows = (int64_t)INT_MAX / nsplit;
+    for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
+        a.row0 = r0;
+        a.n_rows = std::min<int64_t>(max_rows, n - r0);
+        const unsigned nb = (unsigned)(a.n_rows * nsplit);
+        if (p->lds_bytes > kBigLds)
+            hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock),
+                               (size_t)p->lds_bytes, s, a);
+        else
+            hipLaunchKernelGGL(rocket_fused_kernel<kBlock>, dim3(nb), dim3(kBlock),
+                               (size_t)p->lds_bytes, s, a);
+        if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+    }
+    return ROCKET_OK;
+}
+
+extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
+                                               float *F_dev, void *hip_stream) {
+    if (!p || n < 0) return ROCKET_ERR_INVALID_ARG;
+    if (n == 0) return ROCKET_OK;
+    if (!X_dev || !F_dev) return ROCKET_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)hip_stream;
+    return p->direct ? launch_direct(p, X_dev, n, F_dev, s) : launch_fused(p, X_dev, n, F_dev, s);
+}
+
+extern "C" rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L,
+                                          const rocket_kernels *k, float *F_dev, void *hip_stream) {
+    if (n < 0) return ROCKET_ERR_INVALID_ARG;
+    if (n > 0 && (!X_dev || !F_dev)) return ROCKET_ERR_INVALID_ARG;
+    rocket_status st = rocket::validate_kernels(k, L);
+    if (st != ROCKET_OK) return st;
+    if (n == 0) return ROCKET_OK;
+    rocket_plan *p = nullptr;
+    st = rocket_plan_create(k, L, &p);
+    if (st != ROCKET_OK) return st;
+    st = rocket_transform_plan(p, X_dev, n, F_dev, hip_stream);
+    const hipError_t e = hipStreamSynchronize((hipStream_t)hip_stream);
+    rocket_plan_destroy(p);
+    if (st != ROCKET_OK) return st;
+    return e == hipSuccess ? ROCKET_OK : ROCKET_ERR_HIP;
+}

@@ -1,0 +1,290 @@
+"""ctypes binding of librocket.so (the C ABI declared in include/rocket.h).
+
+Argument marshalling only: kernel arrays are passed as host pointers, X and F
+as device pointers of torch tensors, the stream as torch's current HIP
+stream.  Every step of the transform runs in the HIP library; if the library
+is missing, calls raise instead of computing anything elsewhere.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librocket.so")
+
+ROCKET_OK = 0
+ROCKET_ERR_INVALID_ARG = -1
+ROCKET_ERR_LENGTH = -2
+ROCKET_ERR_OOM = -3
+ROCKET_ERR_HIP = -4
+ROCKET_ERR_INTERNAL = -5
+ROCKET_PLAN_DEFAULT = 0
+ROCKET_PLAN_DIRECT = 1
+MAX_KERNEL_LENGTH = 11
+
+# every symbol include/rocket.h declares
+EXPORTED = (
+    "rocket_generate_kernels",
+    "rocket_free_kernels",
+    "rocket_plan_create",
+    "rocket_plan_create_ex",
+    "rocket_plan_destroy",
+    "rocket_transform_plan",
+    "rocket_transform",
+    "rocket_plan_info",
+    "rocket_plan_tables_build",
+    "rocket_plan_tables_free",
+    "rocket_status_string",
+)
+
+
+class RocketError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s failed: %s (%d)" % (what, status_string(status), status))
+
+
+class CKernels(ctypes.Structure):
+    _fields_ = [
+        ("n_kernels", ctypes.c_int32),
+        ("input_length", ctypes.c_int32),
+        ("max_len", ctypes.c_int32),
+        ("length", ctypes.POINTER(ctypes.c_int32)),
+        ("dilation", ctypes.POINTER(ctypes.c_int32)),
+        ("padding", ctypes.POINTER(ctypes.c_int32)),
+        ("bias", ctypes.POINTER(ctypes.c_float)),
+        ("weights", ctypes.POINTER(ctypes.c_float)),
+    ]
+
+
+class CPlanTables(ctypes.Structure):
+    _fields_ = [
+        ("n_items", ctypes.c_int64), ("items", ctypes.POINTER(ctypes.c_int32)),
+        ("n_lanes", ctypes.c_int64), ("lanes", ctypes.POINTER(ctypes.c_uint32)),
+        ("n_wpk", ctypes.c_int64), ("wpk", ctypes.POINTER(ctypes.c_float)),
+        ("n_slots", ctypes.c_int64), ("slot_bias", ctypes.POINTER(ctypes.c_float)),
+        ("slot_kernel", ctypes.POINTER(ctypes.c_int32)),
+        ("n_order", ctypes.c_int64), ("order", ctypes.POINTER(ctypes.c_int32)),
+        ("n_split_begin", ctypes.c_int64), ("split_begin", ctypes.POINTER(ctypes.c_int32)),
+        ("n_layouts", ctypes.c_int32), ("layout_off", ctypes.POINTER(ctypes.c_int32)),
+        ("split_counts", ctypes.POINTER(ctypes.c_int32)),
+        ("halo_lo", ctypes.c_int32), ("halo_hi", ctypes.c_int32), ("row_stride", ctypes.c_int32),
+        ("internal", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """Load librocket.so (built by ``build_lib.build``); raise if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("librocket.so is not built (run paper_2601_17091_amd.build_lib.build())")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    kp = ctypes.POINTER(CKernels)
+    lib.rocket_generate_kernels.argtypes = [ctypes.c_uint64, i32, i32, kp]
+    lib.rocket_generate_kernels.restype = ctypes.c_int
+    lib.rocket_free_kernels.argtypes = [kp]
+    lib.rocket_free_kernels.restype = None
+    lib.rocket_plan_create.argtypes = [kp, i32, ctypes.POINTER(vp)]
+    lib.rocket_plan_create.restype = ctypes.c_int
+    lib.rocket_plan_create_ex.argtypes = [kp, i32, ctypes.c_uint32, ctypes.POINTER(vp)]
+    lib.rocket_plan_create_ex.restype = ctypes.c_int
+    lib.rocket_plan_destroy.argtypes = [vp]
+    lib.rocket_plan_destroy.restype = None
+    lib.rocket_transform_plan.argtypes = [vp, vp, i64, vp, vp]
+    lib.rocket_transform_plan.restype = ctypes.c_int
+    lib.rocket_transform.argtypes = [vp, i64, i32, kp, vp, vp]
+    lib.rocket_transform.restype = ctypes.c_int
+    lib.rocket_plan_info.argtypes = [vp] + [ctypes.POINTER(i64)] * 4 + [ctypes.POINTER(i32)]
+    lib.rocket_plan_info.restype = ctypes.c_int
+    lib.rocket_plan_tables_build.argtypes = [kp, i32, ctypes.POINTER(CPlanTables)]
+    lib.rocket_plan_tables_build.restype = ctypes.c_int
+    lib.rocket_plan_tables_free.argtypes = [ctypes.POINTER(CPlanTables)]
+    lib.rocket_plan_tables_free.restype = None
+    lib.rocket_status_string.argtypes = [ctypes.c_int]
+    lib.rocket_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return library().rocket_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != ROCKET_OK:
+        raise RocketError(status, what)
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def as_c_kernels(kernels: dict):
+    """A CKernels view of numpy kernel arrays (kept alive by the returned tuple)."""
+    length = np.ascontiguousarray(kernels["length"], dtype=np.int32)
+    dilation = np.ascontiguousarray(kernels["dilation"], dtype=np.int32)
+    padding = np.ascontiguousarray(kernels["padding"], dtype=np.int32)
+    bias = np.ascontiguousarray(kernels["bias"], dtype=np.float32)
+    weights = np.ascontiguousarray(kernels["weights"], dtype=np.float32)
+    if weights.ndim != 2 or weights.shape[0] != length.shape[0]:
+        raise ValueError("weights must be [n_kernels, max_len]")
+    c = CKernels(int(length.shape[0]), int(kernels.get("input_length", 0)), int(weights.shape[1]),
+                 _ptr(length, ctypes.c_int32), _ptr(dilation, ctypes.c_int32),
+                 _ptr(padding, ctypes.c_int32), _ptr(bias, ctypes.c_float),
+                 _ptr(weights, ctypes.c_float))
+    return c, (length, dilation, padding, bias, weights)
+
+
+def generate_kernels(seed: int, n_kernels: int, input_length: int) -> dict:
+    """rocket_generate_kernels, copied into numpy arrays (library copy freed)."""
+    lib = library()
+    ck = CKernels()
+    _check(lib.rocket_generate_kernels(ctypes.c_uint64(seed & (2 ** 64 - 1)), n_kernels, input_length,
+                                       ctypes.byref(ck)), "rocket_generate_kernels")
+    try:
+        K, M = ck.n_kernels, ck.max_len
+        out = dict(
+            length=np.ctypeslib.as_array(ck.length, (K,)).copy(),
+            dilation=np.ctypeslib.as_array(ck.dilation, (K,)).copy(),
+            padding=np.ctypeslib.as_array(ck.padding, (K,)).copy(),
+            bias=np.ctypeslib.as_array(ck.bias, (K,)).copy(),
+            weights=np.ctypeslib.as_array(ck.weights, (K * M,)).copy().reshape(K, M),
+            input_length=ck.input_length,
+        )
+    finally:
+        lib.rocket_free_kernels(ctypes.byref(ck))
+    return out
+
+
+def plan_tables(kernels: dict, L: int) -> dict:
+    """rocket_plan_tables_build copied into numpy arrays (host only)."""
+    lib = library()
+    c, keep = as_c_kernels(kernels)
+    t = CPlanTables()
+    _check(lib.rocket_plan_tables_build(ctypes.byref(c), int(L), ctypes.byref(t)),
+           "rocket_plan_tables_build")
+    try:
+        def arr(ptr, n, shape=None):
+            a = np.ctypeslib.as_array(ptr, (int(n),)).copy() if n > 0 else np.zeros(0)
+            return a.reshape(shape) if shape is not None else a
+        out = dict(
+            items=arr(t.items, t.n_items * 16, (int(t.n_items), 16)),
+            lanes=arr(t.lanes, t.n_lanes),
+            wpk=arr(t.wpk, t.n_wpk),
+            slot_bias=arr(t.slot_bias, t.n_slots),
+            slot_kernel=arr(t.slot_kernel, t.n_slots),
+            order=arr(t.order, t.n_order),
+            split_begin=arr(t.split_begin, t.n_split_begin),
+            layout_off=arr(t.layout_off, t.n_layouts),
+            split_counts=arr(t.split_counts, t.n_layouts),
+            halo_lo=t.halo_lo, halo_hi=t.halo_hi, row_stride=t.row_stride,
+        )
+    finally:
+        lib.rocket_plan_tables_free(ctypes.byref(t))
+    del keep
+    return out
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check_series(X, L: int):
+    import torch
+    if not isinstance(X, torch.Tensor) or not X.is_cuda:
+        raise TypeError("X must be a torch tensor on the GPU")
+    if X.dtype != torch.float32 or X.dim() != 2 or X.shape[1] != L or not X.is_contiguous():
+        raise ValueError("X must be contiguous float32 [n, %d]" % L)
+
+
+class Plan:
+    """rocket_plan: a kernel set planned for series of length L on the current device."""
+
+    def __init__(self, kernels: dict, L: int, direct: bool = False):
+        lib = library()
+        self._c, self._keep = as_c_kernels(kernels)
+        self.n_kernels = int(self._c.n_kernels)
+        self.L = int(L)
+        h = ctypes.c_void_p()
+        flags = ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT
+        _check(lib.rocket_plan_create_ex(ctypes.byref(self._c), self.L, flags, ctypes.byref(h)),
+               "rocket_plan_create")
+        self._h = h
+
+    def info(self) -> dict:
+        vals = [ctypes.c_int64() for _ in range(4)]
+        direct = ctypes.c_int32()
+        _check(library().rocket_plan_info(self._h, *[ctypes.byref(v) for v in vals], ctypes.byref(direct)),
+               "rocket_plan_info")
+        return dict(n_items=vals[0].value, n_buckets=vals[1].value, mfma_per_row=vals[2].value,
+                    lds_bytes=vals[3].value, direct=bool(direct.value))
+
+    def transform_into(self, X, F, stream=None):
+        """F[n, 2K] <- features of X[n, L]; asynchronous on `stream`."""
+        import torch
+        _check_series(X, self.L)
+        n = X.shape[0]
+        if (not isinstance(F, torch.Tensor) or not F.is_cuda or F.dtype != torch.float32
+                or tuple(F.shape) != (n, 2 * self.n_kernels) or not F.is_contiguous()):
+            raise ValueError("F must be contiguous float32 [n, 2*n_kernels] on the GPU")
+        if X.device != F.device:
+            raise ValueError("X and F must be on the same device")
+        _check(library().rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), n,
+                                               ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
+               "rocket_transform_plan")
+        return F
+
+    def transform(self, X, stream=None):
+        import torch
+        F = torch.empty((X.shape[0], 2 * self.n_kernels), dtype=torch.float32, device=X.device)
+        return self.transform_into(X, F, stream)
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            library().rocket_plan_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def transform(X, kernels: dict, stream=None):
+    """One-shot rocket_transform: returns F[n, 2K] (blocks until done)."""
+    import torch
+    c, keep = as_c_kernels(kernels)
+    L = int(X.shape[1])
+    _check_series(X, L)
+    F = torch.empty((X.shape[0], 2 * c.n_kernels), dtype=torch.float32, device=X.device)
+    _check(library().rocket_transform(ctypes.c_void_p(X.data_ptr()), X.shape[0], L, ctypes.byref(c),
+                                      ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
+           "rocket_transform")
+    del keep
+    return F
+
+
+def transform_batched(plan: Plan, X, F_batch, batch_rows: int, stream=None, on_batch=None):
+    """Stream X through a reused F buffer of ``batch_rows`` rows (row batching
+    for feature matrices larger than the caller wants resident).  ``on_batch``
+    (optional) is called with (row0, F_view) after each batch is enqueued."""
+    n = X.shape[0]
+    for r0 in range(0, n, batch_rows):
+        nb = min(batch_rows, n - r0)
+        Fv = F_batch[:nb]
+        plan.transform_into(X[r0:r0 + nb], Fv, stream)
+        if on_batch is not None:
+            on_batch(r0, Fv)

@@ -129,3 +129,45 @@ def z_norm(x):
 
 __all__ = ["load_golden", "kernel_set", "brute_force", "random_kernels", "fp32_features",
            "ceil_div", "z_norm", "math"]
+
+
+# ---------------------------------------------------------------------------
+# parity rule shared by the GPU tests
+# ---------------------------------------------------------------------------
+MAX_ABS_TOL = 1e-4   # MAX within 1e-4 absolute on z-normalised input
+COUNT_TOL = 2        # PPV within 2/O, i.e. the positive count within 2
+
+
+def parity_report(F_gpu, ref):
+    """Compare GPU features (fp32 [m, 2K]) with an oracle result on the same
+    rows.  Returns a dict of the worst deviations and violation counts."""
+    F_gpu = np.asarray(F_gpu, dtype=np.float64)
+    O = ref["O"][None, :].astype(np.float64)
+    ppv = F_gpu[:, 0::2]
+    cnt = np.rint(ppv * O).astype(np.int64)
+    mx = F_gpu[:, 1::2]
+    dmax = np.abs(mx - ref["F"][:, 1::2])
+    dcnt = np.abs(cnt - ref["cnt"])
+    return dict(
+        max_abs_err=float(dmax.max()) if dmax.size else 0.0,
+        max_count_err=int(dcnt.max()) if dcnt.size else 0,
+        ppv_not_integral=int((np.abs(ppv * O - cnt) > 1e-3).sum()),
+        outside_count_interval=int(((cnt < ref["cnt_lo"]) | (cnt > ref["cnt_hi"])).sum()),
+        max_beyond_bound=int((dmax > ref["beta"]).sum()),
+        nonfinite=int((~np.isfinite(F_gpu)).sum()),
+        ppv_out_of_range=int(((ppv < 0) | (ppv > 1)).sum()),
+        n_features=int(cnt.size),
+    )
+
+
+def assert_parity(F_gpu, ref, what=""):
+    r = parity_report(F_gpu, ref)
+    assert r["nonfinite"] == 0, (what, r)
+    assert r["ppv_out_of_range"] == 0, (what, r)
+    assert r["ppv_not_integral"] == 0, (what, r)
+    assert r["max_abs_err"] <= MAX_ABS_TOL, (what, r)
+    assert r["max_count_err"] <= COUNT_TOL, (what, r)
+    # stricter: inside the certified fp32 envelope of the exact result
+    assert r["outside_count_interval"] == 0, (what, r)
+    assert r["max_beyond_bound"] == 0, (what, r)
+    return r

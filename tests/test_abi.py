@@ -1,0 +1,148 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol,
+generates the same kernels as the oracle's independent generator, and
+rejects invalid arguments before touching a device."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2601_17091_amd as rk
+from paper_2601_17091_amd import rocket as rb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rocket.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rb.LIB_PATH):
+        from paper_2601_17091_amd import build_lib
+        build_lib.build()
+    return rb.library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rocket_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_exported_set(lib):
+    assert declared_functions() == sorted(rb.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", rb.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert rk.status_string(code) not in ("", "unknown status")
+    assert rk.status_string(7) == "unknown status"
+
+
+@pytest.mark.parametrize("seed,K,L", [(0, 500, 11), (1, 2000, 64), (203, 3000, 1000),
+                                      (2 ** 64 - 1, 1000, 16384), (42, 700, 500)])
+def test_generator_matches_oracle_bitwise(lib, oracle, seed, K, L):
+    a = rk.generate_kernels(seed, K, L)
+    b = oracle.generate_kernels(seed, K, L)
+    for key in ("length", "dilation", "padding", "bias", "weights"):
+        assert a[key].dtype == b[key].dtype, key
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+    assert a["input_length"] == L
+
+
+def test_generator_errors_and_free(lib):
+    ck = rb.CKernels()
+    assert lib.rocket_generate_kernels(1, 0, 100, ctypes.byref(ck)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_generate_kernels(1, 10, 10, ctypes.byref(ck)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_generate_kernels(1, 10, 100, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_generate_kernels(1, 10, 100, ctypes.byref(ck)) == rb.ROCKET_OK
+    assert ck.n_kernels == 10 and ck.max_len == 11
+    lib.rocket_free_kernels(ctypes.byref(ck))
+    assert ck.n_kernels == 0 and not ck.length
+    lib.rocket_free_kernels(ctypes.byref(ck))  # idempotent
+    lib.rocket_free_kernels(None)  # NULL-safe
+
+
+def _kernels(**over):
+    k = dict(length=np.array([7, 9]), dilation=np.array([1, 2]), padding=np.array([0, 8]),
+             bias=np.array([0.1, -0.2], np.float32), weights=np.ones((2, 11), np.float32))
+    k.update(over)
+    return k
+
+
+def _plan_status(lib, k, L, flags=0):
+    c, keep = rb.as_c_kernels(k)
+    h = ctypes.c_void_p()
+    st = lib.rocket_plan_create_ex(ctypes.byref(c), L, flags, ctypes.byref(h))
+    assert not h.value  # every case below fails before a plan exists
+    return st
+
+
+@pytest.mark.parametrize("over,L,expect", [
+    (dict(), 0, rb.ROCKET_ERR_INVALID_ARG),
+    (dict(length=np.array([0, 9])), 100, rb.ROCKET_ERR_INVALID_ARG),
+    (dict(length=np.array([12, 9])), 100, rb.ROCKET_ERR_INVALID_ARG),
+    (dict(dilation=np.array([0, 2])), 100, rb.ROCKET_ERR_INVALID_ARG),
+    (dict(padding=np.array([-1, 8])), 100, rb.ROCKET_ERR_INVALID_ARG),
+    (dict(dilation=np.array([20, 2])), 100, rb.ROCKET_ERR_LENGTH),   # O = 100 - 120 < 1
+    (dict(dilation=np.array([2, 2])), 10, rb.ROCKET_ERR_LENGTH),     # length 7, d 2: O = 10 - 12
+    (dict(padding=np.array([0, 2 ** 24])), 100, rb.ROCKET_ERR_LENGTH),  # O above 2^24 - 1
+])
+def test_plan_validation(lib, over, L, expect):
+    assert _plan_status(lib, _kernels(**over), L) == expect
+
+
+def test_plan_validation_null_and_flags(lib):
+    h = ctypes.c_void_p()
+    assert lib.rocket_plan_create(None, 100, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    k = _kernels()
+    c, keep = rb.as_c_kernels(k)
+    assert lib.rocket_plan_create(ctypes.byref(c), 100, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, 2, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    bad = rb.CKernels(2, 0, 11, c.length, c.dilation, c.padding, c.bias, None)
+    assert lib.rocket_plan_create(ctypes.byref(bad), 100, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    bad = rb.CKernels(2, 0, 12, c.length, c.dilation, c.padding, c.bias, c.weights)
+    assert lib.rocket_plan_create(ctypes.byref(bad), 100, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    bad = rb.CKernels(0, 0, 11, c.length, c.dilation, c.padding, c.bias, c.weights)
+    assert lib.rocket_plan_create(ctypes.byref(bad), 100, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    lib.rocket_plan_destroy(None)
+
+
+def test_transform_validation(lib):
+    k = _kernels()
+    c, keep = rb.as_c_kernels(k)
+    dummy = ctypes.c_void_p(0x1000)
+    assert lib.rocket_transform(dummy, -1, 100, ctypes.byref(c), dummy, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_transform(None, 4, 100, ctypes.byref(c), dummy, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_transform(dummy, 4, 100, ctypes.byref(c), None, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_transform(dummy, 4, 100, None, dummy, None) == rb.ROCKET_ERR_INVALID_ARG
+    bad = _kernels(dilation=np.array([30, 2]))
+    cb, keep2 = rb.as_c_kernels(bad)
+    assert lib.rocket_transform(dummy, 4, 100, ctypes.byref(cb), dummy, None) == rb.ROCKET_ERR_LENGTH
+    # n == 0 is a no-op that never touches memory
+    assert lib.rocket_transform(None, 0, 100, ctypes.byref(c), None, None) == rb.ROCKET_OK
+    assert lib.rocket_transform_plan(None, dummy, 1, dummy, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_info(None, None, None, None, None, None) == rb.ROCKET_ERR_INVALID_ARG
+
+
+def test_plan_tables_errors(lib):
+    t = rb.CPlanTables()
+    assert lib.rocket_plan_tables_build(None, 100, ctypes.byref(t)) == rb.ROCKET_ERR_INVALID_ARG
+    c, keep = rb.as_c_kernels(_kernels())
+    assert lib.rocket_plan_tables_build(ctypes.byref(c), 100, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_tables_build(ctypes.byref(c), 5, ctypes.byref(t)) == rb.ROCKET_ERR_LENGTH
+    assert lib.rocket_plan_tables_build(ctypes.byref(c), 100, ctypes.byref(t)) == rb.ROCKET_OK
+    assert t.n_items == 2
+    lib.rocket_plan_tables_free(ctypes.byref(t))
+    lib.rocket_plan_tables_free(ctypes.byref(t))
+    lib.rocket_plan_tables_free(None)

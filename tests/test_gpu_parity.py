@@ -1,0 +1,163 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle on the
+same seeded inputs.  Full workloads run in the launch configuration the
+benchmark times; the oracle checks every row where it finishes in seconds
+and a row sample (first/last row, first/last of every batch, seeded random
+rows) elsewhere."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+from _util import assert_parity, kernel_set, load_golden, random_kernels
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print("[gpu-parity] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch
+
+
+@pytest.fixture(scope="module")
+def rk():
+    import paper_2601_17091_amd as rk
+    rk.library()
+    return rk
+
+
+def run(rk, torch, X_np, kernels, direct=False):
+    X = torch.from_numpy(np.ascontiguousarray(X_np, dtype=np.float32)).cuda()
+    plan = rk.Plan(kernels, X.shape[1], direct=direct)
+    F = plan.transform(X)
+    torch.cuda.synchronize()
+    return F.cpu().numpy(), plan
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_worked_examples(torch_gpu, rk, oracle, direct):
+    for ex in load_golden():
+        _log("worked example %s direct=%s" % (ex["name"], direct))
+        X = np.asarray(ex["x"], dtype=np.float32)[None, :]
+        ks = kernel_set([len(ex["w"])], [int(ex["dilation"])], [int(ex["padding"])], [ex["b"]], [ex["w"]])
+        F, _ = run(rk, torch_gpu, X, ks, direct)
+        assert F[0, 1] == np.float32(ex["max"]), ex["name"]
+        y = np.atleast_1d(np.asarray(ex["y"]))
+        assert round(float(F[0, 0]) * len(y)) == int((y > 0).sum()), ex["name"]
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_zero_and_constant_series(torch_gpu, rk, direct):
+    _log("zero/constant series direct=%s" % direct)
+    ks = rk.generate_kernels(77, 2000, 300)
+    F, _ = run(rk, torch_gpu, np.zeros((3, 300), np.float32), ks, direct)
+    # X = 0: every dot product is the bias exactly
+    np.testing.assert_array_equal(F[:, 1::2], np.broadcast_to(ks["bias"], (3, 2000)))
+    np.testing.assert_array_equal(F[:, 0::2], np.broadcast_to((ks["bias"] > 0).astype(np.float32), (3, 2000)))
+    F, _ = run(rk, torch_gpu, np.full((1, 300), 1.5, np.float32), ks, direct)
+    unp = ks["padding"] == 0
+    b = ks["bias"].astype(np.float64)
+    assert np.all(np.abs(F[0, 1::2][unp] - b[unp]) < 1e-5)
+    clear = unp & (np.abs(b) > 1e-4)
+    np.testing.assert_array_equal(F[0, 0::2][clear], (b[clear] > 0).astype(np.float32))
+
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_full_workload_every_row(torch_gpu, rk, oracle, name):
+    from paper_2601_17091_amd.workloads import WORKLOADS, workload_series
+    w = WORKLOADS[name]
+    _log("workload %s: %dx%d, K=%d, all rows" % (name, w.n, w.L, w.n_kernels))
+    ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
+    X = workload_series(name)
+    F, plan = run(rk, torch_gpu, X, ks)
+    assert not plan.info()["direct"]
+    ref = oracle.transform(X, ks)
+    r = assert_parity(F, ref, name)
+    _log("  %s" % r)
+
+
+def _sampled(torch, rk, oracle, name, extra, batch_rows=None):
+    from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
+    w = WORKLOADS[name]
+    _log("workload %s: %dx%d, K=%d, sampled rows" % (name, w.n, w.L, w.n_kernels))
+    ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
+    X_np = workload_series(name)
+    X = torch.from_numpy(X_np).cuda()
+    plan = rk.Plan(ks, w.L)
+    assert not plan.info()["direct"]
+    rows = sample_rows(w.n, batch_rows or w.n, extra)
+    got = np.zeros((rows.shape[0], 2 * w.n_kernels), np.float32)
+    if batch_rows is None:
+        F = plan.transform(X)
+        torch.cuda.synchronize()
+        got[:] = F[torch.from_numpy(rows).cuda()].cpu().numpy()
+        del F
+    else:
+        Fb = torch.empty((batch_rows, 2 * w.n_kernels), dtype=torch.float32, device=X.device)
+
+        def grab(r0, Fv):
+            sel = rows[(rows >= r0) & (rows < r0 + Fv.shape[0])]
+            if sel.size:
+                torch.cuda.synchronize()
+                got[np.searchsorted(rows, sel)] = Fv[torch.from_numpy(sel - r0).cuda()].cpu().numpy()
+        rk.transform_batched(plan, X, Fb, batch_rows, on_batch=grab)
+        torch.cuda.synchronize()
+        del Fb
+    ref = oracle.transform(X_np, ks, rows=rows)
+    r = assert_parity(got, ref, name)
+    _log("  rows=%d %s" % (rows.shape[0], r))
+
+
+def test_manufacturing_sampled(torch_gpu, rk, oracle):
+    _sampled(torch_gpu, rk, oracle, "manufacturing", extra=60)
+
+
+def test_long_sampled(torch_gpu, rk, oracle):
+    _sampled(torch_gpu, rk, oracle, "long", extra=14)
+
+
+def test_many_short_batched(torch_gpu, rk, oracle):
+    _sampled(torch_gpu, rk, oracle, "many_short", extra=200, batch_rows=100000)
+
+
+@pytest.mark.parametrize("direct", [False, True])
+def test_all_lengths_and_extremes(torch_gpu, rk, oracle, direct):
+    """Hand-built kernels of every length 1..11, with dilation 1, 2 and the
+    largest admissible one (O = 1 for unpadded kernels), padded or not, on a
+    length that is not a multiple of 64 and a ragged row count."""
+    _log("all lengths direct=%s" % direct)
+    rng = np.random.default_rng(3)
+    L = 97
+    lengths, dil, pad, bias, weights = [], [], [], [], []
+    for ln in range(1, 12):
+        dmax = (L - 1) // max(1, ln - 1) if ln > 1 else 40
+        for d in sorted({1, 2, 3, dmax, max(1, dmax // 2)}):
+            for padded in (0, 1):
+                lengths.append(ln)
+                dil.append(d)
+                pad.append((ln - 1) * d // 2 if padded else 0)
+                bias.append(float(rng.uniform(-1, 1)))
+                weights.append(rng.standard_normal(ln))
+    ks = kernel_set(lengths, dil, pad, bias, weights)
+    X = rng.standard_normal((7, L)).astype(np.float32)
+    F, _ = run(rk, torch_gpu, X, ks, direct)
+    assert_parity(F, oracle.transform(X, ks), "lengths")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_random_small_cases(torch_gpu, rk, oracle, seed):
+    rng = np.random.default_rng(900 + seed)
+    L = int(rng.integers(11, 400))
+    n = int(rng.integers(1, 9))
+    _log("random case seed=%d L=%d n=%d" % (seed, L, n))
+    ks = random_kernels(rng, 300, L)
+    X = rng.standard_normal((n, L)).astype(np.float32)
+    F, _ = run(rk, torch_gpu, X, ks)
+    assert_parity(F, oracle.transform(X, ks), "random")

@@ -1,0 +1,80 @@
+"""Structural GPU checks: determinism, batch and permutation invariance,
+the one-shot entry point, empty input, and the plain kernel against the
+fused one."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+
+    import paper_2601_17091_amd as rk
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    rk.library()
+    from paper_2601_17091_amd.workloads import make_series
+    L = 500
+    ks = rk.generate_kernels(5, 3000, L)
+    X = torch.from_numpy(make_series("sinusoids", 37, L, 55)).cuda()
+    return torch, rk, ks, X
+
+
+def test_deterministic(env):
+    torch, rk, ks, X = env
+    p = rk.Plan(ks, X.shape[1])
+    a = p.transform(X)
+    b = p.transform(X)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_rows_independent_of_batch(env):
+    torch, rk, ks, X = env
+    p = rk.Plan(ks, X.shape[1])
+    full = p.transform(X)
+    for r in (0, 17, 36):
+        one = p.transform(X[r:r + 1].contiguous())
+        torch.cuda.synchronize()
+        assert torch.equal(one[0], full[r])
+
+
+def test_kernel_permutation(env):
+    torch, rk, ks, X = env
+    K = ks["length"].shape[0]
+    perm = np.random.default_rng(1).permutation(K)
+    pk = {k: (v[perm] if isinstance(v, np.ndarray) else v) for k, v in ks.items()}
+    a = rk.Plan(ks, X.shape[1]).transform(X)
+    b = rk.Plan(pk, X.shape[1]).transform(X)
+    torch.cuda.synchronize()
+    a = a.view(X.shape[0], K, 2)
+    b = b.view(X.shape[0], K, 2)
+    assert torch.equal(a[:, torch.from_numpy(perm).cuda()], b)
+
+
+def test_one_shot_matches_plan(env):
+    torch, rk, ks, X = env
+    a = rk.Plan(ks, X.shape[1]).transform(X)
+    b = rk.transform(X, ks)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_empty_input(env):
+    torch, rk, ks, X = env
+    p = rk.Plan(ks, X.shape[1])
+    F = p.transform(X[:0])
+    assert F.shape == (0, 2 * ks["length"].shape[0])
+
+
+def test_direct_kernel_agrees(env):
+    torch, rk, ks, X = env
+    a = rk.Plan(ks, X.shape[1]).transform(X)
+    b = rk.Plan(ks, X.shape[1], direct=True).transform(X)
+    torch.cuda.synchronize()
+    a = a.cpu().numpy()
+    b = b.cpu().numpy()
+    assert np.abs(a[:, 1::2] - b[:, 1::2]).max() < 1e-5
+    O = 500 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"]
+    assert np.abs(np.rint(a[:, 0::2] * O) - np.rint(b[:, 0::2] * O)).max() <= 2
