@@ -83,6 +83,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--direct", action="store_true", help="time the plain kernel instead")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="also run one elementwise copy of this many MiB (reference for "
+                         "hardware byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -130,6 +133,14 @@ def main():
         for r0 in range(0, w.n, batch):
             nb = min(batch, w.n - r0)
             plan.transform_into(X[r0:r0 + nb], F[:nb], stream)
+
+    if args.copy_mb > 0:
+        src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log("copy reference: %d MiB read, %d MiB written" % (args.copy_mb, args.copy_mb))
+        del src, dst
 
     for i in range(args.warmup):
         one_pass()

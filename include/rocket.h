@@ -185,8 +185,10 @@ rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *
  *   wpk          packed weights, per item [G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in
- *                split_counts[n_layouts]: split s of layout i is
- *                order[split_begin[layout_off[i] + s] .. split_begin[layout_off[i] + s + 1])
+ *                split_counts[n_layouts]: the items of variant v in split s
+ *                of layout i (ns = split_counts[i] splits) are
+ *                order[split_begin[layout_off[i] + v*ns + s] ..
+ *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..5
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
  */
 typedef struct {

@@ -175,8 +175,8 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             }
         }
 
-        // item orders: largest cost first (longest-processing-time first),
-        // dealt to splits greedily by accumulated cost
+        // item orders: per variant, largest cost first (longest-processing-
+        // time first), dealt to splits greedily by accumulated cost
         std::vector<int32_t> by_cost(P.items.size());
         for (size_t i = 0; i < by_cost.size(); ++i) by_cost[i] = (int32_t)i;
         std::stable_sort(by_cost.begin(), by_cost.end(), [&](int32_t a, int32_t b) {
@@ -184,19 +184,22 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         });
         for (int li = 0; li < kNumSplitLayouts; ++li) {
             const int ns = kSplitCounts[li];
-            std::vector<std::vector<int32_t>> lists(ns);
-            std::vector<int64_t> load(ns, 0);
-            for (int32_t it : by_cost) {
-                int best = 0;
-                for (int s = 1; s < ns; ++s)
-                    if (load[s] < load[best]) best = s;
-                lists[best].push_back(it);
-                load[best] += P.items[it].cost;
-            }
             P.layout_off.push_back((int32_t)P.split_begin.size());
-            for (int s = 0; s < ns; ++s) {
-                P.split_begin.push_back((int32_t)P.order.size());
-                P.order.insert(P.order.end(), lists[s].begin(), lists[s].end());
+            for (int v = 0; v < kNumVariants; ++v) {
+                std::vector<std::vector<int32_t>> lists(ns);
+                std::vector<int64_t> load(ns, 0);
+                for (int32_t it : by_cost) {
+                    if (P.items[it].variant != v) continue;
+                    int best = 0;
+                    for (int sp = 1; sp < ns; ++sp)
+                        if (load[sp] < load[best]) best = sp;
+                    lists[best].push_back(it);
+                    load[best] += P.items[it].cost;
+                }
+                for (int sp = 0; sp < ns; ++sp) {
+                    P.split_begin.push_back((int32_t)P.order.size());
+                    P.order.insert(P.order.end(), lists[sp].begin(), lists[sp].end());
+                }
             }
             P.split_begin.push_back((int32_t)P.order.size());
         }

@@ -53,8 +53,11 @@ constexpr uint32_t kLaneLastValid = 1u << 30;
 constexpr uint32_t kLaneCounted = 1u << 31;
 constexpr int64_t kMaxOutputs = (int64_t)kLaneQMask;  // O must fit in 24 bits
 
-// Item orders for a few split counts: split s of a layout with `nsplit`
-// splits is order[split_begin[s] .. split_begin[s+1]).
+// Item orders for a few split counts.  Within a layout with `nsplit` splits
+// the items are grouped by variant, so that every workgroup runs one code
+// variant: the items of variant v in split s are
+// order[split_begin[v*nsplit + s] .. split_begin[v*nsplit + s + 1]).
+constexpr int kNumVariants = 2 * kNumEll;
 constexpr int kNumSplitLayouts = 6;  // 1, 2, 4, 8, 16, 32 splits
 constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 
@@ -72,7 +75,7 @@ struct HostPlan {
     std::vector<float> bias;      // per slot
     std::vector<int32_t> kid;     // per slot, -1 = empty
     std::vector<int32_t> order;   // kNumSplitLayouts concatenated item orders
-    std::vector<int32_t> split_begin;  // per layout: nsplit + 1 offsets into order
+    std::vector<int32_t> split_begin;  // per layout: kNumVariants*nsplit + 1 offsets into order
     std::vector<int32_t> layout_off;   // per layout: offset into split_begin
 };
 

@@ -38,6 +38,8 @@ namespace {
 constexpr int kBlock = 256;       // 4 wavefronts per workgroup
 constexpr int kBigBlock = 1024;   // 16 wavefronts share one large staged row
 constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
+constexpr int64_t kRowsLdsBudget = 40 * 1024;  // LDS for the series of one workgroup
+constexpr int kMaxRowsPerBlock = 8;
 
 struct FusedArgs {
     const float *X;
@@ -52,16 +54,40 @@ struct FusedArgs {
     const float *bias;
     const int32_t *kid;
     const int32_t *order;
-    const int32_t *split_begin;  // nsplit + 1 offsets into order
+    const int32_t *split_begin;  // kNumVariants * nsplit + 1 offsets into order
     int32_t nsplit;
+    int32_t n_variants;          // variants that have items, launched variant-major
+    int32_t variants[rocket::kNumVariants];
+    int64_t tiles;               // row tiles of rows_per_block series
     int32_t halo_lo;
     int32_t row_stride;
+    int32_t rows_per_block;  // series staged together in one workgroup's LDS
 };
 
+// DPP controls (GFX9 encoding)
+constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm(1,0,3,2)
+constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
+constexpr int kDppRowHalfMirror = 0x141;
+constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowBcast15 = 0x142;
+constexpr int kDppRowBcast31 = 0x143;
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_max(float v) {
+    const int moved = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL,
+                                                  ROW_MASK, 0xF, false);
+    return fmaxf(v, __int_as_float(moved));
+}
+
+// Maximum over the 64 lanes, with cross-lane moves done by DPP (no LDS).
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-    return v;
+    v = dpp_max<kDppQuadSwap1, 0xF>(v);
+    v = dpp_max<kDppQuadSwap2, 0xF>(v);
+    v = dpp_max<kDppRowHalfMirror, 0xF>(v);
+    v = dpp_max<kDppRowMirror, 0xF>(v);
+    v = dpp_max<kDppRowBcast15, 0xA>(v);
+    v = dpp_max<kDppRowBcast31, 0xC>(v);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 
 // One output step of a work item: load the next series value into the
@@ -129,9 +155,11 @@ struct StepRange<ELL, G, UEND, UEND> {
                                                v4f (&)[G], uint32_t (&)[G][4]) {}
 };
 
+// One work item over the `nrows` series staged in LDS: the item's weights
+// are loaded once and reused for every series.
 template <int ELL, int G>
-__device__ __forceinline__ void run_item(const ItemDesc &it, const float *xrow, const FusedArgs &a,
-                                         float *Frow, int lane) {
+__device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
+                                         const FusedArgs &a, float *F0, int lane) {
     const int d = it.d;
     const int S = it.S;
     // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
@@ -146,116 +174,138 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *xrow, 
     for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int v = 0; v < 4; ++v) bias[g][v] = a.bias[it.k_off + 4 * g + v];
-    v4f mx[G];
-    uint32_t cnt[G][4];
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-#pragma unroll
-        for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
-    }
+    // this lane's output slot when results are written (lane s -> slot s)
+    const int out_kernel = lane < 4 * G ? a.kid[it.k_off + lane] : -1;
     // Step s of a round sits at ring position (s + U0) mod ELL, with U0
     // chosen so that the last step S-1 sits at position ELL-1.
     const int U0 = (ELL - S % ELL) % ELL;
     const int nblocks = (S + U0) / ELL;
-    // xb[q + m*d] is the zero-padded series value under tap m of output q
-    const float *xb = xrow - it.p;
-    for (int rd = 0; rd < it.rounds; ++rd) {
-        const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
-        const int q0 = (int)(e & rocket::kLaneQMask);
-        const bool counted = (e & rocket::kLaneCounted) != 0;
-        const bool last_ok = counted && (e & rocket::kLaneLastValid) != 0;
-        const uint64_t m_last = __builtin_amdgcn_ballot_w64(last_ok);
-        // C operand of the first tap: the slot's bias, or -inf on lanes that
-        // duplicate another lane's chunk
-        v4f binit[G];
+    const float den = (float)it.O;
+    for (int r = 0; r < nrows; ++r) {
+        v4f mx[G];
+        uint32_t cnt[G][4];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+            for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
+        }
+        // xb[q + m*d] is the zero-padded series value under tap m of output q
+        const float *xb = rows0 + r * a.row_stride - it.p;
+        for (int rd = 0; rd < it.rounds; ++rd) {
+            const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
+            const int q0 = (int)(e & rocket::kLaneQMask);
+            const bool counted = (e & rocket::kLaneCounted) != 0;
+            const bool last_ok = counted && (e & rocket::kLaneLastValid) != 0;
+            const uint64_t m_last = __builtin_amdgcn_ballot_w64(last_ok);
+            // C operand of the first tap: the slot's bias, or -inf on lanes
+            // that duplicate another lane's chunk
+            v4f binit[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) binit[g][v] = counted ? bias[g][v] : -INFINITY;
+            // window element m (series value under output q0 + m*d) goes to
+            // ring slot (m + U0) mod ELL; element ELL-1 is loaded by step 0
+            const float *xq = xb + q0;
+            float xw[ELL];
+#pragma unroll
+            for (int i = 0; i < ELL; ++i) {
+                const int m = (i - U0 + ELL) % ELL;
+                xw[i] = (m < ELL - 1) ? xq[m * d] : 0.0f;
+            }
+            const float *xn = xq + (ELL - 1) * d;
+            int ustart = U0;
+            for (int blk = 0; blk + 1 < nblocks; ++blk) {
+                StepRange<ELL, G, 0, ELL>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+                ustart = 0;
+            }
+            StepRange<ELL, G, 0, ELL - 1>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+            item_step<ELL, G, ELL - 1, true>(d, xn, xw, wa, binit, mx, cnt, m_last, last_ok);
+        }
+        // reduce MAX across the wavefront; lane s writes kernel slot s
+        float out_max = 0.0f;
+        uint32_t out_cnt = 0;
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) binit[g][v] = counted ? bias[g][v] : -INFINITY;
-        // window element m (series value under output q0 + m*d) goes to ring
-        // slot (m + U0) mod ELL; element ELL-1 is loaded by the first step
-        const float *xq = xb + q0;
-        float xw[ELL];
-#pragma unroll
-        for (int i = 0; i < ELL; ++i) {
-            const int m = (i - U0 + ELL) % ELL;
-            xw[i] = (m < ELL - 1) ? xq[m * d] : 0.0f;
-        }
-        const float *xn = xq + (ELL - 1) * d;
-        int ustart = U0;
-        for (int blk = 0; blk + 1 < nblocks; ++blk) {
-            StepRange<ELL, G, 0, ELL>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
-            ustart = 0;
-        }
-        StepRange<ELL, G, 0, ELL - 1>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
-        item_step<ELL, G, ELL - 1, true>(d, xn, xw, wa, binit, mx, cnt, m_last, last_ok);
-    }
-    // reduce MAX across the wavefront; lane s writes kernel slot s
-    float out_max = 0.0f;
-    uint32_t out_cnt = 0;
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const float m = wave_max(mx[g][v]);
-            if (lane == 4 * g + v) {
-                out_max = m;
-                out_cnt = cnt[g][v];
+            for (int v = 0; v < 4; ++v) {
+                const float m = wave_max(mx[g][v]);
+                if (lane == 4 * g + v) {
+                    out_max = m;
+                    out_cnt = cnt[g][v];
+                }
             }
-        }
-    if (lane < 4 * G) {
-        const int k = a.kid[it.k_off + lane];
-        if (k >= 0) {
-            float2 r;
-            r.x = (float)out_cnt / (float)it.O;
-            r.y = out_max;
-            *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)k) = r;
+        if (out_kernel >= 0) {
+            float2 res;
+            res.x = (float)out_cnt / den;
+            res.y = out_max;
+            *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K + 2 * (int64_t)out_kernel) = res;
         }
     }
 }
 
+// Items of one variant, taken one at a time from the workgroup's counter.
+template <int ELL, int G>
+__device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items,
+                                          const float *rows0, int nrows, const FusedArgs &a,
+                                          float *F0, int lane) {
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = a.items[a.order[beg + idx]];
+        run_item<ELL, G>(it, rows0, nrows, a, F0, lane);
+    }
+}
+
+// Workgroup = (variant, row tile, split).  Variants are the slowest index,
+// so the waves sharing a CU's instruction cache run the same code variant.
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
-    // Consecutive workgroup ids land on different XCDs; renumber so that the
-    // splits of one series (which write the same F row) share an XCD's L2.
+    // Consecutive workgroup ids land on different XCDs; renumber so that each
+    // XCD walks a contiguous range of (variant, tile, split).
     const int64_t nb = gridDim.x;
     int64_t b = blockIdx.x;
     if (nb % 8 == 0) b = (b % 8) * (nb / 8) + b / 8;
-    const int64_t row = b / a.nsplit;
-    const int split = (int)(b % a.nsplit);
-    if (row >= a.n_rows) return;
-    const int64_t grow = a.row0 + row;
+    const int64_t per_variant = a.tiles * a.nsplit;
+    const int vi = (int)(b / per_variant);
+    const int64_t rest = b % per_variant;
+    const int64_t tile = rest / a.nsplit;
+    const int split = (int)(rest % a.nsplit);
+    const int variant = a.variants[vi];
+    const int beg = a.split_begin[variant * a.nsplit + split];
+    const int cnt_items = a.split_begin[variant * a.nsplit + split + 1] - beg;
+    const int64_t first = tile * a.rows_per_block;
+    if (cnt_items == 0 || first >= a.n_rows) return;
+    const int nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
+    const int64_t grow = a.row0 + first;
 
-    const float *x = a.X + grow * (int64_t)a.L;
-    for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
-        const int m = e - a.halo_lo;
-        smem[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
+    // stage the tile's series with their zero margins, coalesced
+    for (int r = 0; r < nrows; ++r) {
+        const float *x = a.X + (grow + r) * (int64_t)a.L;
+        float *dst = smem + r * a.row_stride;
+        for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
+            const int m = e - a.halo_lo;
+            dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
+        }
     }
     if (threadIdx.x == 0) next_item = 0;
     __syncthreads();
 
     const int lane = threadIdx.x & (rocket::kWave - 1);
-    const int beg = a.split_begin[split];
-    const int cnt_items = a.split_begin[split + 1] - beg;
-    float *Frow = a.F + grow * 2 * (int64_t)a.K;
-    const float *xrow = smem + a.halo_lo;
-    while (true) {
-        int idx = 0;
-        if (lane == 0) idx = atomicAdd(&next_item, 1);
-        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
-        if (idx >= cnt_items) break;
-        const ItemDesc it = a.items[a.order[beg + idx]];
-        switch (it.variant) {
-            case 0: run_item<7, 1>(it, xrow, a, Frow, lane); break;
-            case 1: run_item<7, 2>(it, xrow, a, Frow, lane); break;
-            case 2: run_item<9, 1>(it, xrow, a, Frow, lane); break;
-            case 3: run_item<9, 2>(it, xrow, a, Frow, lane); break;
-            case 4: run_item<11, 1>(it, xrow, a, Frow, lane); break;
-            default: run_item<11, 2>(it, xrow, a, Frow, lane); break;
-        }
+    float *F0 = a.F + grow * 2 * (int64_t)a.K;
+    const float *rows0 = smem + a.halo_lo;
+    switch (variant) {
+        case 0: run_items<7, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 1: run_items<7, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 2: run_items<9, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 3: run_items<9, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 4: run_items<11, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        default: run_items<11, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
     }
 }
 
@@ -456,8 +506,11 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     // enough workgroups to fill the chip several times over: split the work
     // items of a series across workgroups when there are few series
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
+    const int64_t row_bytes = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
+    const int R = (int)std::max<int64_t>(1, std::min<int64_t>(kMaxRowsPerBlock, kRowsLdsBudget / row_bytes));
+    const int64_t tiles = (n + R - 1) / R;
     int li = 0;
-    while (li + 1 < rocket::kNumSplitLayouts && n * rocket::kSplitCounts[li] < target) ++li;
+    while (li + 1 < rocket::kNumSplitLayouts && tiles * rocket::kSplitCounts[li] < target) ++li;
     const int nsplit = rocket::kSplitCounts[li];
     FusedArgs a;
     a.X = X;
@@ -472,19 +525,25 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.order = p->d_order;
     a.split_begin = p->d_split_begin + p->host.layout_off[li];
     a.nsplit = nsplit;
+    a.n_variants = 0;
+    for (int v = 0; v < rocket::kNumVariants; ++v) {
+        const int32_t *sb = p->host.split_begin.data() + p->host.layout_off[li];
+        if (sb[(v + 1) * nsplit] > sb[v * nsplit]) a.variants[a.n_variants++] = v;
+    }
     a.halo_lo = p->host.halo_lo;
     a.row_stride = p->host.row_stride;
-    const int64_t max_rows = (int64_t)INT_MAX / nsplit;
+    a.rows_per_block = R;
+    const int64_t max_rows = ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1))) * R;
     for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
         a.row0 = r0;
         a.n_rows = std::min<int64_t>(max_rows, n - r0);
-        const unsigned nb = (unsigned)(a.n_rows * nsplit);
-        if (p->lds_bytes > kBigLds)
-            hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock),
-                               (size_t)p->lds_bytes, s, a);
+        a.tiles = (a.n_rows + R - 1) / R;
+        const unsigned nb = (unsigned)(a.tiles * nsplit * a.n_variants);
+        const size_t lds = (size_t)(R * row_bytes);
+        if (row_bytes > kBigLds)
+            hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock), lds, s, a);
         else
-            hipLaunchKernelGGL(rocket_fused_kernel<kBlock>, dim3(nb), dim3(kBlock),
-                               (size_t)p->lds_bytes, s, a);
+            hipLaunchKernelGGL(rocket_fused_kernel<kBlock>, dim3(nb), dim3(kBlock), lds, s, a);
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
     }
     return ROCKET_OK;

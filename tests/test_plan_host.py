@@ -93,13 +93,19 @@ def walk(tables, kernels, L, X=None):
 def check_tables(kernels, L, X=None, oracle=None):
     t = rk.plan_tables(kernels, L)
     K = len(kernels["length"])
-    # every item appears exactly once in every split layout
+    # every item appears exactly once in every split layout, in the list of
+    # its own variant
     n_items = t["items"].shape[0]
     for li in range(len(t["layout_off"])):
         ns = t["split_counts"][li]
-        beg = t["split_begin"][t["layout_off"][li]:t["layout_off"][li] + ns + 1]
-        ids = np.concatenate([t["order"][beg[s]:beg[s + 1]] for s in range(ns)])
-        assert np.array_equal(np.sort(ids), np.arange(n_items))
+        beg = t["split_begin"][t["layout_off"][li]:t["layout_off"][li] + 6 * ns + 1]
+        ids = []
+        for v in range(6):
+            for s_ in range(ns):
+                part = t["order"][beg[v * ns + s_]:beg[v * ns + s_ + 1]]
+                assert np.all(t["items"][part, 0] == v)
+                ids.append(part)
+        assert np.array_equal(np.sort(np.concatenate(ids)), np.arange(n_items))
     # every kernel sits in exactly one slot
     kid = t["slot_kernel"]
     assert np.array_equal(np.sort(kid[kid >= 0]), np.arange(K))
