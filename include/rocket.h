@@ -175,13 +175,17 @@ rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *
  * rocket_plan_tables_free (NULL-safe, idempotent).
  *   items        n_items x 16 int32, one row per work item:
  *                [variant, dilation, padding, outputs O, steps S, rounds,
- *                 lane_off, w_off, k_off, cost, 0 x 6];
+ *                 lane_off, w_off, k_off, cost, n_long, n_short,
+ *                 rounds_long, 0 x 3];
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
  *                7/9/11 taps, G kernel groups of 4 slots
- *   lanes        lane table: per item and round, 64 entries; bits 0..23 the
- *                output position of the lane's first step, bit 30 "the
- *                round's last step is inside the lane's chunk", bit 31 "the
- *                lane's outputs are counted" (else it duplicates another lane)
+ *                every residue class (outputs r, r+d, ...) is split into
+ *                chunks of S or S-1 outputs; the first rounds_long rounds
+ *                hold the n_long chunks of S outputs, the rest the n_short
+ *                chunks of S-1 outputs, 64 chunks per round
+ *   lanes        lane table: per item and round, 64 entries, the output
+ *                position of the lane's first step; lanes past the last
+ *                chunk of a length repeat a chunk and are discarded
  *   wpk          packed weights, per item [G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in

@@ -14,6 +14,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "librocket.so")
 SOURCES = ["transform.hip", "plan.cpp", "generate.cpp"]
 ARCH = "gfx950"
@@ -36,6 +37,7 @@ def compile_flags() -> list[str]:
         "-std=c++17",
         "-fPIC",
         "-Wall",
+        "-I", INCLUDE,
         # keep the compiler from forming packed fp32 instructions
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         # host arithmetic (the generator) exactly as written

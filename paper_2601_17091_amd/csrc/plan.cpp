@@ -26,67 +26,81 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
     }
     for (int32_t i = 0; i < k->n_kernels; ++i) {
         const int64_t O = output_length(L, k->length[i], k->dilation[i], k->padding[i]);
-        if (O < 1 || O > kMaxOutputs) return ROCKET_ERR_LENGTH;
+        if (O < 1 || O >= kMaxOutputs) return ROCKET_ERR_LENGTH;
     }
     return ROCKET_OK;
 }
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-void choose_chunking(int64_t O, int64_t d, int32_t *S_out, int32_t *nc_out, int32_t *rounds_out) {
-    const int64_t C = ceil_div(O, d);  // longest residue class
-    int64_t best_cost = -1, best_nc = 1, best_S = C, best_rounds = ceil_div(d, kWave);
-    const int64_t nc_max = std::min<int64_t>(C, 4096);
-    for (int64_t nc = 1; nc <= nc_max; ++nc) {
-        const int64_t S = ceil_div(C, nc);
-        const int64_t rounds = ceil_div(d * nc, kWave);
-        // steps are what costs; a small per-round charge favours fewer rounds
-        const int64_t cost = 4 * rounds * S + rounds;
-        if (best_cost < 0 || cost < best_cost) {
-            best_cost = cost;
-            best_nc = nc;
-            best_S = S;
-            best_rounds = rounds;
-        }
-    }
-    *S_out = (int32_t)best_S;
-    *nc_out = (int32_t)best_nc;
-    *rounds_out = (int32_t)best_rounds;
+// Outputs of residue class r (positions r, r+d, ...) for r < d.
+static int64_t residue_count(int64_t O, int64_t d, int64_t r) { return r < O ? ceil_div(O - r, d) : 0; }
+
+// Chunk counts of the balanced split of every residue class into nc chunks.
+static Chunking split_counts(int64_t O, int64_t d, int64_t nc) {
+    Chunking c;
+    c.nc = nc;
+    const int64_t C = ceil_div(O, d);          // longest residue class
+    c.S = ceil_div(C, nc);
+    // residue classes hold C or C-1 outputs (or none when O < d)
+    const int64_t n_big = std::min(d, O - (C - 1) * d);
+    const int64_t n_small = std::min(d, O) - n_big;
+    auto add = [&](int64_t cr, int64_t count) {
+        if (cr <= 0 || count <= 0) return;
+        const int64_t q = cr / nc, r = cr % nc;  // r chunks of q+1, nc-r of q
+        auto put = [&](int64_t len, int64_t n) {
+            if (len <= 0 || n <= 0) return;
+            if (len == c.S) c.n_long += n;
+            else c.n_short += n;  // len == S - 1
+        };
+        put(q + 1, r * count);
+        put(q, (nc - r) * count);
+    };
+    add(C, n_big);
+    add(C - 1, n_small);
+    c.rounds_long = ceil_div(c.n_long, kWave);
+    c.rounds_short = ceil_div(c.n_short, kWave);
+    return c;
 }
 
-// Lane table of one bucket: chunk c of residue r covers residue positions
-// [floor(c*C_r/nc), floor((c+1)*C_r/nc)), so chunk lengths are S or S-1 and
-// only step S-1 can fall outside a chunk.  Tasks are numbered residue-fastest
-// (task = c*d + r), which keeps neighbouring lanes on neighbouring positions.
-static void build_lane_table(int64_t O, int64_t d, int32_t S, int32_t nc, int32_t rounds,
-                             std::vector<uint32_t> &lanes) {
-    const int64_t ntasks = d * nc;
-    const int64_t nslots = (int64_t)rounds * kWave;
-    // a full-length chunk of residue 0 to duplicate into idle lanes
-    uint32_t dup = 0;
-    {
-        const int64_t C0 = ceil_div(O, d);
-        for (int64_t c = 0; c < nc; ++c) {
-            const int64_t st = c * C0 / nc, en = (c + 1) * C0 / nc;
-            if (en - st == S) {
-                dup = (uint32_t)(st * d) | kLaneLastValid;
-                break;
-            }
+Chunking choose_chunking(int64_t O, int64_t d) {
+    const int64_t C = ceil_div(O, d);
+    Chunking best;
+    int64_t best_cost = -1;
+    const int64_t nc_max = std::min<int64_t>(C, 4096);
+    for (int64_t nc = 1; nc <= nc_max; ++nc) {
+        const Chunking c = split_counts(O, d, nc);
+        const int64_t steps = c.rounds_long * c.S + c.rounds_short * (c.S - 1);
+        // steps are what costs; a small per-round charge favours fewer rounds
+        const int64_t cost = 4 * steps + c.rounds_long + c.rounds_short;
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best = c;
         }
     }
-    for (int64_t t = 0; t < nslots; ++t) {
-        uint32_t e = dup;  // idle lane: exact duplicate, not counted
-        if (t < ntasks) {
-            const int64_t r = t % d, c = t / d;
-            const int64_t Cr = r < O ? ceil_div(O - r, d) : 0;
-            const int64_t st = c * Cr / nc, en = (c + 1) * Cr / nc;
+    return best;
+}
+
+// Lane table of one bucket: the long chunks fill the first rounds, the short
+// chunks the following ones, each numbered residue-fastest so neighbouring
+// lanes work on neighbouring positions.  Lanes past the last chunk of a
+// length repeat its first chunk (their results are discarded).
+static void build_lane_table(int64_t O, int64_t d, const Chunking &c, std::vector<uint32_t> &lanes) {
+    std::vector<uint32_t> longs, shorts;
+    for (int64_t k = 0; k < c.nc; ++k)
+        for (int64_t r = 0; r < std::min(d, O); ++r) {
+            const int64_t cr = residue_count(O, d, r);
+            const int64_t st = k * cr / c.nc, en = (k + 1) * cr / c.nc;
             const int64_t len = en - st;
-            if (len >= 1) {
-                e = (uint32_t)(r + st * d) | kLaneCounted | (len == S ? kLaneLastValid : 0u);
-            }
+            if (len <= 0) continue;
+            (len == c.S ? longs : shorts).push_back((uint32_t)(r + st * d));
         }
-        lanes.push_back(e);
-    }
+    auto emit = [&](const std::vector<uint32_t> &t, int64_t rounds) {
+        for (int64_t i = 0; i < rounds * kWave; ++i)
+            lanes.push_back(i < (int64_t)t.size() ? t[i] : t[0]);
+    };
+    emit(longs, c.rounds_long);
+    emit(shorts, c.rounds_short);
 }
 
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
@@ -97,13 +111,16 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         // bucket kernels by (length, dilation, padding); kernels keep their
         // original order inside a bucket
         std::map<std::tuple<int32_t, int32_t, int32_t>, std::vector<int32_t>> buckets;
+        // every computed output is a real one, so the taps reach from
+        // position -p to L-1+p, plus (ell - length) taps of zero weight for
+        // kernels run at a longer code length
         int64_t halo_lo = 0, halo_hi = 0;
         for (int32_t i = 0; i < k->n_kernels; ++i) {
             const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
             buckets[std::make_tuple(len, d, p)].push_back(i);
             const int64_t ell_eff = kEllValues[ell_index_for(len)];
             halo_lo = std::max<int64_t>(halo_lo, p);
-            halo_hi = std::max<int64_t>(halo_hi, (int64_t)p + d + (ell_eff - len) * (int64_t)d);
+            halo_hi = std::max<int64_t>(halo_hi, (int64_t)p + (ell_eff - len) * (int64_t)d);
         }
         P.n_buckets = (int64_t)buckets.size();
         const int64_t stride = halo_lo + L + halo_hi;
@@ -123,8 +140,9 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             const int eidx = ell_index_for(len);
             const int ell = kEllValues[eidx];
             const int64_t O = output_length(L, len, d, p);
-            int32_t S, nc, rounds;
-            choose_chunking(O, d, &S, &nc, &rounds);
+            const Chunking ch = choose_chunking(O, d);
+            const int32_t S = (int32_t)ch.S;
+            const int32_t rounds = (int32_t)(ch.rounds_long + ch.rounds_short);
             size_t pos = 0;
             bool table_built = false;
             int32_t lane_off = 0;
@@ -134,7 +152,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
                 if (!table_built) {
                     lane_off = (int32_t)P.lanes.size();
-                    build_lane_table(O, d, S, nc, rounds, P.lanes);
+                    build_lane_table(O, d, ch, P.lanes);
                     table_built = true;
                 }
                 ItemDesc it;
@@ -148,7 +166,10 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 it.lane_off = lane_off;
                 it.w_off = (int32_t)P.wpk.size();
                 it.k_off = (int32_t)P.kid.size();
-                it.cost = rounds * S * ell * G;
+                it.cost = (int32_t)((ch.rounds_long * S + ch.rounds_short * (S - 1)) * ell * G);
+                it.n_long = (int32_t)ch.n_long;
+                it.n_short = (int32_t)ch.n_short;
+                it.rounds_long = (int32_t)ch.rounds_long;
                 // A-operand weights: [g][j][slot i]; zeros for empty slots and
                 // for taps past the kernel's own length
                 for (int g = 0; g < G; ++g)

@@ -5,7 +5,7 @@
 #include <cstdint>
 #include <vector>
 
-#include "../../include/rocket.h"
+#include "rocket.h"
 
 namespace rocket {
 
@@ -25,33 +25,32 @@ constexpr int kMaxGroups = 2;  // a work item holds 4 or 8 kernels of one bucket
 
 // One work item: up to 4*G kernels that share (length, dilation, padding).
 // The 64 lanes of a wavefront each own a chunk of consecutive outputs along
-// one dilation residue class (positions q, q+d, q+2d, ...).  A "round" is one
-// pass of 64 such chunks; every chunk has S steps except that step S-1 may be
-// past the end of its chunk (flagged per lane).
+// one dilation residue class (positions q, q+d, q+2d, ...).  Each residue
+// class is split into nc chunks of balanced length, S or S-1 outputs, and a
+// "round" gathers 64 chunks of one length: first the rounds of S-step
+// chunks, then those of (S-1)-step chunks.  Every output is computed by
+// exactly one lane; in the last round of each length the lanes without a
+// chunk start from -inf and contribute nothing.
 struct alignas(16) ItemDesc {
-    int32_t variant;   // ell_index * 2 + (G - 1)
-    int32_t d;         // dilation
-    int32_t p;         // padding
-    int32_t O;         // number of dot products (outputs)
-    int32_t S;         // steps per chunk
-    int32_t rounds;    // rounds per series
-    int32_t lane_off;  // first lane-table entry (rounds * 64 entries)
-    int32_t w_off;     // first packed weight: [G][ell][4] floats
-    int32_t k_off;     // first slot entry: kernel ids and biases, [4G]
-    int32_t cost;      // MFMA instructions per series (scheduling weight)
-    int32_t reserved[6];
+    int32_t variant;      // ell_index * 2 + (G - 1)
+    int32_t d;            // dilation
+    int32_t p;            // padding
+    int32_t O;            // number of dot products (outputs)
+    int32_t S;            // steps of a long chunk (short chunks: S - 1)
+    int32_t rounds;       // rounds per series (long, then short)
+    int32_t lane_off;     // first lane-table entry (rounds * 64 entries)
+    int32_t w_off;        // first packed weight: [G][ell][4] floats
+    int32_t k_off;        // first slot entry: kernel ids and biases, [4G]
+    int32_t cost;         // MFMA instructions per series (scheduling weight)
+    int32_t n_long;       // chunks of S outputs
+    int32_t n_short;      // chunks of S - 1 outputs
+    int32_t rounds_long;  // rounds of long chunks: ceil(n_long / 64)
+    int32_t reserved[3];
 };
 static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
 
-// Lane-table entry: bits 0..23 hold q0, the output position of the lane's
-// step 0; bit 30 says step S-1 is a valid output of this lane; bit 31 says
-// the lane's outputs are counted (a lane without it duplicates another
-// lane's chunk exactly, so its values are safe for MAX but must not be
-// counted twice).
-constexpr uint32_t kLaneQMask = 0x00FFFFFFu;
-constexpr uint32_t kLaneLastValid = 1u << 30;
-constexpr uint32_t kLaneCounted = 1u << 31;
-constexpr int64_t kMaxOutputs = (int64_t)kLaneQMask;  // O must fit in 24 bits
+// Lane-table entry: the output position of the lane's first step.
+constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
 
 // Item orders for a few split counts.  Within a layout with `nsplit` splits
 // the items are grouped by variant, so that every workgroup runs one code
@@ -85,8 +84,12 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L);
 // Build the host-side tables of a plan.  Assumes validate_kernels passed.
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out);
 
-// Choose the chunking of one bucket: number of chunks per residue nc, steps
-// S and rounds, minimising rounds * S (the MFMA steps one series costs).
-void choose_chunking(int64_t O, int64_t d, int32_t *S, int32_t *nc, int32_t *rounds);
+// Chunking of one bucket: nc chunks per residue class, chunk lengths S and
+// S-1, with n_long / n_short chunks of each, chosen to minimise the MFMA
+// steps one series costs.
+struct Chunking {
+    int64_t nc = 1, S = 1, n_long = 0, n_short = 0, rounds_long = 0, rounds_short = 0;
+};
+Chunking choose_chunking(int64_t O, int64_t d);
 
 }  // namespace rocket

@@ -33,6 +33,15 @@ using rocket::ItemDesc;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
 
+// Read-only tables indexed by wavefront-uniform values are read through the
+// constant address space, which lets the compiler use scalar loads.
+template <typename T>
+using ConstPtr = const __attribute__((address_space(4))) T *;
+template <typename T>
+__device__ __forceinline__ ConstPtr<T> as_const(const T *p) {
+    return (ConstPtr<T>)(p);
+}
+
 namespace {
 
 constexpr int kBlock = 256;       // 4 wavefronts per workgroup
@@ -40,6 +49,7 @@ constexpr int kBigBlock = 1024;   // 16 wavefronts share one large staged row
 constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
 constexpr int64_t kRowsLdsBudget = 40 * 1024;  // LDS for the series of one workgroup
 constexpr int kMaxRowsPerBlock = 8;
+constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dealt round-robin
 
 struct FusedArgs {
     const float *X;
@@ -58,7 +68,7 @@ struct FusedArgs {
     int32_t nsplit;
     int32_t n_variants;          // variants that have items, launched variant-major
     int32_t variants[rocket::kNumVariants];
-    int64_t tiles;               // row tiles of rows_per_block series
+    int64_t tiles_per_xcd;       // row tiles (of rows_per_block series) per XCD
     int32_t halo_lo;
     int32_t row_stride;
     int32_t rows_per_block;  // series staged together in one workgroup's LDS
@@ -69,117 +79,148 @@ constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm(1,0,3,2)
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
-constexpr int kDppRowBcast15 = 0x142;
-constexpr int kDppRowBcast31 = 0x143;
 
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ float dpp_max(float v) {
-    const int moved = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL,
-                                                  ROW_MASK, 0xF, false);
-    return fmaxf(v, __int_as_float(moved));
-}
-
-// Maximum over the 64 lanes, with cross-lane moves done by DPP (no LDS).
-__device__ __forceinline__ float wave_max(float v) {
-    v = dpp_max<kDppQuadSwap1, 0xF>(v);
-    v = dpp_max<kDppQuadSwap2, 0xF>(v);
-    v = dpp_max<kDppRowHalfMirror, 0xF>(v);
-    v = dpp_max<kDppRowMirror, 0xF>(v);
-    v = dpp_max<kDppRowBcast15, 0xA>(v);
-    v = dpp_max<kDppRowBcast31, 0xC>(v);
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
-// One output step of a work item: load the next series value into the
-// register window, run the G x ELL MFMA taps, and fold the 4G results into
-// the running MAX and positive counts.  U is the step's position in the
-// window ring, so every register index is a compile-time constant.
-//
-// Lanes that only duplicate another lane's chunk start from a -inf
-// accumulator (binit), so their results are never positive and never raise
-// MAX; no mask is needed for them.  The last step of a round (LAST) can lie
-// past the end of a lane's chunk; there the count uses the mask m_last and
-// MAX skips the lane.
-template <int ELL, int G, int U, bool LAST>
-__device__ __forceinline__ void item_step(int d, const float *&xn, float (&xw)[ELL],
-                                          const float (&wa)[G][ELL], const v4f (&binit)[G],
-                                          v4f (&mx)[G], uint32_t (&cnt)[G][4], uint64_t m_last,
-                                          bool last_ok) {
-    xw[(U + ELL - 1) % ELL] = *xn;
-    xn += d;
-    v4f acc[G];
+// NS consecutive output steps of one round, as an outer-product contraction
+// over the taps.  The window of series values under the NS outputs
+// (NS + ELL - 1 values spaced d apart, starting at xs) is read from LDS
+// first; then tap j of every step and kernel group is issued before tap j+1,
+// so the wavefront keeps NS*G independent MFMA accumulation chains in
+// flight, each starting from binit: the slots' biases, or -inf on lanes
+// without a chunk.  Every other lane computes real outputs only, so MAX
+// folds all results (v_max3 over pairs of steps) and the positive count is
+// a ballot of y > 0 popcounted on the scalar unit.
+template <int ELL, int G, int NS>
+__device__ __forceinline__ void step_block(const float *xs, int d, const float (&wa)[G][ELL],
+                                           const v4f (&binit)[G], v4f (&mx)[G],
+                                           uint32_t (&cnt)[G][4]) {
+    float xw[NS + ELL - 1];
 #pragma unroll
-    for (int g = 0; g < G; ++g) acc[g] = binit[g];
+    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = xs[m * d];
+    v4f acc[NS][G];
 #pragma unroll
-    for (int j = 0; j < ELL; ++j)
+    for (int u = 0; u < NS; ++u)
 #pragma unroll
         for (int g = 0; g < G; ++g)
-            acc[g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[(U + j) % ELL], acc[g], 0, 0, 0);
-    if (!LAST) {
+            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], binit[g], 0, 0, 0);
 #pragma unroll
-        for (int g = 0; g < G; ++g)
+    for (int j = 1; j < ELL; ++j)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[g][v] > 0.0f));
-                mx[g][v] = fmaxf(mx[g][v], acc[g][v]);
-            }
-    } else {
+        for (int u = 0; u < NS; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[u + j], acc[u][g], 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < NS; ++u)
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                cnt[g][v] +=
-                    (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[g][v] > 0.0f) & m_last);
+                cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][g][v] > 0.0f));
+#pragma unroll
+    for (int u = 0; u + 1 < NS; u += 2)
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) mx[g][v] = last_ok ? fmaxf(mx[g][v], acc[g][v]) : mx[g][v];
+            for (int v = 0; v < 4; ++v)
+                mx[g][v] = fmaxf(fmaxf(mx[g][v], acc[u][g][v]), acc[u + 1][g][v]);
+    if (NS % 2 == 1) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) mx[g][v] = fmaxf(mx[g][v], acc[NS - 1][g][v]);
     }
 }
 
-// Steps with ring positions U .. UEND-1 of one block, each run if U >= ustart.
-template <int ELL, int G, int U, int UEND>
-struct StepRange {
-    __device__ __forceinline__ static void run(int ustart, int d, const float *&xn, float (&xw)[ELL],
+// The last block of a round: its length nv (1..N) selects a code copy.
+template <int ELL, int G, int N>
+struct TailBlock {
+    __device__ __forceinline__ static void run(int nv, const float *xs, int d,
                                                const float (&wa)[G][ELL], const v4f (&binit)[G],
                                                v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
-        if (U >= ustart) item_step<ELL, G, U, false>(d, xn, xw, wa, binit, mx, cnt, 0, true);
-        StepRange<ELL, G, U + 1, UEND>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
+        if (nv == N)
+            step_block<ELL, G, N>(xs, d, wa, binit, mx, cnt);
+        else
+            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, mx, cnt);
     }
 };
 
-template <int ELL, int G, int UEND>
-struct StepRange<ELL, G, UEND, UEND> {
-    __device__ __forceinline__ static void run(int, int, const float *&, float (&)[ELL],
-                                               const float (&)[G][ELL], const v4f (&)[G],
-                                               v4f (&)[G], uint32_t (&)[G][4]) {}
+template <int ELL, int G>
+struct TailBlock<ELL, G, 0> {
+    __device__ __forceinline__ static void run(int, const float *, int, const float (&)[G][ELL],
+                                               const v4f (&)[G], v4f (&)[G],
+                                               uint32_t (&)[G][4]) {}
 };
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_max_row(float v) {
+    const int moved = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF,
+                                                  0xF, false);
+    return fmaxf(v, __int_as_float(moved));
+}
+
+// Lane-wise max of two registers after swapping the upper 32 lanes of a
+// with the lower 32 lanes of b: lanes 0-31 then reduce a over lane pairs
+// (i, i+32), lanes 32-63 reduce b.
+__device__ __forceinline__ float fold32(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false,
+                                                    false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// The same with 16-lane rows: odd rows of a swap with even rows of b, so
+// rows 0 and 2 of the result reduce a over row pairs, rows 1 and 3 reduce b.
+__device__ __forceinline__ float fold16(float a, float b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false,
+                                                    false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Max within each 16-lane row, broadcast to the row.
+__device__ __forceinline__ float row_max(float v) {
+    v = dpp_max_row<kDppQuadSwap1>(v);
+    v = dpp_max_row<kDppQuadSwap2>(v);
+    v = dpp_max_row<kDppRowHalfMirror>(v);
+    v = dpp_max_row<kDppRowMirror>(v);
+    return v;
+}
+
+// Reduce the 4 slot maxima of one group over the wavefront: on return, every
+// lane of 16-lane row q holds the maximum of slot kSlotOfRow[q].
+__device__ __forceinline__ float reduce4(const v4f &m) {
+    return row_max(fold16(fold32(m[0], m[1]), fold32(m[2], m[3])));
+}
+// fold32(m0, m1): lanes 0-31 slot 0, lanes 32-63 slot 1; fold16 of
+// (slot0|slot1) and (slot2|slot3): row 0 slot 0, row 1 slot 2, row 2 slot 1,
+// row 3 slot 3.
+__device__ __forceinline__ int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
 
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.
 template <int ELL, int G>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
+    // steps per block: 8 independent accumulation chains per wavefront
+    constexpr int T = 8 / G;
     const int d = it.d;
-    const int S = it.S;
     // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
     float wa[G][ELL];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
-    // biases of block rows v (kernel slots v)
-    float bias[G][4];
+    // C operand of the first tap: the bias of block row v (kernel slot v)
+    v4f bias[G];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) bias[g][v] = a.bias[it.k_off + 4 * g + v];
-    // this lane's output slot when results are written (lane s -> slot s)
-    const int out_kernel = lane < 4 * G ? a.kid[it.k_off + lane] : -1;
-    // Step s of a round sits at ring position (s + U0) mod ELL, with U0
-    // chosen so that the last step S-1 sits at position ELL-1.
-    const int U0 = (ELL - S % ELL) % ELL;
-    const int nblocks = (S + U0) / ELL;
+        for (int v = 0; v < 4; ++v) bias[g][v] = as_const(a.bias)[it.k_off + 4 * g + v];
+    // after the reduction, lane 16q writes slot slot_of_row(q) of each group
+    const int row_of_lane = lane >> 4;
+    const bool writer = (lane & 15) == 0;  // lanes 0, 16, 32, 48
+    int out_kernel[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
     const float den = (float)it.O;
     for (int r = 0; r < nrows; ++r) {
         v4f mx[G];
@@ -193,56 +234,72 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         // xb[q + m*d] is the zero-padded series value under tap m of output q
         const float *xb = rows0 + r * a.row_stride - it.p;
         for (int rd = 0; rd < it.rounds; ++rd) {
-            const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
-            const int q0 = (int)(e & rocket::kLaneQMask);
-            const bool counted = (e & rocket::kLaneCounted) != 0;
-            const bool last_ok = counted && (e & rocket::kLaneLastValid) != 0;
-            const uint64_t m_last = __builtin_amdgcn_ballot_w64(last_ok);
-            // C operand of the first tap: the slot's bias, or -inf on lanes
-            // that duplicate another lane's chunk
+            // rounds of S-output chunks first, then of (S-1)-output chunks
+            const bool is_long = rd < it.rounds_long;
+            const int len = is_long ? it.S : it.S - 1;
+            const int active = is_long ? min(rocket::kWave, it.n_long - rd * rocket::kWave)
+                                       : min(rocket::kWave, it.n_short - (rd - it.rounds_long) * rocket::kWave);
             v4f binit[G];
+            if (active == rocket::kWave) {
 #pragma unroll
-            for (int g = 0; g < G; ++g)
+                for (int g = 0; g < G; ++g) binit[g] = bias[g];
+            } else {
+                const bool own = lane < active;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) binit[g][v] = counted ? bias[g][v] : -INFINITY;
-            // window element m (series value under output q0 + m*d) goes to
-            // ring slot (m + U0) mod ELL; element ELL-1 is loaded by step 0
-            const float *xq = xb + q0;
-            float xw[ELL];
+                for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int i = 0; i < ELL; ++i) {
-                const int m = (i - U0 + ELL) % ELL;
-                xw[i] = (m < ELL - 1) ? xq[m * d] : 0.0f;
+                    for (int v = 0; v < 4; ++v) binit[g][v] = own ? bias[g][v] : -INFINITY;
             }
-            const float *xn = xq + (ELL - 1) * d;
-            int ustart = U0;
-            for (int blk = 0; blk + 1 < nblocks; ++blk) {
-                StepRange<ELL, G, 0, ELL>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
-                ustart = 0;
+            const float *xs = xb + a.lanes[it.lane_off + rd * rocket::kWave + lane];
+            const int nfull = (len - 1) / T;  // full blocks before the last block
+            const int nv = len - nfull * T;   // length of the last block, 1..T
+            for (int blk = 0; blk < nfull; ++blk) {
+                step_block<ELL, G, T>(xs, d, wa, binit, mx, cnt);
+                xs += T * d;
             }
-            StepRange<ELL, G, 0, ELL - 1>::run(ustart, d, xn, xw, wa, binit, mx, cnt);
-            item_step<ELL, G, ELL - 1, true>(d, xn, xw, wa, binit, mx, cnt, m_last, last_ok);
+            TailBlock<ELL, G, T>::run(nv, xs, d, wa, binit, mx, cnt);
         }
-        // reduce MAX across the wavefront; lane s writes kernel slot s
-        float out_max = 0.0f;
-        uint32_t out_cnt = 0;
+        // MAX over the wavefront; counts are already scalar
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const float m = wave_max(mx[g][v]);
-                if (lane == 4 * g + v) {
-                    out_max = m;
-                    out_cnt = cnt[g][v];
-                }
+        for (int g = 0; g < G; ++g) {
+            const float m = reduce4(mx[g]);
+            // the count of slot slot_of_row(q) for the lanes of row q
+            // (readfirstlane keeps the four uniform counts independent scalars,
+            // so the selects stay selects instead of an indexed array)
+            const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
+            const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
+            const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
+            const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
+            uint32_t c = c0;
+            c = lane >= 16 ? c2 : c;
+            c = lane >= 32 ? c1 : c;
+            c = lane >= 48 ? c3 : c;
+            if (out_kernel[g] >= 0) {
+                float2 res;
+                res.x = (float)c / den;
+                res.y = m;
+                *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K + 2 * (int64_t)out_kernel[g]) = res;
             }
-        if (out_kernel >= 0) {
-            float2 res;
-            res.x = (float)out_cnt / den;
-            res.y = out_max;
-            *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K + 2 * (int64_t)out_kernel) = res;
         }
     }
+}
+
+__device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
+    ItemDesc it;
+    it.variant = p->variant;
+    it.d = p->d;
+    it.p = p->p;
+    it.O = p->O;
+    it.S = p->S;
+    it.rounds = p->rounds;
+    it.lane_off = p->lane_off;
+    it.w_off = p->w_off;
+    it.k_off = p->k_off;
+    it.cost = p->cost;
+    it.n_long = p->n_long;
+    it.n_short = p->n_short;
+    it.rounds_long = p->rounds_long;
+    return it;
 }
 
 // Items of one variant, taken one at a time from the workgroup's counter.
@@ -255,30 +312,31 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
         if (lane == 0) idx = atomicAdd(next_item, 1);
         idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
         if (idx >= cnt_items) break;
-        const ItemDesc it = a.items[a.order[beg + idx]];
+        const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
         run_item<ELL, G>(it, rows0, nrows, a, F0, lane);
     }
 }
 
-// Workgroup = (variant, row tile, split).  Variants are the slowest index,
-// so the waves sharing a CU's instruction cache run the same code variant.
+// Workgroup = (variant, row tile, split); each workgroup stages its row tile
+// in LDS and runs the items of one variant over it.
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
-    // Consecutive workgroup ids land on different XCDs; renumber so that each
-    // XCD walks a contiguous range of (variant, tile, split).
-    const int64_t nb = gridDim.x;
-    int64_t b = blockIdx.x;
-    if (nb % 8 == 0) b = (b % 8) * (nb / 8) + b / 8;
-    const int64_t per_variant = a.tiles * a.nsplit;
-    const int vi = (int)(b / per_variant);
-    const int64_t rest = b % per_variant;
-    const int64_t tile = rest / a.nsplit;
+    // Workgroup b runs on XCD b % 8.  Every XCD takes its own share of the
+    // row tiles and walks them variant by variant, so all XCDs get the same
+    // mix of work while the CUs of an XCD run one code variant at a time.
+    const int64_t b = blockIdx.x;
+    const int xcd = (int)(b % kXcds);
+    const int64_t local = b / kXcds;
+    const int64_t per_variant = a.tiles_per_xcd * a.nsplit;
+    const int vi = (int)(local / per_variant);
+    const int64_t rest = local % per_variant;
+    const int64_t tile = xcd * a.tiles_per_xcd + rest / a.nsplit;
     const int split = (int)(rest % a.nsplit);
     const int variant = a.variants[vi];
-    const int beg = a.split_begin[variant * a.nsplit + split];
-    const int cnt_items = a.split_begin[variant * a.nsplit + split + 1] - beg;
+    const int beg = as_const(a.split_begin)[variant * a.nsplit + split];
+    const int cnt_items = as_const(a.split_begin)[variant * a.nsplit + split + 1] - beg;
     const int64_t first = tile * a.rows_per_block;
     if (cnt_items == 0 || first >= a.n_rows) return;
     const int nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
@@ -533,12 +591,14 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.halo_lo = p->host.halo_lo;
     a.row_stride = p->host.row_stride;
     a.rows_per_block = R;
-    const int64_t max_rows = ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1))) * R;
+    const int64_t max_rows =
+        ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1)) / kXcds - 1) * kXcds * R;
     for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
         a.row0 = r0;
         a.n_rows = std::min<int64_t>(max_rows, n - r0);
-        a.tiles = (a.n_rows + R - 1) / R;
-        const unsigned nb = (unsigned)(a.tiles * nsplit * a.n_variants);
+        const int64_t tiles_now = (a.n_rows + R - 1) / R;
+        a.tiles_per_xcd = (tiles_now + kXcds - 1) / kXcds;
+        const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)(R * row_bytes);
         if (row_bytes > kBigLds)
             hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock), lds, s, a);

@@ -2,14 +2,14 @@
 
 The planner's tables (work items, lane tables, packed weights, item orders)
 are read back through rocket_plan_tables_build and walked here exactly the
-way the GPU kernel walks them: every lane of every round takes the output
-positions q0, q0+d, ..., q0+(S-1)d, loads series values at
-halo_lo - p + q + j*d from the zero-margined row, counts only lanes flagged
-as counted (and, on the round's last step, only lanes whose chunk reaches
-it).  The checks: every output of every kernel is counted exactly once,
-MAX only sees real outputs, every load stays inside the staged row, the
-packed weights are the kernels' own, and an fp32 replay of the walk lands
-inside the oracle's certified bounds.
+way the GPU kernel walks them: in every round each active lane takes the
+output positions q0, q0+d, ... (S or S-1 of them, by round) and loads the
+series values at halo_lo - p + q + j*d from the zero-margined row; lanes
+past the round's chunk count are discarded.  The checks: every position an
+active lane computes is a real output, every output of every kernel is
+computed exactly once, every load (idle lanes included) stays inside the
+staged row, the packed weights are the kernels' own, and an fp32 replay of
+the walk lands inside the oracle's certified bounds.
 """
 import numpy as np
 import pytest
@@ -18,9 +18,6 @@ import paper_2601_17091_amd as rk
 from _util import kernel_set
 
 ELLS = (7, 9, 11)
-Q_MASK = 0x00FFFFFF
-LAST_VALID = 1 << 30
-COUNTED = 1 << 31
 
 
 def walk(tables, kernels, L, X=None):
@@ -30,8 +27,7 @@ def walk(tables, kernels, L, X=None):
     items = tables["items"]
     lanes = tables["lanes"].astype(np.int64)
     halo_lo, stride = tables["halo_lo"], tables["row_stride"]
-    cover = [None] * K
-    maxcover = [None] * K
+    cover = [np.zeros(0, np.int64)] * K
     F = None
     if X is not None:
         n = X.shape[0]
@@ -39,7 +35,8 @@ def walk(tables, kernels, L, X=None):
         rows = np.zeros((n, stride), dtype=np.float32)
         rows[:, halo_lo:halo_lo + L] = X
     for it in items:
-        variant, d, p, O, S, rounds, lane_off, w_off, k_off = (int(v) for v in it[:9])
+        (variant, d, p, O, S, rounds, lane_off, w_off, k_off, cost, n_long, n_short,
+         rounds_long) = (int(v) for v in it[:13])
         ell = ELLS[variant // 2]
         G = variant % 2 + 1
         nslot = 4 * G
@@ -53,41 +50,46 @@ def walk(tables, kernels, L, X=None):
                 assert np.array_equal(Wslot[s_, :ln], kernels["weights"][k, :ln])
                 assert np.all(Wslot[s_, ln:] == 0)
                 assert bias[s_] == np.float32(kernels["bias"][k])
-                assert (ln, int(kernels["dilation"][k]), int(kernels["padding"][k])) == (
-                    int(kernels["length"][k]), d, p)
+                assert (int(kernels["dilation"][k]), int(kernels["padding"][k])) == (d, p)
             else:
                 assert np.all(Wslot[s_] == 0)
-        e = lanes[lane_off:lane_off + rounds * 64].reshape(rounds, 64)
-        q0 = e & Q_MASK
-        counted = (e & COUNTED) != 0
-        last_ok = counted & ((e & LAST_VALID) != 0)
-        steps = np.arange(S)
-        q = q0[:, :, None] + steps[None, None, :] * d                    # [round, lane, step]
-        cnt_mask = np.broadcast_to(counted[:, :, None], q.shape).copy()
-        cnt_mask[:, :, S - 1] = last_ok
-        # loads: window elements m = 0 .. S+ell-2 of every lane
-        m = np.arange(S + ell - 1)
-        idx = halo_lo - p + q0[:, :, None] + m[None, None, :] * d
-        assert idx.min() >= 0 and idx.max() < stride, (d, p, O, S)
-        counted_pos = q[cnt_mask]
+        assert rounds == rounds_long + -(-n_short // 64) and rounds_long == -(-n_long // 64)
+        assert cost == (rounds_long * S + (rounds - rounds_long) * (S - 1)) * ell * G
+        counted = []
+        ys = [] if X is not None else None
+        for rd in range(rounds):
+            is_long = rd < rounds_long
+            length = S if is_long else S - 1
+            active = min(64, n_long - 64 * rd) if is_long else min(64, n_short - 64 * (rd - rounds_long))
+            assert length >= 1 and active >= 1
+            q0 = lanes[lane_off + 64 * rd:lane_off + 64 * rd + 64]
+            q = q0[:, None] + np.arange(length)[None, :] * d        # [lane, step]
+            # every lane's loads stay in the staged row, idle lanes included
+            m = np.arange(length + ell - 1)
+            idx = halo_lo - p + q0[:, None] + m[None, :] * d
+            assert idx.min() >= 0 and idx.max() < stride, (d, p, O, S)
+            qa = q[:active]
+            assert qa.min() >= 0 and qa.max() < O                    # real outputs only
+            counted.append(qa.ravel())
+            if X is not None:
+                tap_idx = halo_lo - p + qa[..., None] + np.arange(ell)[None, None, :] * d
+                xv = rows[:, tap_idx]                                # [n, lane, step, tap]
+                acc = np.broadcast_to(bias.astype(np.float32), xv.shape[:3] + (nslot,)).copy()
+                for j in range(ell):
+                    acc = (acc + xv[..., j, None] * Wslot[None, None, None, :, j]).astype(np.float32)
+                ys.append(acc.reshape(acc.shape[0], -1, nslot))
+        allq = np.concatenate(counted)
         for k in kid[kid >= 0]:
-            cover[k] = np.bincount(counted_pos, minlength=O)
-            maxcover[k] = np.unique(q[cnt_mask])
+            cover[k] = np.bincount(allq, minlength=O)
         if X is not None:
-            # y[row, round, lane, step, slot], accumulated tap by tap in fp32
-            tap_idx = halo_lo - p + q[..., None] + np.arange(ell)[None, None, None, :] * d
-            xv = rows[:, tap_idx]                                       # [n, r, l, s, j]
-            acc = np.broadcast_to(bias.astype(np.float32), xv.shape[:4] + (nslot,)).copy()
-            for j in range(ell):
-                acc = (acc + xv[..., j, None] * Wslot[None, None, None, None, :, j]).astype(np.float32)
-            pos = (acc > 0) & cnt_mask[None, ..., None]
-            cnt = pos.sum(axis=(1, 2, 3))
-            mxv = np.where(cnt_mask[None, ..., None], acc, -np.inf).max(axis=(1, 2, 3))
+            y = np.concatenate(ys, axis=1)                               # [n, outputs, slot]
+            cnt = (y > 0).sum(axis=1)
+            mxv = y.max(axis=1)
             for s_, k in enumerate(kid):
                 if k >= 0:
                     F[:, 2 * k] = cnt[:, s_] / O
                     F[:, 2 * k + 1] = mxv[:, s_]
-    return cover, maxcover, F
+    return cover, F
 
 
 def check_tables(kernels, L, X=None, oracle=None):
@@ -109,11 +111,10 @@ def check_tables(kernels, L, X=None, oracle=None):
     # every kernel sits in exactly one slot
     kid = t["slot_kernel"]
     assert np.array_equal(np.sort(kid[kid >= 0]), np.arange(K))
-    cover, maxcover, F = walk(t, kernels, L, X)
+    cover, F = walk(t, kernels, L, X)
     for k in range(K):
         O = L + 2 * int(kernels["padding"][k]) - (int(kernels["length"][k]) - 1) * int(kernels["dilation"][k])
         assert cover[k].shape[0] == O and np.all(cover[k] == 1), k
-        assert np.array_equal(maxcover[k], np.arange(O)), k
     if X is not None:
         r = oracle.transform(X, kernels)
         cnt = np.rint(F[:, 0::2] * r["O"][None, :]).astype(np.int64)
@@ -163,6 +164,8 @@ def test_item_cost_and_groups():
     items = t["items"]
     G = items[:, 0] % 2 + 1
     ell = np.array(ELLS)[items[:, 0] // 2]
-    np.testing.assert_array_equal(items[:, 9], items[:, 5] * items[:, 4] * ell * G)
+    S, rounds, rounds_long = items[:, 4], items[:, 5], items[:, 12]
+    steps = rounds_long * S + (rounds - rounds_long) * (S - 1)
+    np.testing.assert_array_equal(items[:, 9], steps * ell * G)
     # a bucket is split into groups of 8 with at most one smaller group
     assert (G == 2).sum() > (G == 1).sum()
