@@ -176,16 +176,19 @@ rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *
  *   items        n_items x 16 int32, one row per work item:
  *                [variant, dilation, padding, outputs O, steps S, rounds,
  *                 lane_off, w_off, k_off, cost, n_long, n_short,
- *                 rounds_long, 0 x 3];
+ *                 rounds_long, 0, inv_O (words 14-15: 1/O as an IEEE
+ *                 double, little-endian)];
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
- *                7/9/11 taps, G kernel groups of 4 slots
+ *                7/9/11 taps, G kernel groups of 4 slots;
  *                every residue class (outputs r, r+d, ...) is split into
- *                chunks of S or S-1 outputs; the first rounds_long rounds
- *                hold the n_long chunks of S outputs, the rest the n_short
- *                chunks of S-1 outputs, 64 chunks per round
- *   lanes        lane table: per item and round, 64 entries, the output
- *                position of the lane's first step; lanes past the last
- *                chunk of a length repeat a chunk and are discarded
+ *                chunks of S or S-1 outputs, the n_long chunks of S outputs
+ *                first; each round hands the next 64 chunks to the 64 lanes;
+ *                the first rounds_long rounds run S steps, the rest S-1
+ *   lanes        lane table: per item and round, 64 entries: bits 0-23 the
+ *                output position of the lane's first step; bit 31 set: the
+ *                lane's chunk has S-1 outputs in a round of S steps (the
+ *                last step is computed and discarded); bit 30 set: the lane
+ *                has no chunk (every step is discarded)
  *   wpk          packed weights, per item [G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in
@@ -194,6 +197,8 @@ rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *
  *                order[split_begin[layout_off[i] + v*ns + s] ..
  *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..5
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
+ *   tail_pad     zeros staged after the last row of a workgroup, so that
+ *                the discarded extra steps read inside the staged memory
  */
 typedef struct {
     int64_t n_items;
@@ -215,6 +220,7 @@ typedef struct {
     int32_t halo_lo;
     int32_t halo_hi;
     int32_t row_stride;
+    int32_t tail_pad;
     void *internal;
 } rocket_plan_tables;
 

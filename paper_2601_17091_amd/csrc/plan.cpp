@@ -58,21 +58,26 @@ static Chunking split_counts(int64_t O, int64_t d, int64_t nc) {
     };
     add(C, n_big);
     add(C - 1, n_small);
+    c.rounds = ceil_div(c.n_long + c.n_short, kWave);
     c.rounds_long = ceil_div(c.n_long, kWave);
-    c.rounds_short = ceil_div(c.n_short, kWave);
     return c;
 }
 
-Chunking choose_chunking(int64_t O, int64_t d) {
+// Estimated cycles of one series for one group of 4 kernels: a step costs
+// `ell` MFMAs plus the count and max reductions and its share of the window
+// loads; a round costs its lane-table load, address and bias set-up.
+static int64_t chunking_cost(const Chunking &c, int ell) {
+    return c.steps() * (10 * ell + 30) + c.rounds * (4 * ell + 100);
+}
+
+Chunking choose_chunking(int64_t O, int64_t d, int ell) {
     const int64_t C = ceil_div(O, d);
     Chunking best;
     int64_t best_cost = -1;
     const int64_t nc_max = std::min<int64_t>(C, 4096);
     for (int64_t nc = 1; nc <= nc_max; ++nc) {
         const Chunking c = split_counts(O, d, nc);
-        const int64_t steps = c.rounds_long * c.S + c.rounds_short * (c.S - 1);
-        // steps are what costs; a small per-round charge favours fewer rounds
-        const int64_t cost = 4 * steps + c.rounds_long + c.rounds_short;
+        const int64_t cost = chunking_cost(c, ell);
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
             best = c;
@@ -81,11 +86,15 @@ Chunking choose_chunking(int64_t O, int64_t d) {
     return best;
 }
 
-// Lane table of one bucket: the long chunks fill the first rounds, the short
-// chunks the following ones, each numbered residue-fastest so neighbouring
-// lanes work on neighbouring positions.  Lanes past the last chunk of a
-// length repeat its first chunk (their results are discarded).
-static void build_lane_table(int64_t O, int64_t d, const Chunking &c, std::vector<uint32_t> &lanes) {
+// Lane table of one bucket: the long chunks, then the short ones, each
+// numbered residue-fastest so neighbouring lanes work on neighbouring
+// positions, cut into rounds of 64.  Short chunks in a round of S steps get
+// kLaneShort; lanes past the last chunk get kLaneIdle and the position of
+// the round's first chunk.  Returns how far (in floats) the discarded
+// extra step of a short chunk reads past the end of the staged row
+// (`row_end` = L + halo_hi, relative to series index 0).
+static int64_t build_lane_table(int64_t O, int64_t d, int64_t p, int ell, const Chunking &c,
+                                int64_t row_end, std::vector<uint32_t> &lanes) {
     std::vector<uint32_t> longs, shorts;
     for (int64_t k = 0; k < c.nc; ++k)
         for (int64_t r = 0; r < std::min(d, O); ++r) {
@@ -95,12 +104,27 @@ static void build_lane_table(int64_t O, int64_t d, const Chunking &c, std::vecto
             if (len <= 0) continue;
             (len == c.S ? longs : shorts).push_back((uint32_t)(r + st * d));
         }
-    auto emit = [&](const std::vector<uint32_t> &t, int64_t rounds) {
-        for (int64_t i = 0; i < rounds * kWave; ++i)
-            lanes.push_back(i < (int64_t)t.size() ? t[i] : t[0]);
-    };
-    emit(longs, c.rounds_long);
-    emit(shorts, c.rounds_short);
+    std::vector<uint32_t> all(longs);
+    all.insert(all.end(), shorts.begin(), shorts.end());
+    const int64_t n = (int64_t)all.size();
+    int64_t overflow = 0;
+    for (int64_t rd = 0; rd < c.rounds; ++rd) {
+        const bool long_round = rd < c.rounds_long;
+        for (int64_t i = rd * kWave; i < (rd + 1) * kWave; ++i) {
+            if (i >= n) {
+                lanes.push_back(all[rd * kWave] | kLaneIdle);
+            } else if (long_round && i >= (int64_t)longs.size()) {
+                lanes.push_back(all[i] | kLaneShort);
+                // the extra step sits at q + (S-1) d; its last tap reads
+                // series index q + (S-1) d - p + (ell-1) d
+                const int64_t last = (int64_t)all[i] + (c.S - 1 + ell - 1) * d - p;
+                overflow = std::max<int64_t>(overflow, last + 1 - row_end);
+            } else {
+                lanes.push_back(all[i]);
+            }
+        }
+    }
+    return overflow;
 }
 
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
@@ -133,6 +157,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             P.row_stride = (int32_t)stride;
         }
 
+        int64_t tail_pad = 0;
         for (auto &kv : buckets) {
             const int32_t len = std::get<0>(kv.first), d = std::get<1>(kv.first),
                           p = std::get<2>(kv.first);
@@ -140,9 +165,9 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             const int eidx = ell_index_for(len);
             const int ell = kEllValues[eidx];
             const int64_t O = output_length(L, len, d, p);
-            const Chunking ch = choose_chunking(O, d);
+            const Chunking ch = choose_chunking(O, d, ell);
             const int32_t S = (int32_t)ch.S;
-            const int32_t rounds = (int32_t)(ch.rounds_long + ch.rounds_short);
+            const int32_t rounds = (int32_t)ch.rounds;
             size_t pos = 0;
             bool table_built = false;
             int32_t lane_off = 0;
@@ -152,7 +177,8 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
                 if (!table_built) {
                     lane_off = (int32_t)P.lanes.size();
-                    build_lane_table(O, d, ch, P.lanes);
+                    tail_pad = std::max(tail_pad, build_lane_table(O, d, p, ell, ch,
+                                                                   (int64_t)L + halo_hi, P.lanes));
                     table_built = true;
                 }
                 ItemDesc it;
@@ -166,10 +192,11 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 it.lane_off = lane_off;
                 it.w_off = (int32_t)P.wpk.size();
                 it.k_off = (int32_t)P.kid.size();
-                it.cost = (int32_t)((ch.rounds_long * S + ch.rounds_short * (S - 1)) * ell * G);
+                it.cost = (int32_t)(ch.steps() * ell * G);
                 it.n_long = (int32_t)ch.n_long;
                 it.n_short = (int32_t)ch.n_short;
                 it.rounds_long = (int32_t)ch.rounds_long;
+                it.inv_O = 1.0 / (double)O;
                 // A-operand weights: [g][j][slot i]; zeros for empty slots and
                 // for taps past the kernel's own length
                 for (int g = 0; g < G; ++g)
@@ -195,6 +222,8 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 pos += take;
             }
         }
+
+        P.tail_pad = P.row_stride > 0 ? (int32_t)tail_pad : 0;
 
         // item orders: per variant, largest cost first (longest-processing-
         // time first), dealt to splits greedily by accumulated cost
@@ -267,6 +296,7 @@ extern "C" rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32
     out->halo_lo = P->halo_lo;
     out->halo_hi = P->halo_hi;
     out->row_stride = P->row_stride;
+    out->tail_pad = P->tail_pad;
     out->internal = P;
     return ROCKET_OK;
 }

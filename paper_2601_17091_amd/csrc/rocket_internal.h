@@ -26,31 +26,39 @@ constexpr int kMaxGroups = 2;  // a work item holds 4 or 8 kernels of one bucket
 // One work item: up to 4*G kernels that share (length, dilation, padding).
 // The 64 lanes of a wavefront each own a chunk of consecutive outputs along
 // one dilation residue class (positions q, q+d, q+2d, ...).  Each residue
-// class is split into nc chunks of balanced length, S or S-1 outputs, and a
-// "round" gathers 64 chunks of one length: first the rounds of S-step
-// chunks, then those of (S-1)-step chunks.  Every output is computed by
-// exactly one lane; in the last round of each length the lanes without a
-// chunk start from -inf and contribute nothing.
+// class is split into nc chunks of balanced length, S or S-1 outputs.  A
+// "round" hands 64 chunks to the 64 lanes and runs a fixed number of steps
+// for all of them: the chunks of S outputs come first, so the first
+// rounds_long rounds run S steps and the rest S-1.  In a round of S steps a
+// lane holding an (S-1)-output chunk computes one extra output past its
+// chunk, and a lane without a chunk computes junk; both start those
+// accumulations from -inf (lane-table flags), so they change neither the
+// count nor the max.  Every real output is computed by exactly one lane.
 struct alignas(16) ItemDesc {
     int32_t variant;      // ell_index * 2 + (G - 1)
     int32_t d;            // dilation
     int32_t p;            // padding
     int32_t O;            // number of dot products (outputs)
     int32_t S;            // steps of a long chunk (short chunks: S - 1)
-    int32_t rounds;       // rounds per series (long, then short)
+    int32_t rounds;       // rounds per series
     int32_t lane_off;     // first lane-table entry (rounds * 64 entries)
     int32_t w_off;        // first packed weight: [G][ell][4] floats
     int32_t k_off;        // first slot entry: kernel ids and biases, [4G]
     int32_t cost;         // MFMA instructions per series (scheduling weight)
     int32_t n_long;       // chunks of S outputs
     int32_t n_short;      // chunks of S - 1 outputs
-    int32_t rounds_long;  // rounds of long chunks: ceil(n_long / 64)
-    int32_t reserved[3];
+    int32_t rounds_long;  // rounds that run S steps: ceil(n_long / 64)
+    int32_t reserved;
+    double inv_O;         // 1 / O rounded to double (exact PPV, see transform.hip)
 };
 static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
 
-// Lane-table entry: the output position of the lane's first step.
+// Lane-table entry: the output position of the lane's first step (below
+// 2^24) and two flags.
 constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
+constexpr uint32_t kLanePosMask = 0x00FFFFFFu;
+constexpr uint32_t kLaneShort = 1u << 31;  // chunk is one output short: last step discarded
+constexpr uint32_t kLaneIdle = 1u << 30;   // no chunk: every step discarded
 
 // Item orders for a few split counts.  Within a layout with `nsplit` splits
 // the items are grouped by variant, so that every workgroup runs one code
@@ -66,6 +74,7 @@ struct HostPlan {
     int32_t halo_lo = 0;   // zeros staged before the series in LDS
     int32_t halo_hi = 0;   // zeros staged after the series in LDS
     int32_t row_stride = 0;  // floats per staged row
+    int32_t tail_pad = 0;    // zeros staged after the last row (reads of discarded steps)
     int64_t n_buckets = 0;
     int64_t mfma_per_row = 0;
     std::vector<ItemDesc> items;
@@ -85,11 +94,13 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L);
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out);
 
 // Chunking of one bucket: nc chunks per residue class, chunk lengths S and
-// S-1, with n_long / n_short chunks of each, chosen to minimise the MFMA
-// steps one series costs.
+// S-1, with n_long / n_short chunks of each; rounds of 64 chunks, the first
+// rounds_long of them running S steps.  Chosen to minimise an estimate of
+// the cycles one series costs (MFMA steps, reductions, round set-up).
 struct Chunking {
-    int64_t nc = 1, S = 1, n_long = 0, n_short = 0, rounds_long = 0, rounds_short = 0;
+    int64_t nc = 1, S = 1, n_long = 0, n_short = 0, rounds = 0, rounds_long = 0;
+    int64_t steps() const { return rounds_long * S + (rounds - rounds_long) * (S - 1); }
 };
-Chunking choose_chunking(int64_t O, int64_t d);
+Chunking choose_chunking(int64_t O, int64_t d, int ell);
 
 }  // namespace rocket

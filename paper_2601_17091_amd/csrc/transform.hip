@@ -71,6 +71,7 @@ struct FusedArgs {
     int64_t tiles_per_xcd;       // row tiles (of rows_per_block series) per XCD
     int32_t halo_lo;
     int32_t row_stride;
+    int32_t tail_pad;        // zero floats staged after the last row
     int32_t rows_per_block;  // series staged together in one workgroup's LDS
 };
 
@@ -85,14 +86,16 @@ constexpr int kDppRowMirror = 0x140;
 // (NS + ELL - 1 values spaced d apart, starting at xs) is read from LDS
 // first; then tap j of every step and kernel group is issued before tap j+1,
 // so the wavefront keeps NS*G independent MFMA accumulation chains in
-// flight, each starting from binit: the slots' biases, or -inf on lanes
-// without a chunk.  Every other lane computes real outputs only, so MAX
-// folds all results (v_max3 over pairs of steps) and the positive count is
-// a ballot of y > 0 popcounted on the scalar unit.
-template <int ELL, int G, int NS>
+// flight.  Each chain starts from binit (the slots' biases, or -inf on a
+// lane without a chunk); when LAST is set the block ends the round and its
+// final step starts from blast instead (also -inf on a lane whose chunk is
+// one output short).  A chain started at -inf stays -inf, so MAX folds every
+// result (v_max3 over pairs of steps) and the positive count is a ballot of
+// y > 0 popcounted on the scalar unit.
+template <int ELL, int G, int NS, bool LAST>
 __device__ __forceinline__ void step_block(const float *xs, int d, const float (&wa)[G][ELL],
-                                           const v4f (&binit)[G], v4f (&mx)[G],
-                                           uint32_t (&cnt)[G][4]) {
+                                           const v4f (&binit)[G], const v4f (&blast)[G],
+                                           v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
     float xw[NS + ELL - 1];
 #pragma unroll
     for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = xs[m * d];
@@ -101,7 +104,9 @@ __device__ __forceinline__ void step_block(const float *xs, int d, const float (
     for (int u = 0; u < NS; ++u)
 #pragma unroll
         for (int g = 0; g < G; ++g)
-            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], binit[g], 0, 0, 0);
+            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u],
+                                                          (LAST && u == NS - 1) ? blast[g] : binit[g],
+                                                          0, 0, 0);
 #pragma unroll
     for (int j = 1; j < ELL; ++j)
 #pragma unroll
@@ -136,18 +141,19 @@ template <int ELL, int G, int N>
 struct TailBlock {
     __device__ __forceinline__ static void run(int nv, const float *xs, int d,
                                                const float (&wa)[G][ELL], const v4f (&binit)[G],
-                                               v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+                                               const v4f (&blast)[G], v4f (&mx)[G],
+                                               uint32_t (&cnt)[G][4]) {
         if (nv == N)
-            step_block<ELL, G, N>(xs, d, wa, binit, mx, cnt);
+            step_block<ELL, G, N, true>(xs, d, wa, binit, blast, mx, cnt);
         else
-            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, mx, cnt);
+            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, blast, mx, cnt);
     }
 };
 
 template <int ELL, int G>
 struct TailBlock<ELL, G, 0> {
     __device__ __forceinline__ static void run(int, const float *, int, const float (&)[G][ELL],
-                                               const v4f (&)[G], v4f (&)[G],
+                                               const v4f (&)[G], const v4f (&)[G], v4f (&)[G],
                                                uint32_t (&)[G][4]) {}
 };
 
@@ -221,7 +227,8 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
     for (int g = 0; g < G; ++g)
         out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
-    const float den = (float)it.O;
+    // the lane-table entry of round 0, shared by every series
+    const uint32_t e0 = a.lanes[it.lane_off + lane];
     for (int r = 0; r < nrows; ++r) {
         v4f mx[G];
         uint32_t cnt[G][4];
@@ -234,30 +241,35 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         // xb[q + m*d] is the zero-padded series value under tap m of output q
         const float *xb = rows0 + r * a.row_stride - it.p;
         for (int rd = 0; rd < it.rounds; ++rd) {
-            // rounds of S-output chunks first, then of (S-1)-output chunks
-            const bool is_long = rd < it.rounds_long;
-            const int len = is_long ? it.S : it.S - 1;
-            const int active = is_long ? min(rocket::kWave, it.n_long - rd * rocket::kWave)
-                                       : min(rocket::kWave, it.n_short - (rd - it.rounds_long) * rocket::kWave);
-            v4f binit[G];
-            if (active == rocket::kWave) {
+            // rounds of S steps first, then of S-1 steps
+            const int len = rd < it.rounds_long ? it.S : it.S - 1;
+            const uint32_t e = rd == 0 ? e0 : a.lanes[it.lane_off + rd * rocket::kWave + lane];
+            v4f binit[G], blast[G];
+            if (__builtin_amdgcn_ballot_w64((e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0) == 0) {
 #pragma unroll
-                for (int g = 0; g < G; ++g) binit[g] = bias[g];
+                for (int g = 0; g < G; ++g) {
+                    binit[g] = bias[g];
+                    blast[g] = bias[g];
+                }
             } else {
-                const bool own = lane < active;
+                const bool idle = (e & rocket::kLaneIdle) != 0;
+                const bool drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
 #pragma unroll
                 for (int g = 0; g < G; ++g)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) binit[g][v] = own ? bias[g][v] : -INFINITY;
+                    for (int v = 0; v < 4; ++v) {
+                        binit[g][v] = idle ? -INFINITY : bias[g][v];
+                        blast[g][v] = drop_last ? -INFINITY : bias[g][v];
+                    }
             }
-            const float *xs = xb + a.lanes[it.lane_off + rd * rocket::kWave + lane];
+            const float *xs = xb + (e & rocket::kLanePosMask);
             const int nfull = (len - 1) / T;  // full blocks before the last block
             const int nv = len - nfull * T;   // length of the last block, 1..T
             for (int blk = 0; blk < nfull; ++blk) {
-                step_block<ELL, G, T>(xs, d, wa, binit, mx, cnt);
+                step_block<ELL, G, T, false>(xs, d, wa, binit, blast, mx, cnt);
                 xs += T * d;
             }
-            TailBlock<ELL, G, T>::run(nv, xs, d, wa, binit, mx, cnt);
+            TailBlock<ELL, G, T>::run(nv, xs, d, wa, binit, blast, mx, cnt);
         }
         // MAX over the wavefront; counts are already scalar
 #pragma unroll
@@ -275,8 +287,13 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
             c = lane >= 32 ? c1 : c;
             c = lane >= 48 ? c3 : c;
             if (out_kernel[g] >= 0) {
+                // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
+                // quotient is never a float midpoint and lies at least 2^-49
+                // (relative) from one, while c * fl64(1/O) is within 2^-52 of
+                // it, so rounding the double product to float gives the same
+                // float as the fp32 division
                 float2 res;
-                res.x = (float)c / den;
+                res.x = (float)((double)c * it.inv_O);
                 res.y = m;
                 *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K + 2 * (int64_t)out_kernel[g]) = res;
             }
@@ -299,6 +316,7 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
     it.n_long = p->n_long;
     it.n_short = p->n_short;
     it.rounds_long = p->rounds_long;
+    it.inv_O = p->inv_O;
     return it;
 }
 
@@ -351,6 +369,9 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
             dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
         }
     }
+    // zeros after the last row: discarded extra steps may read up to
+    // tail_pad floats past it
+    for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[nrows * a.row_stride + e] = 0.0f;
     if (threadIdx.x == 0) next_item = 0;
     __syncthreads();
 
@@ -433,7 +454,8 @@ struct rocket_plan {
     int device = 0;
     int n_cu = 0;
     bool direct = false;
-    int64_t lds_bytes = 0;
+    int rows_per_block = 1;  // series staged per workgroup
+    int64_t lds_bytes = 0;   // per workgroup: the rows plus the tail pad
     ItemDesc *d_items = nullptr;
     uint32_t *d_lanes = nullptr;
     float *d_wpk = nullptr;
@@ -485,7 +507,13 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         return ROCKET_ERR_HIP;
     }
     p->n_cu = prop.multiProcessorCount;
-    const int64_t lds = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
+    // rows per workgroup: as many as fit the LDS budget (at least one)
+    const int64_t row_bytes = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
+    const int64_t pad_bytes = (int64_t)p->host.tail_pad * (int64_t)sizeof(float);
+    if (row_bytes > 0)
+        p->rows_per_block = (int)std::max<int64_t>(
+            1, std::min<int64_t>(kMaxRowsPerBlock, (kRowsLdsBudget - pad_bytes) / row_bytes));
+    const int64_t lds = p->rows_per_block * row_bytes + pad_bytes;
     p->direct = (flags & ROCKET_PLAN_DIRECT) || p->host.row_stride == 0 ||
                 lds > (int64_t)prop.sharedMemPerBlock;
     p->lds_bytes = p->direct ? 0 : lds;
@@ -506,6 +534,9 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
         if (e == hipSuccess && lds > 64 * 1024)
             e = hipFuncSetAttribute((const void *)rocket_fused_kernel<kBigBlock>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e == hipSuccess && lds > 64 * 1024)
+            e = hipFuncSetAttribute((const void *)rocket_fused_kernel<kBlock>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     }
     if (e != hipSuccess) {
@@ -565,7 +596,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     // items of a series across workgroups when there are few series
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
     const int64_t row_bytes = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
-    const int R = (int)std::max<int64_t>(1, std::min<int64_t>(kMaxRowsPerBlock, kRowsLdsBudget / row_bytes));
+    const int R = p->rows_per_block;
     const int64_t tiles = (n + R - 1) / R;
     int li = 0;
     while (li + 1 < rocket::kNumSplitLayouts && tiles * rocket::kSplitCounts[li] < target) ++li;
@@ -590,6 +621,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     }
     a.halo_lo = p->host.halo_lo;
     a.row_stride = p->host.row_stride;
+    a.tail_pad = p->host.tail_pad;
     a.rows_per_block = R;
     const int64_t max_rows =
         ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1)) / kXcds - 1) * kXcds * R;
@@ -599,7 +631,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         const int64_t tiles_now = (a.n_rows + R - 1) / R;
         a.tiles_per_xcd = (tiles_now + kXcds - 1) / kXcds;
         const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
-        const size_t lds = (size_t)(R * row_bytes);
+        const size_t lds = (size_t)p->lds_bytes;
         if (row_bytes > kBigLds)
             hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock), lds, s, a);
         else

@@ -72,7 +72,7 @@ class CPlanTables(ctypes.Structure):
         ("n_layouts", ctypes.c_int32), ("layout_off", ctypes.POINTER(ctypes.c_int32)),
         ("split_counts", ctypes.POINTER(ctypes.c_int32)),
         ("halo_lo", ctypes.c_int32), ("halo_hi", ctypes.c_int32), ("row_stride", ctypes.c_int32),
-        ("internal", ctypes.c_void_p),
+        ("tail_pad", ctypes.c_int32), ("internal", ctypes.c_void_p),
     ]
 
 
@@ -187,6 +187,7 @@ def plan_tables(kernels: dict, L: int) -> dict:
             layout_off=arr(t.layout_off, t.n_layouts),
             split_counts=arr(t.split_counts, t.n_layouts),
             halo_lo=t.halo_lo, halo_hi=t.halo_hi, row_stride=t.row_stride,
+            tail_pad=t.tail_pad,
         )
     finally:
         lib.rocket_plan_tables_free(ctypes.byref(t))

@@ -2,14 +2,16 @@
 
 The planner's tables (work items, lane tables, packed weights, item orders)
 are read back through rocket_plan_tables_build and walked here exactly the
-way the GPU kernel walks them: in every round each active lane takes the
-output positions q0, q0+d, ... (S or S-1 of them, by round) and loads the
-series values at halo_lo - p + q + j*d from the zero-margined row; lanes
-past the round's chunk count are discarded.  The checks: every position an
-active lane computes is a real output, every output of every kernel is
-computed exactly once, every load (idle lanes included) stays inside the
-staged row, the packed weights are the kernels' own, and an fp32 replay of
-the walk lands inside the oracle's certified bounds.
+way the GPU kernel walks them: every round runs S steps (the first
+rounds_long rounds) or S-1 steps for all 64 lanes; an active lane takes the
+output positions q0, q0+d, ... and loads the series values at
+halo_lo - p + q + j*d from the zero-margined row; a lane flagged "short"
+discards its last step and an idle lane discards every step (both start
+those accumulations from -inf on the GPU).  The checks: every position a
+lane keeps is a real output, every output of every kernel is kept exactly
+once, every load stays inside the staged row (discarded steps: inside the
+row plus the tail pad), the packed weights are the kernels' own, and an
+fp32 replay of the walk lands inside the oracle's certified bounds.
 """
 import numpy as np
 import pytest
@@ -18,15 +20,26 @@ import paper_2601_17091_amd as rk
 from _util import kernel_set
 
 ELLS = (7, 9, 11)
+POS_MASK = 0x00FFFFFF
+SHORT = 1 << 31
+IDLE = 1 << 30
+
+
+def item_fields(row):
+    (variant, d, p, O, S, rounds, lane_off, w_off, k_off, cost, n_long, n_short,
+     rounds_long) = (int(v) for v in row[:13])
+    inv_O = row[14:16].astype(np.int32).view(np.float64)[0]
+    return dict(variant=variant, d=d, p=p, O=O, S=S, rounds=rounds, lane_off=lane_off,
+                w_off=w_off, k_off=k_off, cost=cost, n_long=n_long, n_short=n_short,
+                rounds_long=rounds_long, inv_O=inv_O)
 
 
 def walk(tables, kernels, L, X=None):
     """Replay the fused kernel's schedule; returns per-kernel coverage and,
     if X is given, fp32 features [n, 2K]."""
     K = len(kernels["length"])
-    items = tables["items"]
     lanes = tables["lanes"].astype(np.int64)
-    halo_lo, stride = tables["halo_lo"], tables["row_stride"]
+    halo_lo, stride, pad = tables["halo_lo"], tables["row_stride"], tables["tail_pad"]
     cover = [np.zeros(0, np.int64)] * K
     F = None
     if X is not None:
@@ -34,15 +47,14 @@ def walk(tables, kernels, L, X=None):
         F = np.full((n, 2 * K), np.nan, dtype=np.float64)
         rows = np.zeros((n, stride), dtype=np.float32)
         rows[:, halo_lo:halo_lo + L] = X
-    for it in items:
-        (variant, d, p, O, S, rounds, lane_off, w_off, k_off, cost, n_long, n_short,
-         rounds_long) = (int(v) for v in it[:13])
-        ell = ELLS[variant // 2]
-        G = variant % 2 + 1
+    for row in tables["items"]:
+        f = item_fields(row)
+        d, p, O, S, ell = f["d"], f["p"], f["O"], f["S"], ELLS[f["variant"] // 2]
+        G = f["variant"] % 2 + 1
         nslot = 4 * G
-        kid = tables["slot_kernel"][k_off:k_off + nslot]
-        bias = tables["slot_bias"][k_off:k_off + nslot]
-        W = tables["wpk"][w_off:w_off + G * ell * 4].reshape(G, ell, 4)
+        kid = tables["slot_kernel"][f["k_off"]:f["k_off"] + nslot]
+        bias = tables["slot_bias"][f["k_off"]:f["k_off"] + nslot]
+        W = tables["wpk"][f["w_off"]:f["w_off"] + G * ell * 4].reshape(G, ell, 4)
         Wslot = np.concatenate([W[g].T for g in range(G)], axis=0)  # [slot, tap]
         for s_, k in enumerate(kid):
             if k >= 0:
@@ -53,32 +65,50 @@ def walk(tables, kernels, L, X=None):
                 assert (int(kernels["dilation"][k]), int(kernels["padding"][k])) == (d, p)
             else:
                 assert np.all(Wslot[s_] == 0)
-        assert rounds == rounds_long + -(-n_short // 64) and rounds_long == -(-n_long // 64)
-        assert cost == (rounds_long * S + (rounds - rounds_long) * (S - 1)) * ell * G
-        counted = []
+        n_chunks = f["n_long"] + f["n_short"]
+        assert f["rounds"] == -(-n_chunks // 64) and f["rounds_long"] == -(-f["n_long"] // 64)
+        steps = f["rounds_long"] * S + (f["rounds"] - f["rounds_long"]) * (S - 1)
+        assert f["cost"] == steps * ell * G
+        assert f["inv_O"] == 1.0 / O
+        kept = []
         ys = [] if X is not None else None
-        for rd in range(rounds):
-            is_long = rd < rounds_long
-            length = S if is_long else S - 1
-            active = min(64, n_long - 64 * rd) if is_long else min(64, n_short - 64 * (rd - rounds_long))
-            assert length >= 1 and active >= 1
-            q0 = lanes[lane_off + 64 * rd:lane_off + 64 * rd + 64]
-            q = q0[:, None] + np.arange(length)[None, :] * d        # [lane, step]
-            # every lane's loads stay in the staged row, idle lanes included
+        for rd in range(f["rounds"]):
+            length = S if rd < f["rounds_long"] else S - 1
+            assert length >= 1
+            e = lanes[f["lane_off"] + 64 * rd:f["lane_off"] + 64 * rd + 64]
+            q0 = e & POS_MASK
+            short = (e & SHORT) != 0
+            idle = (e & IDLE) != 0
+            # flags: short chunks only in rounds of S steps, idle lanes only
+            # past the last chunk
+            assert not np.any(short & idle)
+            if length == S - 1:
+                assert not short.any()
+            assert np.array_equal(idle, np.arange(64) + 64 * rd >= n_chunks)
+            # every load of every lane and step, discarded ones included
             m = np.arange(length + ell - 1)
             idx = halo_lo - p + q0[:, None] + m[None, :] * d
-            assert idx.min() >= 0 and idx.max() < stride, (d, p, O, S)
-            qa = q[:active]
-            assert qa.min() >= 0 and qa.max() < O                    # real outputs only
-            counted.append(qa.ravel())
+            assert idx.min() >= 0 and idx.max() < stride + pad, (d, p, O, S)
+            # steps each lane keeps
+            keep_steps = np.where(idle, 0, np.where(short, length - 1, length))
+            for lane in range(64):
+                ks_ = keep_steps[lane]
+                if ks_ == 0:
+                    continue
+                q = q0[lane] + np.arange(ks_) * d
+                assert q.min() >= 0 and q.max() < O                  # real outputs only
+                last_idx = halo_lo - p + q.max() + (ell - 1) * d
+                assert last_idx < stride                              # kept steps read the row
+                kept.append(q)
             if X is not None:
-                tap_idx = halo_lo - p + qa[..., None] + np.arange(ell)[None, None, :] * d
-                xv = rows[:, tap_idx]                                # [n, lane, step, tap]
-                acc = np.broadcast_to(bias.astype(np.float32), xv.shape[:3] + (nslot,)).copy()
+                qa = np.concatenate([q0[l] + np.arange(keep_steps[l]) * d for l in range(64)])
+                tap_idx = halo_lo - p + qa[:, None] + np.arange(ell)[None, :] * d
+                xv = rows[:, tap_idx]                                 # [n, output, tap]
+                acc = np.broadcast_to(bias.astype(np.float32), xv.shape[:2] + (nslot,)).copy()
                 for j in range(ell):
-                    acc = (acc + xv[..., j, None] * Wslot[None, None, None, :, j]).astype(np.float32)
-                ys.append(acc.reshape(acc.shape[0], -1, nslot))
-        allq = np.concatenate(counted)
+                    acc = (acc + xv[..., j, None] * Wslot[None, None, :, j]).astype(np.float32)
+                ys.append(acc)
+        allq = np.concatenate(kept)
         for k in kid[kid >= 0]:
             cover[k] = np.bincount(allq, minlength=O)
         if X is not None:
@@ -169,3 +199,28 @@ def test_item_cost_and_groups():
     np.testing.assert_array_equal(items[:, 9], steps * ell * G)
     # a bucket is split into groups of 8 with at most one smaller group
     assert (G == 2).sum() > (G == 1).sum()
+    # small dilations need one round of long chunks per series
+    d = items[:, 1]
+    assert np.all(rounds[d == 1] == 1)
+    # MFMA work issued stays within 20% of the nominal taps x outputs
+    nominal = (ks["length"] * (1000 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
+    assert items[:, 9].sum() * 256 < 1.2 * nominal
+
+
+def test_ppv_through_double_reciprocal():
+    """The kernel writes PPV as (float)(c * fl64(1/O)); for 0 <= c <= O < 2^24
+    that equals the correctly rounded fp32 quotient (float)c / (float)O.
+    Exhaustive for O < 1200, then random (c, O) pairs up to 2^24 - 1."""
+    rng = np.random.default_rng(5)
+    cs = []
+    for O in range(1, 1200):
+        cs.append(np.arange(O + 1))
+    O_all = np.concatenate([np.full(O + 1, O) for O in range(1, 1200)])
+    c_all = np.concatenate(cs)
+    O_r = rng.integers(1, 1 << 24, size=2_000_000)
+    c_r = (rng.random(O_r.shape[0]) * (O_r + 1)).astype(np.int64)
+    O_all = np.concatenate([O_all, O_r, np.full(4, (1 << 24) - 1)])
+    c_all = np.concatenate([c_all, c_r, [1, 2, (1 << 23), (1 << 24) - 2]])
+    want = c_all.astype(np.float32) / O_all.astype(np.float32)
+    got = (c_all.astype(np.float64) * (1.0 / O_all.astype(np.float64))).astype(np.float32)
+    assert np.array_equal(want, got)
