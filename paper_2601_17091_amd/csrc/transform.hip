@@ -159,8 +159,9 @@ struct TailBlock<ELL, G, 0> {
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_max_row(float v) {
-    const int moved = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF,
-                                                  0xF, false);
+    // every lane of a full row reads a valid lane for these controls, so the
+    // move can fold into v_max_f32's DPP source
+    const int moved = __builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true);
     return fmaxf(v, __int_as_float(moved));
 }
 
@@ -227,75 +228,94 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
     for (int g = 0; g < G; ++g)
         out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
-    // the lane-table entry of round 0, shared by every series
-    const uint32_t e0 = a.lanes[it.lane_off + lane];
-    for (int r = 0; r < nrows; ++r) {
-        v4f mx[G];
-        uint32_t cnt[G][4];
+    // Items with one round (small dilations) share the round's lane entry,
+    // start values and step count across all series: the rows then loop
+    // inside the round.  Items with several rounds loop rounds inside rows.
+    const bool single = it.rounds == 1;
+    const int n_outer = single ? 1 : nrows;
+    const int n_inner = single ? nrows : it.rounds;
+    v4f binit[G], blast[G];
+    uint32_t pos = 0;
+    int len = 0;
+    v4f mx[G];
+    uint32_t cnt[G][4];
+    for (int o = 0; o < n_outer; ++o) {
+        for (int i = 0; i < n_inner; ++i) {
+            const int r = single ? i : o;
+            const int rd = single ? 0 : i;
+            if (single ? i == 0 : true) {
+                // round set-up: rounds of S steps first, then of S-1 steps
+                len = rd < it.rounds_long ? it.S : it.S - 1;
+                const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
+                pos = e & rocket::kLanePosMask;
+                if (__builtin_amdgcn_ballot_w64((e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0) == 0) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+                    for (int g = 0; g < G; ++g) {
+                        binit[g] = bias[g];
+                        blast[g] = bias[g];
+                    }
+                } else {
+                    const bool idle = (e & rocket::kLaneIdle) != 0;
+                    const bool drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
-        }
-        // xb[q + m*d] is the zero-padded series value under tap m of output q
-        const float *xb = rows0 + r * a.row_stride - it.p;
-        for (int rd = 0; rd < it.rounds; ++rd) {
-            // rounds of S steps first, then of S-1 steps
-            const int len = rd < it.rounds_long ? it.S : it.S - 1;
-            const uint32_t e = rd == 0 ? e0 : a.lanes[it.lane_off + rd * rocket::kWave + lane];
-            v4f binit[G], blast[G];
-            if (__builtin_amdgcn_ballot_w64((e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0) == 0) {
+                    for (int g = 0; g < G; ++g)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            binit[g][v] = idle ? -INFINITY : bias[g][v];
+                            blast[g][v] = drop_last ? -INFINITY : bias[g][v];
+                        }
+                }
+            }
+            if (single ? true : i == 0) {
 #pragma unroll
                 for (int g = 0; g < G; ++g) {
-                    binit[g] = bias[g];
-                    blast[g] = bias[g];
+                    mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
                 }
-            } else {
-                const bool idle = (e & rocket::kLaneIdle) != 0;
-                const bool drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
-#pragma unroll
-                for (int g = 0; g < G; ++g)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        binit[g][v] = idle ? -INFINITY : bias[g][v];
-                        blast[g][v] = drop_last ? -INFINITY : bias[g][v];
-                    }
             }
-            const float *xs = xb + (e & rocket::kLanePosMask);
+            // xs[m*d] is the zero-padded series value under tap m of the
+            // lane's step-0 output
+            const float *xs = rows0 + r * a.row_stride - it.p + pos;
             const int nfull = (len - 1) / T;  // full blocks before the last block
             const int nv = len - nfull * T;   // length of the last block, 1..T
+            // block b reads xs[b*T*d + m*d]: one lane address plus a
+            // wavefront-uniform offset per load
             for (int blk = 0; blk < nfull; ++blk) {
-                step_block<ELL, G, T, false>(xs, d, wa, binit, blast, mx, cnt);
-                xs += T * d;
+                const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
+                step_block<ELL, G, T, false>(xs + off, d, wa, binit, blast, mx, cnt);
             }
-            TailBlock<ELL, G, T>::run(nv, xs, d, wa, binit, blast, mx, cnt);
-        }
-        // MAX over the wavefront; counts are already scalar
+            TailBlock<ELL, G, T>::run(nv, xs + __builtin_amdgcn_readfirstlane(nfull * T * d), d, wa,
+                                      binit, blast, mx, cnt);
+            if (single ? true : i == n_inner - 1) {
+                // MAX over the wavefront; counts are already scalar
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float m = reduce4(mx[g]);
-            // the count of slot slot_of_row(q) for the lanes of row q
-            // (readfirstlane keeps the four uniform counts independent scalars,
-            // so the selects stay selects instead of an indexed array)
-            const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
-            const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
-            const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
-            const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
-            uint32_t c = c0;
-            c = lane >= 16 ? c2 : c;
-            c = lane >= 32 ? c1 : c;
-            c = lane >= 48 ? c3 : c;
-            if (out_kernel[g] >= 0) {
-                // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
-                // quotient is never a float midpoint and lies at least 2^-49
-                // (relative) from one, while c * fl64(1/O) is within 2^-52 of
-                // it, so rounding the double product to float gives the same
-                // float as the fp32 division
-                float2 res;
-                res.x = (float)((double)c * it.inv_O);
-                res.y = m;
-                *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K + 2 * (int64_t)out_kernel[g]) = res;
+                for (int g = 0; g < G; ++g) {
+                    const float m = reduce4(mx[g]);
+                    // the count of slot slot_of_row(q) for the lanes of row q
+                    // (readfirstlane keeps the four uniform counts independent
+                    // scalars, so the selects stay selects)
+                    const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
+                    const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
+                    const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
+                    const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
+                    uint32_t c = c0;
+                    c = lane >= 16 ? c2 : c;
+                    c = lane >= 32 ? c1 : c;
+                    c = lane >= 48 ? c3 : c;
+                    if (out_kernel[g] >= 0) {
+                        // (float)c / (float)O, correctly rounded: for c <= O < 2^24
+                        // the quotient is never a float midpoint and lies at
+                        // least 2^-49 (relative) from one, while c * fl64(1/O)
+                        // is within 2^-52 of it, so rounding the double product
+                        // to float gives the same float as the fp32 division
+                        float2 res;
+                        res.x = (float)((double)c * it.inv_O);
+                        res.y = m;
+                        *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K +
+                                                    2 * (int64_t)out_kernel[g]) = res;
+                    }
+                }
             }
         }
     }
