@@ -47,7 +47,7 @@ namespace {
 constexpr int kBlock = 256;       // 4 wavefronts per workgroup
 constexpr int kBigBlock = 1024;   // 16 wavefronts share one large staged row
 constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
-constexpr int64_t kRowsLdsBudget = 40 * 1024;  // LDS for the series of one workgroup
+constexpr int64_t kRowsLdsBudget = 30 * 1024;  // LDS for the series of one workgroup (5 per CU)
 constexpr int kMaxRowsPerBlock = 8;
 constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dealt round-robin
 
@@ -88,13 +88,13 @@ constexpr int kDppRowMirror = 0x140;
 // so the wavefront keeps NS*G independent MFMA accumulation chains in
 // flight.  Each chain starts from binit (the slots' biases, or -inf on a
 // lane without a chunk); when LAST is set the block ends the round and its
-// final step starts from blast instead (also -inf on a lane whose chunk is
-// one output short).  A chain started at -inf stays -inf, so MAX folds every
+// final step starts from -inf on lanes with drop_last set (a chunk one
+// output short, or no chunk).  A chain started at -inf stays -inf, so MAX folds every
 // result (v_max3 over pairs of steps) and the positive count is a ballot of
 // y > 0 popcounted on the scalar unit.
 template <int ELL, int G, int NS, bool LAST>
 __device__ __forceinline__ void step_block(const float *xs, int d, const float (&wa)[G][ELL],
-                                           const v4f (&binit)[G], const v4f (&blast)[G],
+                                           const v4f (&binit)[G], bool drop_last,
                                            v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
     float xw[NS + ELL - 1];
 #pragma unroll
@@ -104,9 +104,14 @@ __device__ __forceinline__ void step_block(const float *xs, int d, const float (
     for (int u = 0; u < NS; ++u)
 #pragma unroll
         for (int g = 0; g < G; ++g)
-            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u],
-                                                          (LAST && u == NS - 1) ? blast[g] : binit[g],
-                                                          0, 0, 0);
+        {
+            v4f c = binit[g];
+            if (LAST && u == NS - 1) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
+            }
+            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], c, 0, 0, 0);
+        }
 #pragma unroll
     for (int j = 1; j < ELL; ++j)
 #pragma unroll
@@ -141,19 +146,19 @@ template <int ELL, int G, int N>
 struct TailBlock {
     __device__ __forceinline__ static void run(int nv, const float *xs, int d,
                                                const float (&wa)[G][ELL], const v4f (&binit)[G],
-                                               const v4f (&blast)[G], v4f (&mx)[G],
+                                               bool drop_last, v4f (&mx)[G],
                                                uint32_t (&cnt)[G][4]) {
         if (nv == N)
-            step_block<ELL, G, N, true>(xs, d, wa, binit, blast, mx, cnt);
+            step_block<ELL, G, N, true>(xs, d, wa, binit, drop_last, mx, cnt);
         else
-            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, blast, mx, cnt);
+            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, drop_last, mx, cnt);
     }
 };
 
 template <int ELL, int G>
 struct TailBlock<ELL, G, 0> {
     __device__ __forceinline__ static void run(int, const float *, int, const float (&)[G][ELL],
-                                               const v4f (&)[G], const v4f (&)[G], v4f (&)[G],
+                                               const v4f (&)[G], bool, v4f (&)[G],
                                                uint32_t (&)[G][4]) {}
 };
 
@@ -201,13 +206,103 @@ __device__ __forceinline__ float reduce4(const v4f &m) {
 // row 3 slot 3.
 __device__ __forceinline__ int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
 
+// Lane state of one round: where the lane's chunk starts, the start values
+// of its accumulations, and whether its last step is discarded.
+template <int G>
+struct RoundState {
+    v4f binit[G];
+    uint32_t pos;
+    int len;
+    bool drop_last;
+};
+
+template <int G>
+__device__ __forceinline__ void setup_round(const ItemDesc &it, int rd, const FusedArgs &a,
+                                            const float (&bias)[G][4], int lane,
+                                            RoundState<G> &st) {
+    // rounds of S steps first, then of S-1 steps
+    st.len = rd < it.rounds_long ? it.S : it.S - 1;
+    const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
+    st.pos = e & rocket::kLanePosMask;
+    const bool idle = (e & rocket::kLaneIdle) != 0;
+    st.drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) st.binit[g][v] = idle ? -INFINITY : bias[g][v];
+}
+
+// All steps of one round for one series; xs[m*d] is the zero-padded series
+// value under tap m of the lane's step-0 output.
+template <int ELL, int G, int T>
+__device__ __forceinline__ void run_round(const float *xs, int d, const RoundState<G> &st,
+                                          const float (&wa)[G][ELL], v4f (&mx)[G],
+                                          uint32_t (&cnt)[G][4]) {
+    const int nfull = (st.len - 1) / T;  // full blocks before the last block
+    const int nv = st.len - nfull * T;   // length of the last block, 1..T
+    // block b reads xs[b*T*d + m*d]: one lane address plus a
+    // wavefront-uniform offset per load
+    for (int blk = 0; blk < nfull; ++blk) {
+        const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
+        step_block<ELL, G, T, false>(xs + off, d, wa, st.binit, st.drop_last, mx, cnt);
+    }
+    TailBlock<ELL, G, T>::run(nv, xs + __builtin_amdgcn_readfirstlane(nfull * T * d), d, wa,
+                              st.binit, st.drop_last, mx, cnt);
+}
+
+template <int G>
+__device__ __forceinline__ void init_row(v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
+    }
+}
+
+// MAX over the wavefront (counts are already scalar), then one float2
+// {PPV, MAX} per kernel, written by lanes 0, 16, 32 and 48.
+template <int G>
+__device__ __forceinline__ void write_row(const v4f (&mx)[G], const uint32_t (&cnt)[G][4],
+                                          const int (&out_kernel)[G], double inv_O, int lane,
+                                          float *Frow) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const float m = reduce4(mx[g]);
+        // the count of slot slot_of_row(q) for the lanes of row q
+        // (readfirstlane keeps the four uniform counts independent scalars,
+        // so the selects stay selects)
+        const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
+        const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
+        const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
+        const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
+        uint32_t c = c0;
+        c = lane >= 16 ? c2 : c;
+        c = lane >= 32 ? c1 : c;
+        c = lane >= 48 ? c3 : c;
+        if (out_kernel[g] >= 0) {
+            // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
+            // quotient is never a float midpoint and lies at least 2^-49
+            // (relative) from one, while c * fl64(1/O) is within 2^-52 of
+            // it, so rounding the double product to float gives the same
+            // float as the fp32 division
+            float2 res;
+            res.x = (float)((double)c * inv_O);
+            res.y = m;
+            *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)out_kernel[g]) = res;
+        }
+    }
+}
+
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.
 template <int ELL, int G>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
-    // steps per block: 8 independent accumulation chains per wavefront
-    constexpr int T = 8 / G;
+    // steps per block: 8 (G = 1) or 6 (G = 2) independent accumulation
+    // chains per wavefront; T = 3 for G = 2 keeps the kernel within 96 VGPRs
+    // (5 wavefronts per SIMD)
+    constexpr int T = G == 1 ? 8 : 3;
     const int d = it.d;
     // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
     float wa[G][ELL];
@@ -216,7 +311,8 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
         for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
     // C operand of the first tap: the bias of block row v (kernel slot v)
-    v4f bias[G];
+    // (wavefront-uniform: scalar registers)
+    float bias[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
@@ -228,95 +324,28 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
     for (int g = 0; g < G; ++g)
         out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
-    // Items with one round (small dilations) share the round's lane entry,
-    // start values and step count across all series: the rows then loop
-    // inside the round.  Items with several rounds loop rounds inside rows.
-    const bool single = it.rounds == 1;
-    const int n_outer = single ? 1 : nrows;
-    const int n_inner = single ? nrows : it.rounds;
-    v4f binit[G], blast[G];
-    uint32_t pos = 0;
-    int len = 0;
-    v4f mx[G];
-    uint32_t cnt[G][4];
-    for (int o = 0; o < n_outer; ++o) {
-        for (int i = 0; i < n_inner; ++i) {
-            const int r = single ? i : o;
-            const int rd = single ? 0 : i;
-            if (single ? i == 0 : true) {
-                // round set-up: rounds of S steps first, then of S-1 steps
-                len = rd < it.rounds_long ? it.S : it.S - 1;
-                const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
-                pos = e & rocket::kLanePosMask;
-                if (__builtin_amdgcn_ballot_w64((e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0) == 0) {
-#pragma unroll
-                    for (int g = 0; g < G; ++g) {
-                        binit[g] = bias[g];
-                        blast[g] = bias[g];
-                    }
-                } else {
-                    const bool idle = (e & rocket::kLaneIdle) != 0;
-                    const bool drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
-#pragma unroll
-                    for (int g = 0; g < G; ++g)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) {
-                            binit[g][v] = idle ? -INFINITY : bias[g][v];
-                            blast[g][v] = drop_last ? -INFINITY : bias[g][v];
-                        }
-                }
+    const int64_t f_stride = 2 * (int64_t)a.K;
+    RoundState<G> st;
+    if (it.rounds == 1) {
+        // one round (small dilations): its lane state serves every series
+        setup_round<G>(it, 0, a, bias, lane, st);
+        for (int r = 0; r < nrows; ++r) {
+            v4f mx[G];
+            uint32_t cnt[G][4];
+            init_row<G>(mx, cnt);
+            run_round<ELL, G, T>(rows0 + r * a.row_stride - it.p + st.pos, d, st, wa, mx, cnt);
+            write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
+        }
+    } else {
+        for (int r = 0; r < nrows; ++r) {
+            v4f mx[G];
+            uint32_t cnt[G][4];
+            init_row<G>(mx, cnt);
+            for (int rd = 0; rd < it.rounds; ++rd) {
+                setup_round<G>(it, rd, a, bias, lane, st);
+                run_round<ELL, G, T>(rows0 + r * a.row_stride - it.p + st.pos, d, st, wa, mx, cnt);
             }
-            if (single ? true : i == 0) {
-#pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
-                }
-            }
-            // xs[m*d] is the zero-padded series value under tap m of the
-            // lane's step-0 output
-            const float *xs = rows0 + r * a.row_stride - it.p + pos;
-            const int nfull = (len - 1) / T;  // full blocks before the last block
-            const int nv = len - nfull * T;   // length of the last block, 1..T
-            // block b reads xs[b*T*d + m*d]: one lane address plus a
-            // wavefront-uniform offset per load
-            for (int blk = 0; blk < nfull; ++blk) {
-                const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
-                step_block<ELL, G, T, false>(xs + off, d, wa, binit, blast, mx, cnt);
-            }
-            TailBlock<ELL, G, T>::run(nv, xs + __builtin_amdgcn_readfirstlane(nfull * T * d), d, wa,
-                                      binit, blast, mx, cnt);
-            if (single ? true : i == n_inner - 1) {
-                // MAX over the wavefront; counts are already scalar
-#pragma unroll
-                for (int g = 0; g < G; ++g) {
-                    const float m = reduce4(mx[g]);
-                    // the count of slot slot_of_row(q) for the lanes of row q
-                    // (readfirstlane keeps the four uniform counts independent
-                    // scalars, so the selects stay selects)
-                    const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
-                    const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
-                    const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
-                    const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
-                    uint32_t c = c0;
-                    c = lane >= 16 ? c2 : c;
-                    c = lane >= 32 ? c1 : c;
-                    c = lane >= 48 ? c3 : c;
-                    if (out_kernel[g] >= 0) {
-                        // (float)c / (float)O, correctly rounded: for c <= O < 2^24
-                        // the quotient is never a float midpoint and lies at
-                        // least 2^-49 (relative) from one, while c * fl64(1/O)
-                        // is within 2^-52 of it, so rounding the double product
-                        // to float gives the same float as the fp32 division
-                        float2 res;
-                        res.x = (float)((double)c * it.inv_O);
-                        res.y = m;
-                        *reinterpret_cast<float2 *>(F0 + (int64_t)r * 2 * a.K +
-                                                    2 * (int64_t)out_kernel[g]) = res;
-                    }
-                }
-            }
+            write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
         }
     }
 }
