@@ -86,6 +86,9 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run one elementwise copy of this many MiB (reference for "
                          "hardware byte counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the paper's one-factor sweep instead (n, L, K around "
+                         "1,000 x 10,000 x 10,000), device-resident and host-to-host")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -99,6 +102,9 @@ def main():
 
     import paper_2601_17091_amd as rk
     from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
+
+    if args.sweep:
+        return sweep(args)
 
     if not os.path.exists(rk.rocket.LIB_PATH):
         from paper_2601_17091_amd import build_lib
@@ -246,6 +252,78 @@ def main():
         "cpu_baseline": cpu,
         "parity": parity,
     }
+    print(json.dumps(out), flush=True)
+
+
+SWEEP_DEFAULT = (1000, 10000, 10000)
+SWEEP_POINTS = ([SWEEP_DEFAULT]
+                + [(n, 10000, 10000) for n in (100, 500, 2000)]
+                + [(1000, L, 10000) for L in (1000, 5000, 20000)]
+                + [(1000, 10000, K) for K in (1000, 5000, 20000)])
+
+
+def sweep(args):
+    """The paper's timing sweep (Sec. 4): defaults n = 1,000 series, length
+    L = 10,000, K = 10,000 kernels, one factor varied at a time.  Each point
+    is timed with the series resident on the device, and host-to-host with
+    pinned buffers through rocket_transform_host (copies overlapped with
+    the transform).  The paper finds time linear in n, L and K; the line
+    reports time per series x kernel x sample relative to the default."""
+    import torch
+
+    import paper_2601_17091_amd as rk
+    from paper_2601_17091_amd.workloads import make_series
+
+    dev = torch.device("cuda:0")
+    points = []
+    for (n, L, K) in SWEEP_POINTS:
+        ks = rk.generate_kernels(206, K, L)
+        X_np = make_series("random_walk", n, L, 106)
+        X = torch.from_numpy(X_np).to(dev)
+        plan = rk.Plan(ks, L)
+        info = plan.info()
+        F = torch.empty((n, 2 * K), dtype=torch.float32, device=dev)
+        stream = torch.cuda.current_stream()
+        for _ in range(max(1, args.warmup)):
+            plan.transform_into(X, F, stream)
+        torch.cuda.synchronize()
+        reps = max(1, args.steps)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            plan.transform_into(X, F, stream)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        dev_ms = t0.elapsed_time(t1) / reps
+        Xh = torch.empty((n, L), dtype=torch.float32, pin_memory=True)
+        Xh.copy_(torch.from_numpy(X_np))
+        Fh = torch.empty((n, 2 * K), dtype=torch.float32, pin_memory=True)
+        plan.transform_host(Xh, Fh)
+        h_reps = 2
+        w0 = time.perf_counter()
+        for _ in range(h_reps):
+            plan.transform_host(Xh, Fh)
+        host_ms = (time.perf_counter() - w0) * 1e3 / h_reps
+        same = bool(torch.equal(Fh, F.cpu()))
+        valid, _ = valid_taps(ks, L)
+        flops = 2.0 * n * valid
+        pt = {"n": n, "L": L, "K": K, "device_ms": dev_ms, "host_to_host_ms": host_ms,
+              "host_matches_device": same, "tflops": flops / (dev_ms * 1e-3) / 1e12,
+              "series_kernels_per_s": n * K / (dev_ms * 1e-3),
+              "ns_per_series_kernel_sample": dev_ms * 1e6 / (n * K * L),
+              "clamped": info["clamped"], "direct": info["direct"]}
+        log("sweep %s" % json.dumps(pt))
+        points.append(pt)
+        plan.close()
+        del X, F, Xh, Fh
+    base = points[0]["ns_per_series_kernel_sample"]
+    rel = [p["ns_per_series_kernel_sample"] / base for p in points]
+    out = {"metric": "ROCKET transform time over the paper's n/L/K sweep (fp32, 1 MI355X)",
+           "unit": "ms", "dtype": "fp32", "data": "synthetic (seeded random walks; seeded ROCKET kernels)",
+           "config": {"workload": "paper_sweep", "default": {"n": 1000, "L": 10000, "K": 10000}},
+           "points": points,
+           "linearity": {"time_per_unit_vs_default_min": min(rel), "time_per_unit_vs_default_max": max(rel)},
+           "source_digest": source_digest()}
     print(json.dumps(out), flush=True)
 
 

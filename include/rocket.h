@@ -117,7 +117,8 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
 
 /* Plan flags for rocket_plan_create_ex. */
 #define ROCKET_PLAN_DEFAULT 0u
-#define ROCKET_PLAN_DIRECT 1u /* use the plain one-wavefront-per-pair kernel */
+#define ROCKET_PLAN_DIRECT 1u  /* use the plain one-wavefront-per-pair kernel */
+#define ROCKET_PLAN_CLAMPED 2u /* fused kernel with clamped indices (one-zero margins) */
 
 /*
  * rocket_plan_create with flags.  ROCKET_PLAN_DIRECT selects the plain
@@ -125,7 +126,11 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
  * global memory.  It is slower and serves as a second GPU reference; the
  * default plan also falls back to it when a series (plus the zero margins
  * the kernels need) does not fit one workgroup's LDS.  Unknown flag bits
- * give ROCKET_ERR_INVALID_ARG.  Same errors as rocket_plan_create otherwise.
+ * give ROCKET_ERR_INVALID_ARG.  ROCKET_PLAN_CLAMPED forces the layout the
+ * default plan picks for long series: rows staged with a single zero on each
+ * side and every series index clamped into [-1, L] (same results; two more
+ * instructions per load).  Both flags together are ROCKET_ERR_INVALID_ARG.
+ * Same errors as rocket_plan_create otherwise.
  */
 rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t flags,
                                     rocket_plan **out);
@@ -156,6 +161,25 @@ rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const r
                                float *F_dev, void *hip_stream);
 
 /*
+ * Transform series held in HOST memory: X_host [n, L] -> F_host [n, 2K]
+ * (same layout and feature order as rocket_transform_plan).  Rows go
+ * through the device in batches of batch_rows (0: about n/8 rows, at most
+ * 256 MiB of staging per buffer).  Each
+ * batch's copy in, transform and copy out run on three HIP streams (the
+ * caller's stream for the transform, two of the library's own for the
+ * copies), double-buffered, so copies overlap the transform of the
+ * neighbouring batches.  Returns when F_host is complete.  For overlap the
+ * host buffers should be pinned (hipHostMalloc, or torch pin_memory);
+ * pageable buffers work but the copies then serialise.  The function
+ * allocates and frees its own device staging buffers (2 x batch of X and
+ * of F).  n == 0 is a no-op.
+ * Errors: ROCKET_ERR_INVALID_ARG (p NULL, n < 0, X_host or F_host NULL with
+ *         n > 0, batch_rows < 0); ROCKET_ERR_OOM; ROCKET_ERR_HIP.
+ */
+rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, int64_t n,
+                                    float *F_host, int64_t batch_rows, void *hip_stream);
+
+/*
  * Plan facts for benchmarks and tests (host only).  Any output pointer may
  * be NULL.
  *   n_items      number of work items (groups of kernels sharing one bucket)
@@ -163,10 +187,15 @@ rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const r
  *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks)
  *   lds_bytes    LDS one workgroup uses (0 for the direct kernel)
  *   direct       1 if the plan runs the direct kernel, else 0
+ *   clamped      1 if the fused kernel stages rows with a single zero on
+ *                each side and clamps series indices (chosen when the full
+ *                zero margins of the padded kernels would not fit in LDS),
+ *                else 0
  * Errors: ROCKET_ERR_INVALID_ARG if p is NULL.
  */
 rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
-                               int64_t *mfma_per_row, int64_t *lds_bytes, int32_t *direct);
+                               int64_t *mfma_per_row, int64_t *lds_bytes, int32_t *direct,
+                               int32_t *clamped);
 
 /*
  * Host-side work tables of the fused kernel, for tests and tools (no GPU is

@@ -81,10 +81,37 @@ constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
 
+// Where a lane's window values come from.  value(m) is the zero-padded
+// series value under tap m of the lane's current step-0 output (positions
+// m*d apart); shifted(k) moves the window k positions along the row (k is
+// wavefront-uniform).
+//   PaddedRow:  the row sits in LDS with zero margins wide enough for every
+//               padded tap, so value(m) is one load at xs + m*d.
+//   ClampedRow: the row sits in LDS with one zero on each side (index -1 and
+//               L); value(m) clamps the series index into [-1, L] first.
+//               Used when the margins would not fit in LDS (long series);
+//               it costs two more VALU instructions per load.
+struct PaddedRow {
+    const float *xs;
+    int d;
+    __device__ __forceinline__ float value(int m) const { return xs[m * d]; }
+    __device__ __forceinline__ PaddedRow shifted(int k) const { return PaddedRow{xs + k, d}; }
+};
+
+struct ClampedRow {
+    const float *row;  // series index 0
+    int i0;            // series index under tap 0 of the lane's step-0 output
+    int d;
+    int L;
+    __device__ __forceinline__ float value(int m) const {
+        return row[min(max(i0 + m * d, -1), L)];
+    }
+    __device__ __forceinline__ ClampedRow shifted(int k) const { return ClampedRow{row, i0 + k, d, L}; }
+};
+
 // NS consecutive output steps of one round, as an outer-product contraction
 // over the taps.  The window of series values under the NS outputs
-// (NS + ELL - 1 values spaced d apart, starting at xs) is read from LDS
-// first; then tap j of every step and kernel group is issued before tap j+1,
+// (NS + ELL - 1 values spaced d apart) is read from LDS first; then tap j of every step and kernel group is issued before tap j+1,
 // so the wavefront keeps NS*G independent MFMA accumulation chains in
 // flight.  Each chain starts from binit (the slots' biases, or -inf on a
 // lane without a chunk); when LAST is set the block ends the round and its
@@ -92,13 +119,13 @@ constexpr int kDppRowMirror = 0x140;
 // output short, or no chunk).  A chain started at -inf stays -inf, so MAX folds every
 // result (v_max3 over pairs of steps) and the positive count is a ballot of
 // y > 0 popcounted on the scalar unit.
-template <int ELL, int G, int NS, bool LAST>
-__device__ __forceinline__ void step_block(const float *xs, int d, const float (&wa)[G][ELL],
+template <int ELL, int G, int NS, bool LAST, typename Src>
+__device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][ELL],
                                            const v4f (&binit)[G], bool drop_last,
                                            v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
     float xw[NS + ELL - 1];
 #pragma unroll
-    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = xs[m * d];
+    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
     v4f acc[NS][G];
 #pragma unroll
     for (int u = 0; u < NS; ++u)
@@ -142,22 +169,21 @@ __device__ __forceinline__ void step_block(const float *xs, int d, const float (
 }
 
 // The last block of a round: its length nv (1..N) selects a code copy.
-template <int ELL, int G, int N>
+template <int ELL, int G, int N, typename Src>
 struct TailBlock {
-    __device__ __forceinline__ static void run(int nv, const float *xs, int d,
-                                               const float (&wa)[G][ELL], const v4f (&binit)[G],
-                                               bool drop_last, v4f (&mx)[G],
-                                               uint32_t (&cnt)[G][4]) {
+    __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
+                                               const v4f (&binit)[G], bool drop_last,
+                                               v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
         if (nv == N)
-            step_block<ELL, G, N, true>(xs, d, wa, binit, drop_last, mx, cnt);
+            step_block<ELL, G, N, true>(src, wa, binit, drop_last, mx, cnt);
         else
-            TailBlock<ELL, G, N - 1>::run(nv, xs, d, wa, binit, drop_last, mx, cnt);
+            TailBlock<ELL, G, N - 1, Src>::run(nv, src, wa, binit, drop_last, mx, cnt);
     }
 };
 
-template <int ELL, int G>
-struct TailBlock<ELL, G, 0> {
-    __device__ __forceinline__ static void run(int, const float *, int, const float (&)[G][ELL],
+template <int ELL, int G, typename Src>
+struct TailBlock<ELL, G, 0, Src> {
+    __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL],
                                                const v4f (&)[G], bool, v4f (&)[G],
                                                uint32_t (&)[G][4]) {}
 };
@@ -232,22 +258,22 @@ __device__ __forceinline__ void setup_round(const ItemDesc &it, int rd, const Fu
         for (int v = 0; v < 4; ++v) st.binit[g][v] = idle ? -INFINITY : bias[g][v];
 }
 
-// All steps of one round for one series; xs[m*d] is the zero-padded series
-// value under tap m of the lane's step-0 output.
-template <int ELL, int G, int T>
-__device__ __forceinline__ void run_round(const float *xs, int d, const RoundState<G> &st,
+// All steps of one round for one series; src.value(m) is the zero-padded
+// series value under tap m of the lane's step-0 output.
+template <int ELL, int G, int T, typename Src>
+__device__ __forceinline__ void run_round(const Src &src, int d, const RoundState<G> &st,
                                           const float (&wa)[G][ELL], v4f (&mx)[G],
                                           uint32_t (&cnt)[G][4]) {
     const int nfull = (st.len - 1) / T;  // full blocks before the last block
     const int nv = st.len - nfull * T;   // length of the last block, 1..T
-    // block b reads xs[b*T*d + m*d]: one lane address plus a
-    // wavefront-uniform offset per load
+    // block b starts b*T*d positions along the row: a wavefront-uniform
+    // offset, so each load is one lane address plus a scalar
     for (int blk = 0; blk < nfull; ++blk) {
         const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
-        step_block<ELL, G, T, false>(xs + off, d, wa, st.binit, st.drop_last, mx, cnt);
+        step_block<ELL, G, T, false>(src.shifted(off), wa, st.binit, st.drop_last, mx, cnt);
     }
-    TailBlock<ELL, G, T>::run(nv, xs + __builtin_amdgcn_readfirstlane(nfull * T * d), d, wa,
-                              st.binit, st.drop_last, mx, cnt);
+    TailBlock<ELL, G, T, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
+                                   wa, st.binit, st.drop_last, mx, cnt);
 }
 
 template <int G>
@@ -294,16 +320,27 @@ __device__ __forceinline__ void write_row(const v4f (&mx)[G], const uint32_t (&c
     }
 }
 
+// One round over the series whose index 0 sits at `row` in LDS.
+template <int ELL, int G, int T, bool CLAMP>
+__device__ __forceinline__ void run_row_round(const float *row, const ItemDesc &it, int L,
+                                              const RoundState<G> &st, const float (&wa)[G][ELL],
+                                              v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+    const int i0 = (int)st.pos - it.p;  // series index under tap 0 of step 0
+    if (CLAMP)
+        run_round<ELL, G, T>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, mx, cnt);
+    else
+        run_round<ELL, G, T>(PaddedRow{row + i0, it.d}, it.d, st, wa, mx, cnt);
+}
+
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.
-template <int ELL, int G>
+template <int ELL, int G, bool CLAMP>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
     // steps per block: 8 (G = 1) or 6 (G = 2) independent accumulation
     // chains per wavefront; T = 3 for G = 2 keeps the kernel within 96 VGPRs
     // (5 wavefronts per SIMD)
     constexpr int T = G == 1 ? 8 : 3;
-    const int d = it.d;
     // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
     float wa[G][ELL];
 #pragma unroll
@@ -333,7 +370,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
             v4f mx[G];
             uint32_t cnt[G][4];
             init_row<G>(mx, cnt);
-            run_round<ELL, G, T>(rows0 + r * a.row_stride - it.p + st.pos, d, st, wa, mx, cnt);
+            run_row_round<ELL, G, T, CLAMP>(rows0 + r * a.row_stride, it, a.L, st, wa, mx, cnt);
             write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
         }
     } else {
@@ -343,7 +380,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
             init_row<G>(mx, cnt);
             for (int rd = 0; rd < it.rounds; ++rd) {
                 setup_round<G>(it, rd, a, bias, lane, st);
-                run_round<ELL, G, T>(rows0 + r * a.row_stride - it.p + st.pos, d, st, wa, mx, cnt);
+                run_row_round<ELL, G, T, CLAMP>(rows0 + r * a.row_stride, it, a.L, st, wa, mx, cnt);
             }
             write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
         }
@@ -370,7 +407,7 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
 }
 
 // Items of one variant, taken one at a time from the workgroup's counter.
-template <int ELL, int G>
+template <int ELL, int G, bool CLAMP>
 __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items,
                                           const float *rows0, int nrows, const FusedArgs &a,
                                           float *F0, int lane) {
@@ -380,13 +417,13 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
         idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
         if (idx >= cnt_items) break;
         const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
-        run_item<ELL, G>(it, rows0, nrows, a, F0, lane);
+        run_item<ELL, G, CLAMP>(it, rows0, nrows, a, F0, lane);
     }
 }
 
 // Workgroup = (variant, row tile, split); each workgroup stages its row tile
 // in LDS and runs the items of one variant over it.
-template <int BLOCK>
+template <int BLOCK, bool CLAMP>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
@@ -428,12 +465,12 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     float *F0 = a.F + grow * 2 * (int64_t)a.K;
     const float *rows0 = smem + a.halo_lo;
     switch (variant) {
-        case 0: run_items<7, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 1: run_items<7, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 2: run_items<9, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 3: run_items<9, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 4: run_items<11, 1>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        default: run_items<11, 2>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 0: run_items<7, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 1: run_items<7, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 2: run_items<9, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 3: run_items<9, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 4: run_items<11, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        default: run_items<11, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
     }
 }
 
@@ -503,6 +540,10 @@ struct rocket_plan {
     int device = 0;
     int n_cu = 0;
     bool direct = false;
+    bool clamp = false;      // rows staged with one-zero margins, indices clamped
+    int32_t halo_lo = 0;     // staged layout actually used (floats)
+    int32_t row_stride = 0;
+    int32_t tail_pad = 0;
     int rows_per_block = 1;  // series staged per workgroup
     int64_t lds_bytes = 0;   // per workgroup: the rows plus the tail pad
     ItemDesc *d_items = nullptr;
@@ -538,7 +579,9 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
                                                rocket_plan **out) {
     if (!out) return ROCKET_ERR_INVALID_ARG;
     *out = nullptr;
-    if (flags & ~ROCKET_PLAN_DIRECT) return ROCKET_ERR_INVALID_ARG;
+    if ((flags & ~(ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED)) ||
+        ((flags & ROCKET_PLAN_DIRECT) && (flags & ROCKET_PLAN_CLAMPED)))
+        return ROCKET_ERR_INVALID_ARG;
     rocket_status st = rocket::validate_kernels(k, L);
     if (st != ROCKET_OK) return st;
     rocket_plan *p = new (std::nothrow) rocket_plan();
@@ -556,15 +599,33 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         return ROCKET_ERR_HIP;
     }
     p->n_cu = prop.multiProcessorCount;
-    // rows per workgroup: as many as fit the LDS budget (at least one)
-    const int64_t row_bytes = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
-    const int64_t pad_bytes = (int64_t)p->host.tail_pad * (int64_t)sizeof(float);
-    if (row_bytes > 0)
-        p->rows_per_block = (int)std::max<int64_t>(
+    // Staged layout: rows with zero margins wide enough for every padded tap
+    // if that fits one workgroup's LDS, else rows with one zero on each side
+    // and clamped indices, else the direct kernel.  Rows per workgroup: as
+    // many as fit the LDS budget (at least one).
+    const int64_t limit = (int64_t)prop.sharedMemPerBlock;
+    auto layout = [&](int64_t stride, int64_t pad, int *rows) {
+        const int64_t row_bytes = stride * (int64_t)sizeof(float);
+        const int64_t pad_bytes = pad * (int64_t)sizeof(float);
+        *rows = (int)std::max<int64_t>(
             1, std::min<int64_t>(kMaxRowsPerBlock, (kRowsLdsBudget - pad_bytes) / row_bytes));
-    const int64_t lds = p->rows_per_block * row_bytes + pad_bytes;
-    p->direct = (flags & ROCKET_PLAN_DIRECT) || p->host.row_stride == 0 ||
-                lds > (int64_t)prop.sharedMemPerBlock;
+        return *rows * row_bytes + pad_bytes;
+    };
+    int64_t lds = 0;
+    p->direct = (flags & ROCKET_PLAN_DIRECT) != 0;
+    if (!p->direct && !(flags & ROCKET_PLAN_CLAMPED) && p->host.row_stride > 0 &&
+        (lds = layout(p->host.row_stride, p->host.tail_pad, &p->rows_per_block)) <= limit) {
+        p->halo_lo = p->host.halo_lo;
+        p->row_stride = p->host.row_stride;
+        p->tail_pad = p->host.tail_pad;
+    } else if (!p->direct && (lds = layout((int64_t)L + 2, 0, &p->rows_per_block)) <= limit) {
+        p->clamp = true;
+        p->halo_lo = 1;
+        p->row_stride = L + 2;
+        p->tail_pad = 0;
+    } else {
+        p->direct = true;
+    }
     p->lds_bytes = p->direct ? 0 : lds;
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
@@ -581,12 +642,15 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
         if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
         if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
-        if (e == hipSuccess && lds > 64 * 1024)
-            e = hipFuncSetAttribute((const void *)rocket_fused_kernel<kBigBlock>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e == hipSuccess && lds > 64 * 1024)
-            e = hipFuncSetAttribute((const void *)rocket_fused_kernel<kBlock>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e == hipSuccess && lds > 64 * 1024) {
+            const void *fns[] = {(const void *)rocket_fused_kernel<kBlock, false>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, false>,
+                                 (const void *)rocket_fused_kernel<kBlock, true>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, true>};
+            for (const void *f : fns)
+                if (e == hipSuccess)
+                    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        }
     }
     if (e != hipSuccess) {
         plan_free_device(p);
@@ -609,13 +673,14 @@ extern "C" void rocket_plan_destroy(rocket_plan *p) {
 
 extern "C" rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
                                           int64_t *mfma_per_row, int64_t *lds_bytes,
-                                          int32_t *direct) {
+                                          int32_t *direct, int32_t *clamped) {
     if (!p) return ROCKET_ERR_INVALID_ARG;
     if (n_items) *n_items = (int64_t)p->host.items.size();
     if (n_buckets) *n_buckets = p->host.n_buckets;
     if (mfma_per_row) *mfma_per_row = p->host.mfma_per_row;
     if (lds_bytes) *lds_bytes = p->lds_bytes;
     if (direct) *direct = p->direct ? 1 : 0;
+    if (clamped) *clamped = p->clamp ? 1 : 0;
     return ROCKET_OK;
 }
 
@@ -644,7 +709,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     // enough workgroups to fill the chip several times over: split the work
     // items of a series across workgroups when there are few series
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
-    const int64_t row_bytes = (int64_t)p->host.row_stride * (int64_t)sizeof(float);
+    const int64_t row_bytes = (int64_t)p->row_stride * (int64_t)sizeof(float);
     const int R = p->rows_per_block;
     const int64_t tiles = (n + R - 1) / R;
     int li = 0;
@@ -668,9 +733,9 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         const int32_t *sb = p->host.split_begin.data() + p->host.layout_off[li];
         if (sb[(v + 1) * nsplit] > sb[v * nsplit]) a.variants[a.n_variants++] = v;
     }
-    a.halo_lo = p->host.halo_lo;
-    a.row_stride = p->host.row_stride;
-    a.tail_pad = p->host.tail_pad;
+    a.halo_lo = p->halo_lo;
+    a.row_stride = p->row_stride;
+    a.tail_pad = p->tail_pad;
     a.rows_per_block = R;
     const int64_t max_rows =
         ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1)) / kXcds - 1) * kXcds * R;
@@ -681,10 +746,15 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         a.tiles_per_xcd = (tiles_now + kXcds - 1) / kXcds;
         const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)p->lds_bytes;
-        if (row_bytes > kBigLds)
-            hipLaunchKernelGGL(rocket_fused_kernel<kBigBlock>, dim3(nb), dim3(kBigBlock), lds, s, a);
+        const bool big = row_bytes > kBigLds;
+        if (p->clamp && big)
+            hipLaunchKernelGGL((rocket_fused_kernel<kBigBlock, true>), dim3(nb), dim3(kBigBlock), lds, s, a);
+        else if (p->clamp)
+            hipLaunchKernelGGL((rocket_fused_kernel<kBlock, true>), dim3(nb), dim3(kBlock), lds, s, a);
+        else if (big)
+            hipLaunchKernelGGL((rocket_fused_kernel<kBigBlock, false>), dim3(nb), dim3(kBigBlock), lds, s, a);
         else
-            hipLaunchKernelGGL(rocket_fused_kernel<kBlock>, dim3(nb), dim3(kBlock), lds, s, a);
+            hipLaunchKernelGGL((rocket_fused_kernel<kBlock, false>), dim3(nb), dim3(kBlock), lds, s, a);
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
     }
     return ROCKET_OK;
@@ -697,6 +767,74 @@ extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float
     if (!X_dev || !F_dev) return ROCKET_ERR_INVALID_ARG;
     hipStream_t s = (hipStream_t)hip_stream;
     return p->direct ? launch_direct(p, X_dev, n, F_dev, s) : launch_fused(p, X_dev, n, F_dev, s);
+}
+
+// Host-to-host transform with copies overlapped against the transform:
+// batch i uses X and F staging buffer i % 2.  Its copy in waits until the
+// transform of batch i-2 (the last reader of that X buffer) is done; its
+// transform waits for its copy in and for the copy out of batch i-2 (the
+// last reader of that F buffer); its copy out waits for its transform.
+extern "C" rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, int64_t n,
+                                               float *F_host, int64_t batch_rows,
+                                               void *hip_stream) {
+    if (!p || n < 0 || batch_rows < 0) return ROCKET_ERR_INVALID_ARG;
+    if (n == 0) return ROCKET_OK;
+    if (!X_host || !F_host) return ROCKET_ERR_INVALID_ARG;
+    const int64_t L = p->host.L, K2 = 2 * (int64_t)p->host.n_kernels;
+    int64_t B = batch_rows;
+    // default: about 8 batches, so copies have neighbours to overlap with,
+    // each within 256 MiB of staging
+    if (B == 0)
+        B = std::max<int64_t>(1, std::min<int64_t>((n + 7) / 8, (int64_t)(256 << 20) / ((L + K2) * 4)));
+    B = std::min(B, n);
+    const int64_t nb = (n + B - 1) / B;
+    hipStream_t sc = (hipStream_t)hip_stream;
+    hipStream_t s_in = nullptr, s_out = nullptr;
+    float *dX[2] = {nullptr, nullptr}, *dF[2] = {nullptr, nullptr};
+    hipEvent_t ev_in[2] = {}, ev_tr[2] = {}, ev_out[2] = {};
+    rocket_status st = ROCKET_OK;
+    hipError_t e = hipStreamCreateWithFlags(&s_in, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&s_out, hipStreamNonBlocking);
+    for (int j = 0; j < 2 && e == hipSuccess; ++j) {
+        e = hipMalloc((void **)&dX[j], (size_t)(B * L * 4));
+        if (e == hipSuccess) e = hipMalloc((void **)&dF[j], (size_t)(B * K2 * 4));
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_in[j], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_tr[j], hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev_out[j], hipEventDisableTiming);
+    }
+    for (int64_t i = 0; i < nb && e == hipSuccess && st == ROCKET_OK; ++i) {
+        const int j = (int)(i & 1);
+        const int64_t r0 = i * B, m = std::min(B, n - r0);
+        if (i >= 2) e = hipStreamWaitEvent(s_in, ev_tr[j], 0);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(dX[j], X_host + r0 * L, (size_t)(m * L * 4), hipMemcpyHostToDevice, s_in);
+        if (e == hipSuccess) e = hipEventRecord(ev_in[j], s_in);
+        if (e == hipSuccess) e = hipStreamWaitEvent(sc, ev_in[j], 0);
+        if (e == hipSuccess && i >= 2) e = hipStreamWaitEvent(sc, ev_out[j], 0);
+        if (e == hipSuccess) st = rocket_transform_plan(p, dX[j], m, dF[j], sc);
+        if (e == hipSuccess && st == ROCKET_OK) e = hipEventRecord(ev_tr[j], sc);
+        if (e == hipSuccess && st == ROCKET_OK) e = hipStreamWaitEvent(s_out, ev_tr[j], 0);
+        if (e == hipSuccess && st == ROCKET_OK)
+            e = hipMemcpyAsync(F_host + r0 * K2, dF[j], (size_t)(m * K2 * 4), hipMemcpyDeviceToHost, s_out);
+        if (e == hipSuccess && st == ROCKET_OK) e = hipEventRecord(ev_out[j], s_out);
+    }
+    // drain every stream before the staging buffers go away
+    const hipError_t e1 = s_in ? hipStreamSynchronize(s_in) : hipSuccess;
+    const hipError_t e2 = hipStreamSynchronize(sc);
+    const hipError_t e3 = s_out ? hipStreamSynchronize(s_out) : hipSuccess;
+    for (int j = 0; j < 2; ++j) {
+        if (dX[j]) (void)hipFree(dX[j]);
+        if (dF[j]) (void)hipFree(dF[j]);
+        if (ev_in[j]) (void)hipEventDestroy(ev_in[j]);
+        if (ev_tr[j]) (void)hipEventDestroy(ev_tr[j]);
+        if (ev_out[j]) (void)hipEventDestroy(ev_out[j]);
+    }
+    if (s_in) (void)hipStreamDestroy(s_in);
+    if (s_out) (void)hipStreamDestroy(s_out);
+    if (st != ROCKET_OK) return st;
+    if (e != hipSuccess) return map_hip(e);
+    if (e1 != hipSuccess || e2 != hipSuccess || e3 != hipSuccess) return ROCKET_ERR_HIP;
+    return ROCKET_OK;
 }
 
 extern "C" rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L,

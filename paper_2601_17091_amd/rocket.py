@@ -23,6 +23,7 @@ ROCKET_ERR_HIP = -4
 ROCKET_ERR_INTERNAL = -5
 ROCKET_PLAN_DEFAULT = 0
 ROCKET_PLAN_DIRECT = 1
+ROCKET_PLAN_CLAMPED = 2
 MAX_KERNEL_LENGTH = 11
 
 # every symbol include/rocket.h declares
@@ -34,6 +35,7 @@ EXPORTED = (
     "rocket_plan_destroy",
     "rocket_transform_plan",
     "rocket_transform",
+    "rocket_transform_host",
     "rocket_plan_info",
     "rocket_plan_tables_build",
     "rocket_plan_tables_free",
@@ -103,7 +105,9 @@ def library() -> ctypes.CDLL:
     lib.rocket_transform_plan.restype = ctypes.c_int
     lib.rocket_transform.argtypes = [vp, i64, i32, kp, vp, vp]
     lib.rocket_transform.restype = ctypes.c_int
-    lib.rocket_plan_info.argtypes = [vp] + [ctypes.POINTER(i64)] * 4 + [ctypes.POINTER(i32)]
+    lib.rocket_transform_host.argtypes = [vp, vp, i64, vp, i64, vp]
+    lib.rocket_transform_host.restype = ctypes.c_int
+    lib.rocket_plan_info.argtypes = [vp] + [ctypes.POINTER(i64)] * 4 + [ctypes.POINTER(i32)] * 2
     lib.rocket_plan_info.restype = ctypes.c_int
     lib.rocket_plan_tables_build.argtypes = [kp, i32, ctypes.POINTER(CPlanTables)]
     lib.rocket_plan_tables_build.restype = ctypes.c_int
@@ -213,24 +217,25 @@ def _check_series(X, L: int):
 class Plan:
     """rocket_plan: a kernel set planned for series of length L on the current device."""
 
-    def __init__(self, kernels: dict, L: int, direct: bool = False):
+    def __init__(self, kernels: dict, L: int, direct: bool = False, clamped: bool = False):
         lib = library()
         self._c, self._keep = as_c_kernels(kernels)
         self.n_kernels = int(self._c.n_kernels)
         self.L = int(L)
         h = ctypes.c_void_p()
-        flags = ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT
+        flags = (ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT) | (ROCKET_PLAN_CLAMPED if clamped else 0)
         _check(lib.rocket_plan_create_ex(ctypes.byref(self._c), self.L, flags, ctypes.byref(h)),
                "rocket_plan_create")
         self._h = h
 
     def info(self) -> dict:
         vals = [ctypes.c_int64() for _ in range(4)]
-        direct = ctypes.c_int32()
-        _check(library().rocket_plan_info(self._h, *[ctypes.byref(v) for v in vals], ctypes.byref(direct)),
+        direct, clamped = ctypes.c_int32(), ctypes.c_int32()
+        _check(library().rocket_plan_info(self._h, *[ctypes.byref(v) for v in vals], ctypes.byref(direct),
+                                          ctypes.byref(clamped)),
                "rocket_plan_info")
         return dict(n_items=vals[0].value, n_buckets=vals[1].value, mfma_per_row=vals[2].value,
-                    lds_bytes=vals[3].value, direct=bool(direct.value))
+                    lds_bytes=vals[3].value, direct=bool(direct.value), clamped=bool(clamped.value))
 
     def transform_into(self, X, F, stream=None):
         """F[n, 2K] <- features of X[n, L]; asynchronous on `stream`."""
@@ -251,6 +256,29 @@ class Plan:
         import torch
         F = torch.empty((X.shape[0], 2 * self.n_kernels), dtype=torch.float32, device=X.device)
         return self.transform_into(X, F, stream)
+
+    def transform_host(self, X_host, F_host, batch_rows: int = 0, stream=None):
+        """F_host[n, 2K] <- features of X_host[n, L], both in host memory
+        (CPU torch tensors, pinned for overlap, or numpy arrays); copies and
+        transforms of successive row batches overlap.  Blocks until done."""
+        import torch
+        X_t = X_host if isinstance(X_host, torch.Tensor) else torch.from_numpy(X_host)
+        F_t = F_host if isinstance(F_host, torch.Tensor) else torch.from_numpy(F_host)
+        if X_t.is_cuda or F_t.is_cuda:
+            raise ValueError("transform_host takes host tensors")
+        if X_t.dtype != torch.float32 or not X_t.is_contiguous() or X_t.dim() != 2 or X_t.shape[1] != self.L:
+            raise ValueError("X_host must be a contiguous float32 [n, %d] array" % self.L)
+        n = X_t.shape[0]
+        if (F_t.dtype != torch.float32 or not F_t.is_contiguous()
+                or tuple(F_t.shape) != (n, 2 * self.n_kernels)):
+            raise ValueError("F_host must be a contiguous float32 [%d, %d] array" % (n, 2 * self.n_kernels))
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        _check(library().rocket_transform_host(self._h, ctypes.c_void_p(X_t.data_ptr()), n,
+                                               ctypes.c_void_p(F_t.data_ptr()), int(batch_rows),
+                                               ctypes.c_void_p(stream.cuda_stream)),
+               "rocket_transform_host")
+        return F_host
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -1,6 +1,6 @@
 """Structural GPU checks: determinism, batch and permutation invariance,
-the one-shot entry point, empty input, and the plain kernel against the
-fused one."""
+the one-shot entry point, the host-to-host entry point, empty input, and
+the plain kernel against the fused one."""
 import numpy as np
 import pytest
 
@@ -78,3 +78,29 @@ def test_direct_kernel_agrees(env):
     assert np.abs(a[:, 1::2] - b[:, 1::2]).max() < 1e-5
     O = 500 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"]
     assert np.abs(np.rint(a[:, 0::2] * O) - np.rint(b[:, 0::2] * O)).max() <= 2
+
+
+@pytest.mark.parametrize("pinned,batch", [(True, 0), (True, 8), (False, 5)])
+def test_host_to_host_matches_device(env, pinned, batch):
+    """rocket_transform_host (overlapped copies, double-buffered batches,
+    ragged last batch) gives exactly the device-resident result."""
+    torch, rk, ks, X = env
+    p = rk.Plan(ks, X.shape[1])
+    want = p.transform(X)
+    torch.cuda.synchronize()
+    Xh = torch.empty(X.shape, dtype=torch.float32, pin_memory=pinned)
+    Xh.copy_(X.cpu())
+    Fh = torch.empty((X.shape[0], 2 * ks["length"].shape[0]), dtype=torch.float32, pin_memory=pinned)
+    Fh.fill_(float("nan"))
+    p.transform_host(Xh, Fh, batch_rows=batch)
+    assert torch.equal(Fh, want.cpu())
+
+
+def test_clamped_layout_matches_padded(env):
+    """The clamped-index layout computes the same dot products in the same
+    order as the zero-margin layout, so the features agree bitwise."""
+    torch, rk, ks, X = env
+    a = rk.Plan(ks, X.shape[1]).transform(X)
+    b = rk.Plan(ks, X.shape[1], clamped=True).transform(X)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
