@@ -35,6 +35,20 @@
  * floating-point dot product of m terms; the 2^-126 term covers flushing of
  * subnormal intermediates).  beta_max = max_t beta_t bounds the error of MAX.
  *
+ * Optional third feature, MPV (mean of the positive values; Sec. 5 names it
+ * as one that fuses into the same pass because it does not depend on where
+ * in the series the values fall):
+ *       MPV = sum_{t : y_t > 0} y_t / |{t : y_t > 0}|,  0 when no y_t > 0.
+ * Its certified range for an fp32 evaluation (values within beta_t of y_t,
+ * any of the outputs within beta_t of zero counted either way, the positive
+ * values summed in fp32 in any order, then one rounded division):
+ *       sure  = {t : y_t > beta_t},   maybe = {t : |y_t| <= beta_t}
+ *       mpv_lo = sum_sure (y_t - beta_t) (1 - gamma_c) (1 - u) / cnt_hi
+ *       mpv_hi = (sum_sure (y_t + beta_t) + sum_maybe 2 beta_t)
+ *                (1 + gamma_c) (1 + u) / cnt_lo
+ * with c = cnt_hi; when cnt_lo = 0 the range is [0, max_maybe 2 beta_t
+ * (1 + gamma_c)(1 + u)].
+ *
  * Plain loops: rows -> kernels -> t -> j.  No SIMD intrinsics, no fast-math.
  * OpenMP only splits rows across threads (for timing the CPU baseline).
  */
@@ -64,13 +78,15 @@ int64_t oracle_output_length(int32_t L, int32_t length, int32_t dilation, int32_
  * F        : fp64 [n_out, 2K]  (PPV, MAX interleaved per kernel).
  * cnt, cnt_lo, cnt_hi : int64 [n_out, K] (may be NULL).
  * beta_max : fp64 [n_out, K] (may be NULL).
+ * mpv, mpv_lo, mpv_hi : fp64 [n_out, K] (may be NULL).
  * nthreads : OpenMP threads (<= 0: runtime default).
  */
 int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, int64_t n_out,
                      int32_t L, int32_t K, const int32_t *length, const int32_t *dilation,
                      const int32_t *padding, const float *bias, const float *weights,
                      int32_t wstride, double *F, int64_t *cnt, int64_t *cnt_lo,
-                     int64_t *cnt_hi, double *beta_max, int nthreads) {
+                     int64_t *cnt_hi, double *beta_max, double *mpv, double *mpv_lo,
+                     double *mpv_hi, int nthreads) {
     if (!X || !length || !dilation || !padding || !bias || !weights || !F) return ORACLE_ERR_ARG;
     if (L < 1 || K < 1 || n_out < 0 || wstride < 1) return ORACLE_ERR_ARG;
     for (int32_t k = 0; k < K; ++k) {
@@ -103,6 +119,7 @@ int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, 
             const double tiny = (len + 1) * ldexp(1.0, -126);
             int64_t positive = 0, lo = 0, hi = 0;
             double mx = -INFINITY, bmax = 0.0;
+            double pos_sum = 0.0, sure_lo = 0.0, sure_hi = 0.0, maybe = 0.0, maybe_max = 0.0;
             for (int64_t t = 0; t < O; ++t) {
                 double y = b;
                 double mag = fabs(b);
@@ -113,8 +130,18 @@ int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, 
                     mag += fabs((double)w[j] * xv);
                 }
                 const double beta = g * mag + tiny;
-                if (y > 0.0) ++positive;
-                if (y > beta) ++lo;
+                if (y > 0.0) {
+                    ++positive;
+                    pos_sum += y;
+                }
+                if (y > beta) {
+                    ++lo;
+                    sure_lo += y - beta;
+                    sure_hi += y + beta;
+                } else if (y > -beta) {
+                    maybe += 2.0 * beta;
+                    if (2.0 * beta > maybe_max) maybe_max = 2.0 * beta;
+                }
                 if (y > -beta) ++hi;
                 if (y > mx) mx = y;
                 if (beta > bmax) bmax = beta;
@@ -125,6 +152,21 @@ int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, 
             if (cnt_lo) cnt_lo[r * (int64_t)K + k] = lo;
             if (cnt_hi) cnt_hi[r * (int64_t)K + k] = hi;
             if (beta_max) beta_max[r * (int64_t)K + k] = bmax;
+            if (mpv) mpv[r * (int64_t)K + k] = positive > 0 ? pos_sum / (double)positive : 0.0;
+            if (mpv_lo || mpv_hi) {
+                const double u = ldexp(1.0, -24);
+                const double gs = gamma_m((int)(hi > 0 ? hi : 1));
+                double mlo, mhi;
+                if (lo > 0) {
+                    mlo = sure_lo * (1.0 - gs) * (1.0 - u) / (double)hi;
+                    mhi = (sure_hi + maybe) * (1.0 + gs) * (1.0 + u) / (double)lo;
+                } else {
+                    mlo = 0.0;
+                    mhi = maybe_max * (1.0 + gs) * (1.0 + u);
+                }
+                if (mpv_lo) mpv_lo[r * (int64_t)K + k] = mlo;
+                if (mpv_hi) mpv_hi[r * (int64_t)K + k] = mhi;
+            }
         }
     }
     return ORACLE_OK;

@@ -72,7 +72,7 @@ def _load():
         lib.oracle_transform.restype = ctypes.c_int
         lib.oracle_transform.argtypes = [p, ctypes.c_int64, p, ctypes.c_int64, ctypes.c_int32,
                                          ctypes.c_int32, p, p, p, p, p, ctypes.c_int32,
-                                         p, p, p, p, p, ctypes.c_int]
+                                         p, p, p, p, p, p, p, p, ctypes.c_int]
         lib.oracle_output_length.restype = ctypes.c_int64
         lib.oracle_output_length.argtypes = [ctypes.c_int32] * 4
         lib.oracle_max_threads.restype = ctypes.c_int
@@ -106,6 +106,9 @@ def transform(X, kernels: dict, rows=None, threads: int = 0) -> dict:
       cnt_lo, cnt_hi int64 [m, K]: certified range of counts any fp32
                evaluation can give;
       beta     fp64 [m, K]: certified bound on |MAX_fp32 - MAX_exact|;
+      mpv      fp64 [m, K]: mean of the positive dot products (0 if none);
+      mpv_lo, mpv_hi fp64 [m, K]: certified range of MPV for any fp32
+               evaluation (see rocket_oracle.c);
       O        int64 [K]: number of dot products per kernel.
     ``rows`` selects a subset of rows (m = len(rows)); default all rows.
     """
@@ -132,14 +135,19 @@ def transform(X, kernels: dict, rows=None, threads: int = 0) -> dict:
     lo = np.empty((m, K), dtype=np.int64)
     hi = np.empty((m, K), dtype=np.int64)
     beta = np.empty((m, K), dtype=np.float64)
+    mpv = np.empty((m, K), dtype=np.float64)
+    mpv_lo = np.empty((m, K), dtype=np.float64)
+    mpv_hi = np.empty((m, K), dtype=np.float64)
     rc = _load().oracle_transform(_ptr(X), n, None if rows_arr is None else _ptr(rows_arr), m, L, K,
                                   _ptr(ln), _ptr(dl), _ptr(pd), _ptr(bs), _ptr(wt), wt.shape[1],
-                                  _ptr(F), _ptr(cnt), _ptr(lo), _ptr(hi), _ptr(beta), int(threads))
+                                  _ptr(F), _ptr(cnt), _ptr(lo), _ptr(hi), _ptr(beta), _ptr(mpv),
+                                  _ptr(mpv_lo), _ptr(mpv_hi), int(threads))
     if rc == ORACLE_ERR_LENGTH:
         raise ValueError("a kernel has no dot products on series of length %d" % L)
     if rc != ORACLE_OK:
         raise ValueError("oracle_transform rejected its arguments (code %d)" % rc)
-    return dict(F=F, cnt=cnt, cnt_lo=lo, cnt_hi=hi, beta=beta, O=output_lengths(kernels, L))
+    return dict(F=F, cnt=cnt, cnt_lo=lo, cnt_hi=hi, beta=beta, mpv=mpv, mpv_lo=mpv_lo, mpv_hi=mpv_hi,
+                O=output_lengths(kernels, L))
 
 
 # ---------------------------------------------------------------------------

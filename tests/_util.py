@@ -69,6 +69,33 @@ def brute_force(X, kernels):
     return F
 
 
+def brute_force_mpv(X, kernels):
+    """Mean of the strictly positive dot products per (row, kernel), 0 when
+    none is positive; literal Python loops in fp64, small inputs only."""
+    n, L = X.shape
+    K = len(kernels["length"])
+    out = np.zeros((n, K))
+    for i in range(n):
+        x = [float(v) for v in X[i]]
+        for k in range(K):
+            ln = int(kernels["length"][k])
+            d = int(kernels["dilation"][k])
+            p = int(kernels["padding"][k])
+            b = float(kernels["bias"][k])
+            w = [float(v) for v in kernels["weights"][k][:ln]]
+            pos = []
+            for t in range(L + 2 * p - (ln - 1) * d):
+                acc = b
+                for j in range(ln):
+                    m = t - p + j * d
+                    if 0 <= m < L:
+                        acc += w[j] * x[m]
+                if acc > 0:
+                    pos.append(acc)
+            out[i, k] = sum(pos) / len(pos) if pos else 0.0
+    return out
+
+
 def random_kernels(rng, K, L, max_len=MAX_LEN):
     """Random valid kernels (any length 1..11, any admissible dilation, either
     padding choice) for brute-force cross-checks."""
@@ -89,13 +116,14 @@ def random_kernels(rng, K, L, max_len=MAX_LEN):
     return kernel_set(lengths, dil, pad, bias, weights)
 
 
-def fp32_features(X, kernels, order="ascending"):
+def fp32_features(X, kernels, order="ascending", with_mpv=False):
     """fp32 evaluation in numpy with a chosen summation order, used to check
     that the oracle's certified intervals contain real fp32 results."""
     n, L = X.shape
     K = len(kernels["length"])
     cnt = np.zeros((n, K), dtype=np.int64)
     mx = np.zeros((n, K), dtype=np.float64)
+    mpv = np.zeros((n, K), dtype=np.float64)
     for k in range(K):
         ln = int(kernels["length"][k])
         d = int(kernels["dilation"][k])
@@ -113,7 +141,14 @@ def fp32_features(X, kernels, order="ascending"):
             y = (y + b).astype(np.float32)
         cnt[:, k] = (y > 0).sum(axis=1)
         mx[:, k] = y.max(axis=1)
-    return cnt, mx
+        if with_mpv:
+            # positive values summed in fp32 in output order, then one fp32 division
+            s32 = np.zeros(n, dtype=np.float32)
+            for t in range(O):
+                s32 = np.where(y[:, t] > 0, (s32 + y[:, t]).astype(np.float32), s32)
+            c = cnt[:, k].astype(np.float32)
+            mpv[:, k] = np.where(cnt[:, k] > 0, (s32 / np.maximum(c, 1)).astype(np.float32), 0.0)
+    return (cnt, mx, mpv) if with_mpv else (cnt, mx)
 
 
 def ceil_div(a, b):
@@ -127,7 +162,7 @@ def z_norm(x):
     return ((x - x.mean(axis=1, keepdims=True)) / sd).astype(np.float32)
 
 
-__all__ = ["load_golden", "kernel_set", "brute_force", "random_kernels", "fp32_features",
+__all__ = ["load_golden", "kernel_set", "brute_force", "brute_force_mpv", "random_kernels", "fp32_features",
            "ceil_div", "z_norm", "math"]
 
 

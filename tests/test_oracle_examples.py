@@ -3,7 +3,7 @@ literal brute-force loop on small random cases."""
 import numpy as np
 import pytest
 
-from _util import brute_force, kernel_set, load_golden, random_kernels
+from _util import brute_force, brute_force_mpv, kernel_set, load_golden, random_kernels
 
 GOLDEN = load_golden()
 
@@ -19,6 +19,9 @@ def test_worked_example(oracle, ex):
     assert r["F"][0, 0] == pytest.approx(ex["ppv"], abs=1e-15)
     assert r["F"][0, 1] == ex["max"]
     assert r["cnt"][0, 0] == int((y > 0).sum())
+    # MPV: the mean of the fixture's positive dot products (0 when none)
+    pos = y[y > 0]
+    assert r["mpv"][0, 0] == pytest.approx(pos.mean() if pos.size else 0.0, abs=1e-12)
     # the convolution (reversed-weight) reading must not reproduce these
     if (ex["flipped_ppv"], ex["flipped_max"]) != (ex["ppv"], ex["max"]):
         assert (r["F"][0, 0], r["F"][0, 1]) != pytest.approx((ex["flipped_ppv"], ex["flipped_max"]))
@@ -48,6 +51,7 @@ def test_brute_force_random(oracle, seed):
     ref = brute_force(X, ks)
     np.testing.assert_allclose(r["F"][:, 1::2], ref[:, 1::2], rtol=0, atol=1e-12)
     np.testing.assert_array_equal(r["F"][:, 0::2], ref[:, 0::2])
+    np.testing.assert_allclose(r["mpv"], brute_force_mpv(X, ks), rtol=0, atol=1e-12)
 
 
 def test_row_subset_matches_full(oracle):

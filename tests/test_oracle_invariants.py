@@ -25,6 +25,8 @@ def test_zero_series_gives_bias(oracle):
     b = ks["bias"].astype(np.float64)
     np.testing.assert_array_equal(r["F"][:, 1::2], np.broadcast_to(b, (2, 300)))
     np.testing.assert_array_equal(r["F"][:, 0::2], np.broadcast_to((b > 0).astype(float), (2, 300)))
+    # MPV: the mean of O copies of b when b > 0, else no positive value
+    np.testing.assert_array_equal(r["mpv"], np.broadcast_to(np.where(b > 0, b, 0.0), (2, 300)))
 
 
 def test_zero_bias_zero_series_is_not_positive(oracle):
@@ -133,6 +135,7 @@ def test_power_of_two_scaling(oracle):
         b = oracle.transform((X * np.float32(2.0 ** s)).astype(np.float32), ks)
         np.testing.assert_array_equal(b["F"][:, 0::2], a["F"][:, 0::2])
         np.testing.assert_array_equal(b["F"][:, 1::2], a["F"][:, 1::2] * 2.0 ** s)
+        np.testing.assert_array_equal(b["mpv"], a["mpv"] * 2.0 ** s)
 
 
 def test_range_and_consistency(oracle):
@@ -147,6 +150,11 @@ def test_range_and_consistency(oracle):
     assert np.abs(scaled - r["cnt"]).max() < 1e-9
     np.testing.assert_array_equal(ppv > 0, mx > 0)
     assert np.all(r["cnt_lo"] <= r["cnt"]) and np.all(r["cnt"] <= r["cnt_hi"])
+    # MPV is a mean of positive values: 0 exactly when PPV is 0, else in (0, MAX]
+    mpv = r["mpv"]
+    np.testing.assert_array_equal(mpv > 0, ppv > 0)
+    assert np.all(mpv[ppv > 0] <= mx[ppv > 0] * (1 + 1e-15))
+    assert np.all((r["mpv_lo"] <= mpv) & (mpv <= r["mpv_hi"]))
 
 
 @pytest.mark.parametrize("seed", range(3))
@@ -196,9 +204,14 @@ def test_certified_bounds_hold_for_fp32(oracle, order):
     ks = oracle.generate_kernels(51, 400, L)
     X = z_norm(rng.standard_normal((6, L)).cumsum(axis=1))
     r = oracle.transform(X, ks)
-    cnt32, mx32 = fp32_features(X, ks, order)
+    cnt32, mx32, mpv32 = fp32_features(X, ks, order, with_mpv=True)
     assert np.all(r["cnt_lo"] <= cnt32) and np.all(cnt32 <= r["cnt_hi"])
     assert np.all(np.abs(mx32 - r["F"][:, 1::2]) <= r["beta"])
+    assert np.all((r["mpv_lo"] <= mpv32) & (mpv32 <= r["mpv_hi"]))
+    # and the MPV range is narrow where no output is within beta of zero
+    tight = r["cnt_lo"] == r["cnt_hi"]
+    width = (r["mpv_hi"] - r["mpv_lo"])[tight & (r["cnt"] > 0)] / r["mpv"][tight & (r["cnt"] > 0)]
+    assert np.percentile(width, 99) < 2e-4 and width.max() < 1e-2
     # the interval is tight: it is a handful of outputs wide at most
     assert (r["cnt_hi"] - r["cnt_lo"]).max() <= 3
     assert r["beta"].max() < 1e-4
