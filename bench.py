@@ -83,6 +83,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample budget")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--direct", action="store_true", help="time the plain kernel instead")
+    ap.add_argument("--mpv", action="store_true",
+                    help="also compute the third feature, MPV (F has 3 columns per kernel)")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run one elementwise copy of this many MiB (reference for "
                          "hardware byte counters)")
@@ -122,13 +124,13 @@ def main():
     X = torch.from_numpy(X_np).to(dev)
 
     t0 = time.perf_counter()
-    plan = rk.Plan(ks, w.L, direct=args.direct)
+    plan = rk.Plan(ks, w.L, direct=args.direct, mpv=args.mpv)
     torch.cuda.synchronize()
     plan_ms = (time.perf_counter() - t0) * 1e3
     info = plan.info()
     log("plan: %s (%.1f ms)" % (info, plan_ms))
 
-    K2 = 2 * w.n_kernels
+    K2 = plan.n_features
     batch = args.batch_rows or (w.n if w.n * K2 * 4 <= F_RESIDENT_LIMIT else DEFAULT_BATCH_ROWS)
     batch = min(batch, w.n)
     F = torch.empty((batch, K2), dtype=torch.float32, device=dev)
@@ -172,7 +174,7 @@ def main():
     mfma_fma_per_pass = 256.0 * info["mfma_per_row"] * w.n
     pairs_per_s = w.n * w.n_kernels / (ms_per_step * 1e-3)
     digest = source_digest()
-    traffic = None if args.direct else traffic_from_profile(w.name, digest)
+    traffic = None if (args.direct or args.mpv) else traffic_from_profile(w.name, digest)
 
     # parity of sampled rows and the CPU baseline on the same rows
     cpu = None
@@ -208,14 +210,23 @@ def main():
             torch.cuda.synchronize()
             got[np.searchsorted(rows, sel)] = F[torch.from_numpy(sel - r0).to(dev)].cpu().numpy()
         O = ref["O"][None, :]
-        cnt = np.rint(got[:, 0::2].astype(np.float64) * O)
+        nf = plan.features_per_kernel
+        ppv, mxv = got[:, 0::nf], got[:, 1::nf]
+        cnt = np.rint(ppv.astype(np.float64) * O)
         parity = {
             "rows": int(rows.shape[0]),
-            "max_abs_err_max": float(np.abs(got[:, 1::2] - ref["F"][:, 1::2]).max()),
+            "max_abs_err_max": float(np.abs(mxv - ref["F"][:, 1::2]).max()),
             "max_count_err": int(np.abs(cnt - ref["cnt"]).max()),
             "outside_certified": int(((cnt < ref["cnt_lo"]) | (cnt > ref["cnt_hi"])).sum()
-                                     + (np.abs(got[:, 1::2] - ref["F"][:, 1::2]) > ref["beta"]).sum()),
+                                     + (np.abs(mxv - ref["F"][:, 1::2]) > ref["beta"]).sum()),
         }
+        if nf == 3:
+            mpv = got[:, 2::3].astype(np.float64)
+            parity["mpv_outside_certified"] = int(((mpv < ref["mpv_lo"]) | (mpv > ref["mpv_hi"])).sum())
+            same = cnt == ref["cnt"]
+            # error beyond the test rule 1e-4 * MPV + beta (0 when inside)
+            excess = np.abs(mpv - ref["mpv"]) - (1e-4 * np.abs(ref["mpv"]) + ref["beta"])
+            parity["mpv_max_excess_over_rule"] = float(max(0.0, excess[same].max()))
         log("parity %s" % parity)
 
     out = {

@@ -17,7 +17,9 @@
  *
  * Memory and threading rules for every entry point:
  *   - X (n x L fp32, row-major, contiguous) and F (n x 2 n_kernels fp32,
- *     row-major) are caller-owned DEVICE memory on the current HIP device.
+ *     row-major; n x 3 n_kernels with the MPV feature) are caller-owned
+ *     DEVICE memory on the current HIP device (rocket_transform_host takes
+ *     host memory instead).
  *     The library never frees them.  F is fully overwritten.
  *   - Kernel sets (rocket_kernels) live in HOST memory.
  *   - Every argument is validated on the host before any device work; an
@@ -119,18 +121,27 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
 #define ROCKET_PLAN_DEFAULT 0u
 #define ROCKET_PLAN_DIRECT 1u  /* use the plain one-wavefront-per-pair kernel */
 #define ROCKET_PLAN_CLAMPED 2u /* fused kernel with clamped indices (one-zero margins) */
+#define ROCKET_PLAN_MPV 4u     /* a third feature per kernel: mean of positive values */
 
 /*
  * rocket_plan_create with flags.  ROCKET_PLAN_DIRECT selects the plain
  * kernel: one wavefront per (series, kernel) pair reading the series from
  * global memory.  It is slower and serves as a second GPU reference; the
- * default plan also falls back to it when a series (plus the zero margins
- * the kernels need) does not fit one workgroup's LDS.  Unknown flag bits
- * give ROCKET_ERR_INVALID_ARG.  ROCKET_PLAN_CLAMPED forces the layout the
- * default plan picks for long series: rows staged with a single zero on each
- * side and every series index clamped into [-1, L] (same results; two more
- * instructions per load).  Both flags together are ROCKET_ERR_INVALID_ARG.
- * Same errors as rocket_plan_create otherwise.
+ * default plan also falls back to it when a series does not fit one
+ * workgroup's LDS even with clamped indices.  ROCKET_PLAN_CLAMPED forces the
+ * layout the default plan picks for long series: rows staged with a single
+ * zero on each side and every series index clamped into [-1, L] (same
+ * results; two more instructions per load).  ROCKET_PLAN_DIRECT together
+ * with ROCKET_PLAN_CLAMPED is ROCKET_ERR_INVALID_ARG.
+ * ROCKET_PLAN_MPV adds a third feature per kernel, the mean of the positive
+ * values (MPV; the CUROCKET paper, Sec. 5, names it as a feature that does
+ * not depend on time positions and so fuses into the same pass):
+ *     MPV = sum_{t : y_t > 0} y_t / |{t : y_t > 0}|, 0 when no y_t > 0,
+ * computed as the fp32 sum of the positive values divided in fp32 by the
+ * count.  The feature matrix is then F [n, 3 n_kernels], per kernel
+ * (PPV, MAX, MPV), and every entry point that writes F writes that layout
+ * for this plan.  Unknown flag bits give ROCKET_ERR_INVALID_ARG.  Same
+ * errors as rocket_plan_create otherwise.
  */
 rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t flags,
                                     rocket_plan **out);
@@ -140,8 +151,9 @@ rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t
 void rocket_plan_destroy(rocket_plan *p);
 
 /*
- * Transform n series with a plan: X_dev [n, L] -> F_dev [n, 2 n_kernels],
- * features in the ORIGINAL kernel order, interleaved (PPV, MAX) per kernel.
+ * Transform n series with a plan: X_dev [n, L] -> F_dev [n, f n_kernels],
+ * features in the ORIGINAL kernel order, interleaved (PPV, MAX) per kernel
+ * (f = 2), or (PPV, MAX, MPV) for a plan made with ROCKET_PLAN_MPV (f = 3).
  * Asynchronous on hip_stream (a hipStream_t; NULL = null stream).
  * n == 0 is a no-op.  Rows are independent; any row range of X may be
  * passed (row batching is the caller's loop over pointer offsets).
@@ -161,7 +173,7 @@ rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const r
                                float *F_dev, void *hip_stream);
 
 /*
- * Transform series held in HOST memory: X_host [n, L] -> F_host [n, 2K]
+ * Transform series held in HOST memory: X_host [n, L] -> F_host [n, f K]
  * (same layout and feature order as rocket_transform_plan).  Rows go
  * through the device in batches of batch_rows (0: about n/8 rows, at most
  * 256 MiB of staging per buffer).  Each
@@ -180,8 +192,7 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
                                     float *F_host, int64_t batch_rows, void *hip_stream);
 
 /*
- * Plan facts for benchmarks and tests (host only).  Any output pointer may
- * be NULL.
+ * Plan facts for benchmarks and tests (host only).
  *   n_items      number of work items (groups of kernels sharing one bucket)
  *   n_buckets    number of distinct (length, dilation, padding) buckets
  *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks)
@@ -189,13 +200,25 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *   direct       1 if the plan runs the direct kernel, else 0
  *   clamped      1 if the fused kernel stages rows with a single zero on
  *                each side and clamps series indices (chosen when the full
- *                zero margins of the padded kernels would not fit in LDS),
- *                else 0
- * Errors: ROCKET_ERR_INVALID_ARG if p is NULL.
+ *                zero margins of the padded kernels would not fit in LDS,
+ *                or forced by ROCKET_PLAN_CLAMPED), else 0
+ *   features_per_kernel  2 (PPV, MAX) or 3 (PPV, MAX, MPV)
+ *   rows_per_block       series staged per workgroup (0 for the direct kernel)
  */
-rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
-                               int64_t *mfma_per_row, int64_t *lds_bytes, int32_t *direct,
-                               int32_t *clamped);
+typedef struct {
+    int64_t n_items;
+    int64_t n_buckets;
+    int64_t mfma_per_row;
+    int64_t lds_bytes;
+    int32_t direct;
+    int32_t clamped;
+    int32_t features_per_kernel;
+    int32_t rows_per_block;
+} rocket_plan_facts;
+
+/* Fill *out with the plan's facts.  Errors: ROCKET_ERR_INVALID_ARG if p or
+ * out is NULL. */
+rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
 
 /*
  * Host-side work tables of the fused kernel, for tests and tools (no GPU is

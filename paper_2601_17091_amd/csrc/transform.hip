@@ -58,6 +58,7 @@ struct FusedArgs {
     int64_t n_rows;    // rows in this launch
     int32_t L;
     int32_t K;
+    int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV)
     const ItemDesc *items;
     const uint32_t *lanes;
     const float *wpk;
@@ -109,6 +110,16 @@ struct ClampedRow {
     __device__ __forceinline__ ClampedRow shifted(int k) const { return ClampedRow{row, i0 + k, d, L}; }
 };
 
+// Per-series accumulators of one work item, per lane and kernel slot: the
+// running max, the positive count (wavefront-uniform, scalar registers) and,
+// when MPV is computed, the sum of the positive values.
+template <int G>
+struct RowAcc {
+    v4f mx[G];
+    uint32_t cnt[G][4];
+    v4f ps[G];
+};
+
 // NS consecutive output steps of one round, as an outer-product contraction
 // over the taps.  The window of series values under the NS outputs
 // (NS + ELL - 1 values spaced d apart) is read from LDS first; then tap j of every step and kernel group is issued before tap j+1,
@@ -119,10 +130,9 @@ struct ClampedRow {
 // output short, or no chunk).  A chain started at -inf stays -inf, so MAX folds every
 // result (v_max3 over pairs of steps) and the positive count is a ballot of
 // y > 0 popcounted on the scalar unit.
-template <int ELL, int G, int NS, bool LAST, typename Src>
+template <int ELL, int G, int NS, bool LAST, bool MPV, typename Src>
 __device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][ELL],
-                                           const v4f (&binit)[G], bool drop_last,
-                                           v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+                                           const v4f (&binit)[G], bool drop_last, RowAcc<G> &ra) {
     float xw[NS + ELL - 1];
 #pragma unroll
     for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
@@ -152,80 +162,101 @@ __device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][g][v] > 0.0f));
+                ra.cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][g][v] > 0.0f));
+    if (MPV) {
+        // sum of the positive values (-inf and non-positive results add 0)
+#pragma unroll
+        for (int u = 0; u < NS; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) ra.ps[g][v] += fmaxf(acc[u][g][v], 0.0f);
+    }
 #pragma unroll
     for (int u = 0; u + 1 < NS; u += 2)
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
-                mx[g][v] = fmaxf(fmaxf(mx[g][v], acc[u][g][v]), acc[u + 1][g][v]);
+                ra.mx[g][v] = fmaxf(fmaxf(ra.mx[g][v], acc[u][g][v]), acc[u + 1][g][v]);
     if (NS % 2 == 1) {
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) mx[g][v] = fmaxf(mx[g][v], acc[NS - 1][g][v]);
+            for (int v = 0; v < 4; ++v) ra.mx[g][v] = fmaxf(ra.mx[g][v], acc[NS - 1][g][v]);
     }
 }
 
 // The last block of a round: its length nv (1..N) selects a code copy.
-template <int ELL, int G, int N, typename Src>
+template <int ELL, int G, int N, bool MPV, typename Src>
 struct TailBlock {
     __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
                                                const v4f (&binit)[G], bool drop_last,
-                                               v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+                                               RowAcc<G> &ra) {
         if (nv == N)
-            step_block<ELL, G, N, true>(src, wa, binit, drop_last, mx, cnt);
+            step_block<ELL, G, N, true, MPV>(src, wa, binit, drop_last, ra);
         else
-            TailBlock<ELL, G, N - 1, Src>::run(nv, src, wa, binit, drop_last, mx, cnt);
+            TailBlock<ELL, G, N - 1, MPV, Src>::run(nv, src, wa, binit, drop_last, ra);
     }
 };
 
-template <int ELL, int G, typename Src>
-struct TailBlock<ELL, G, 0, Src> {
+template <int ELL, int G, bool MPV, typename Src>
+struct TailBlock<ELL, G, 0, MPV, Src> {
     __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL],
-                                               const v4f (&)[G], bool, v4f (&)[G],
-                                               uint32_t (&)[G][4]) {}
+                                               const v4f (&)[G], bool, RowAcc<G> &) {}
 };
 
-template <int CTRL>
-__device__ __forceinline__ float dpp_max_row(float v) {
+// Combining operations of the wavefront reductions: max for MAX, sum for
+// the MPV numerator.
+struct OpMax {
+    __device__ __forceinline__ static float f(float a, float b) { return fmaxf(a, b); }
+};
+struct OpSum {
+    __device__ __forceinline__ static float f(float a, float b) { return a + b; }
+};
+
+template <typename Op, int CTRL>
+__device__ __forceinline__ float dpp_row_step(float v) {
     // every lane of a full row reads a valid lane for these controls, so the
-    // move can fold into v_max_f32's DPP source
+    // move can fold into the combining instruction's DPP source
     const int moved = __builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true);
-    return fmaxf(v, __int_as_float(moved));
+    return Op::f(v, __int_as_float(moved));
 }
 
-// Lane-wise max of two registers after swapping the upper 32 lanes of a
-// with the lower 32 lanes of b: lanes 0-31 then reduce a over lane pairs
+// Lane-wise combination of two registers after swapping the upper 32 lanes
+// of a with the lower 32 lanes of b: lanes 0-31 then reduce a over lane pairs
 // (i, i+32), lanes 32-63 reduce b.
+template <typename Op>
 __device__ __forceinline__ float fold32(float a, float b) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false,
                                                     false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // The same with 16-lane rows: odd rows of a swap with even rows of b, so
 // rows 0 and 2 of the result reduce a over row pairs, rows 1 and 3 reduce b.
+template <typename Op>
 __device__ __forceinline__ float fold16(float a, float b) {
     const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false,
                                                     false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return Op::f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
-// Max within each 16-lane row, broadcast to the row.
-__device__ __forceinline__ float row_max(float v) {
-    v = dpp_max_row<kDppQuadSwap1>(v);
-    v = dpp_max_row<kDppQuadSwap2>(v);
-    v = dpp_max_row<kDppRowHalfMirror>(v);
-    v = dpp_max_row<kDppRowMirror>(v);
+// Reduction within each 16-lane row, broadcast to the row.
+template <typename Op>
+__device__ __forceinline__ float row_reduce(float v) {
+    v = dpp_row_step<Op, kDppQuadSwap1>(v);
+    v = dpp_row_step<Op, kDppQuadSwap2>(v);
+    v = dpp_row_step<Op, kDppRowHalfMirror>(v);
+    v = dpp_row_step<Op, kDppRowMirror>(v);
     return v;
 }
 
-// Reduce the 4 slot maxima of one group over the wavefront: on return, every
-// lane of 16-lane row q holds the maximum of slot kSlotOfRow[q].
+// Reduce the 4 slot values of one group over the wavefront: on return, the
+// lanes of 16-lane row q hold the result of slot slot_of_row(q).
+template <typename Op>
 __device__ __forceinline__ float reduce4(const v4f &m) {
-    return row_max(fold16(fold32(m[0], m[1]), fold32(m[2], m[3])));
+    return row_reduce<Op>(fold16<Op>(fold32<Op>(m[0], m[1]), fold32<Op>(m[2], m[3])));
 }
 // fold32(m0, m1): lanes 0-31 slot 0, lanes 32-63 slot 1; fold16 of
 // (slot0|slot1) and (slot2|slot3): row 0 slot 0, row 1 slot 2, row 2 slot 1,
@@ -260,48 +291,49 @@ __device__ __forceinline__ void setup_round(const ItemDesc &it, int rd, const Fu
 
 // All steps of one round for one series; src.value(m) is the zero-padded
 // series value under tap m of the lane's step-0 output.
-template <int ELL, int G, int T, typename Src>
+template <int ELL, int G, int T, bool MPV, typename Src>
 __device__ __forceinline__ void run_round(const Src &src, int d, const RoundState<G> &st,
-                                          const float (&wa)[G][ELL], v4f (&mx)[G],
-                                          uint32_t (&cnt)[G][4]) {
+                                          const float (&wa)[G][ELL], RowAcc<G> &ra) {
     const int nfull = (st.len - 1) / T;  // full blocks before the last block
     const int nv = st.len - nfull * T;   // length of the last block, 1..T
     // block b starts b*T*d positions along the row: a wavefront-uniform
     // offset, so each load is one lane address plus a scalar
     for (int blk = 0; blk < nfull; ++blk) {
         const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
-        step_block<ELL, G, T, false>(src.shifted(off), wa, st.binit, st.drop_last, mx, cnt);
+        step_block<ELL, G, T, false, MPV>(src.shifted(off), wa, st.binit, st.drop_last, ra);
     }
-    TailBlock<ELL, G, T, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
-                                   wa, st.binit, st.drop_last, mx, cnt);
+    TailBlock<ELL, G, T, MPV, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
+                                        wa, st.binit, st.drop_last, ra);
 }
 
-template <int G>
-__device__ __forceinline__ void init_row(v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+template <int G, bool MPV>
+__device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        ra.mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        if (MPV) ra.ps[g] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int v = 0; v < 4; ++v) cnt[g][v] = 0;
+        for (int v = 0; v < 4; ++v) ra.cnt[g][v] = 0;
     }
 }
 
-// MAX over the wavefront (counts are already scalar), then one float2
-// {PPV, MAX} per kernel, written by lanes 0, 16, 32 and 48.
-template <int G>
-__device__ __forceinline__ void write_row(const v4f (&mx)[G], const uint32_t (&cnt)[G][4],
-                                          const int (&out_kernel)[G], double inv_O, int lane,
-                                          float *Frow) {
+// MAX (and the MPV numerator) over the wavefront (counts are already
+// scalar), then per kernel {PPV, MAX} (or {PPV, MAX, MPV}), written by lanes
+// 0, 16, 32 and 48.
+template <int G, bool MPV>
+__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&out_kernel)[G],
+                                          double inv_O, int lane, float *Frow) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        const float m = reduce4(mx[g]);
+        const float m = reduce4<OpMax>(ra.mx[g]);
+        const float psum = MPV ? reduce4<OpSum>(ra.ps[g]) : 0.0f;
         // the count of slot slot_of_row(q) for the lanes of row q
         // (readfirstlane keeps the four uniform counts independent scalars,
         // so the selects stay selects)
-        const uint32_t c0 = __builtin_amdgcn_readfirstlane(cnt[g][0]);
-        const uint32_t c1 = __builtin_amdgcn_readfirstlane(cnt[g][1]);
-        const uint32_t c2 = __builtin_amdgcn_readfirstlane(cnt[g][2]);
-        const uint32_t c3 = __builtin_amdgcn_readfirstlane(cnt[g][3]);
+        const uint32_t c0 = __builtin_amdgcn_readfirstlane(ra.cnt[g][0]);
+        const uint32_t c1 = __builtin_amdgcn_readfirstlane(ra.cnt[g][1]);
+        const uint32_t c2 = __builtin_amdgcn_readfirstlane(ra.cnt[g][2]);
+        const uint32_t c3 = __builtin_amdgcn_readfirstlane(ra.cnt[g][3]);
         uint32_t c = c0;
         c = lane >= 16 ? c2 : c;
         c = lane >= 32 ? c1 : c;
@@ -312,29 +344,38 @@ __device__ __forceinline__ void write_row(const v4f (&mx)[G], const uint32_t (&c
             // (relative) from one, while c * fl64(1/O) is within 2^-52 of
             // it, so rounding the double product to float gives the same
             // float as the fp32 division
-            float2 res;
-            res.x = (float)((double)c * inv_O);
-            res.y = m;
-            *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)out_kernel[g]) = res;
+            const float ppv = (float)((double)c * inv_O);
+            if (MPV) {
+                // rows of 3 floats: 4-byte aligned only
+                float *f = Frow + 3 * (int64_t)out_kernel[g];
+                f[0] = ppv;
+                f[1] = m;
+                f[2] = c > 0 ? psum / (float)c : 0.0f;
+            } else {
+                float2 res;
+                res.x = ppv;
+                res.y = m;
+                *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)out_kernel[g]) = res;
+            }
         }
     }
 }
 
 // One round over the series whose index 0 sits at `row` in LDS.
-template <int ELL, int G, int T, bool CLAMP>
+template <int ELL, int G, int T, bool CLAMP, bool MPV>
 __device__ __forceinline__ void run_row_round(const float *row, const ItemDesc &it, int L,
                                               const RoundState<G> &st, const float (&wa)[G][ELL],
-                                              v4f (&mx)[G], uint32_t (&cnt)[G][4]) {
+                                              RowAcc<G> &ra) {
     const int i0 = (int)st.pos - it.p;  // series index under tap 0 of step 0
     if (CLAMP)
-        run_round<ELL, G, T>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, mx, cnt);
+        run_round<ELL, G, T, MPV>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, ra);
     else
-        run_round<ELL, G, T>(PaddedRow{row + i0, it.d}, it.d, st, wa, mx, cnt);
+        run_round<ELL, G, T, MPV>(PaddedRow{row + i0, it.d}, it.d, st, wa, ra);
 }
 
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.
-template <int ELL, int G, bool CLAMP>
+template <int ELL, int G, bool CLAMP, bool MPV>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
     // steps per block: 8 (G = 1) or 6 (G = 2) independent accumulation
@@ -361,28 +402,26 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
     for (int g = 0; g < G; ++g)
         out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
-    const int64_t f_stride = 2 * (int64_t)a.K;
+    const int64_t f_stride = (int64_t)a.nf * a.K;
     RoundState<G> st;
     if (it.rounds == 1) {
         // one round (small dilations): its lane state serves every series
         setup_round<G>(it, 0, a, bias, lane, st);
         for (int r = 0; r < nrows; ++r) {
-            v4f mx[G];
-            uint32_t cnt[G][4];
-            init_row<G>(mx, cnt);
-            run_row_round<ELL, G, T, CLAMP>(rows0 + r * a.row_stride, it, a.L, st, wa, mx, cnt);
-            write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
+            RowAcc<G> ra;
+            init_row<G, MPV>(ra);
+            run_row_round<ELL, G, T, CLAMP, MPV>(rows0 + r * a.row_stride, it, a.L, st, wa, ra);
+            write_row<G, MPV>(ra, out_kernel, it.inv_O, lane, F0 + r * f_stride);
         }
     } else {
         for (int r = 0; r < nrows; ++r) {
-            v4f mx[G];
-            uint32_t cnt[G][4];
-            init_row<G>(mx, cnt);
+            RowAcc<G> ra;
+            init_row<G, MPV>(ra);
             for (int rd = 0; rd < it.rounds; ++rd) {
                 setup_round<G>(it, rd, a, bias, lane, st);
-                run_row_round<ELL, G, T, CLAMP>(rows0 + r * a.row_stride, it, a.L, st, wa, mx, cnt);
+                run_row_round<ELL, G, T, CLAMP, MPV>(rows0 + r * a.row_stride, it, a.L, st, wa, ra);
             }
-            write_row<G>(mx, cnt, out_kernel, it.inv_O, lane, F0 + r * f_stride);
+            write_row<G, MPV>(ra, out_kernel, it.inv_O, lane, F0 + r * f_stride);
         }
     }
 }
@@ -407,7 +446,7 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
 }
 
 // Items of one variant, taken one at a time from the workgroup's counter.
-template <int ELL, int G, bool CLAMP>
+template <int ELL, int G, bool CLAMP, bool MPV>
 __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items,
                                           const float *rows0, int nrows, const FusedArgs &a,
                                           float *F0, int lane) {
@@ -417,13 +456,13 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
         idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
         if (idx >= cnt_items) break;
         const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
-        run_item<ELL, G, CLAMP>(it, rows0, nrows, a, F0, lane);
+        run_item<ELL, G, CLAMP, MPV>(it, rows0, nrows, a, F0, lane);
     }
 }
 
 // Workgroup = (variant, row tile, split); each workgroup stages its row tile
 // in LDS and runs the items of one variant over it.
-template <int BLOCK, bool CLAMP>
+template <int BLOCK, bool CLAMP, bool MPV>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
@@ -462,15 +501,15 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     __syncthreads();
 
     const int lane = threadIdx.x & (rocket::kWave - 1);
-    float *F0 = a.F + grow * 2 * (int64_t)a.K;
+    float *F0 = a.F + grow * (int64_t)a.nf * a.K;
     const float *rows0 = smem + a.halo_lo;
     switch (variant) {
-        case 0: run_items<7, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 1: run_items<7, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 2: run_items<9, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 3: run_items<9, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 4: run_items<11, 1, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        default: run_items<11, 2, CLAMP>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 0: run_items<7, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 1: run_items<7, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 2: run_items<9, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 3: run_items<9, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 4: run_items<11, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        default: run_items<11, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
     }
 }
 
@@ -481,7 +520,7 @@ __global__ __launch_bounds__(kBlock) void rocket_direct_kernel(
     const float *__restrict__ X, int64_t row0, int32_t L, int32_t K, int32_t k0,
     const int32_t *__restrict__ len, const int32_t *__restrict__ dil,
     const int32_t *__restrict__ pad, const float *__restrict__ bias,
-    const float *__restrict__ w, int32_t max_len, float *__restrict__ F) {
+    const float *__restrict__ w, int32_t max_len, int32_t nf, float *__restrict__ F) {
     const int64_t row = row0 + blockIdx.x;
     const int k = k0 + (int)blockIdx.y * (kBlock / 64) + (int)(threadIdx.x >> 6);
     if (k >= K) return;
@@ -491,7 +530,7 @@ __global__ __launch_bounds__(kBlock) void rocket_direct_kernel(
     const float *wk = w + (int64_t)k * max_len;
     const int64_t O = (int64_t)L + 2 * (int64_t)p - (int64_t)(ell - 1) * d;
     const float *x = X + row * (int64_t)L;
-    float mx = -INFINITY;
+    float mx = -INFINITY, ps = 0.0f;
     uint32_t c = 0;
     for (int64_t t = lane; t < O; t += 64) {
         float acc = b;
@@ -501,18 +540,20 @@ __global__ __launch_bounds__(kBlock) void rocket_direct_kernel(
             acc = fmaf(wk[j], xv, acc);
         }
         c += acc > 0.0f ? 1u : 0u;
+        ps += acc > 0.0f ? acc : 0.0f;
         mx = fmaxf(mx, acc);
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         mx = fmaxf(mx, __shfl_xor(mx, off, 64));
         c += __shfl_xor(c, off, 64);
+        ps += __shfl_xor(ps, off, 64);
     }
     if (lane == 0) {
-        float2 r;
-        r.x = (float)c / (float)O;
-        r.y = mx;
-        *reinterpret_cast<float2 *>(F + row * 2 * (int64_t)K + 2 * (int64_t)k) = r;
+        float *f = F + row * (int64_t)nf * K + (int64_t)nf * k;
+        f[0] = (float)c / (float)O;
+        f[1] = mx;
+        if (nf == 3) f[2] = c > 0 ? ps / (float)c : 0.0f;
     }
 }
 
@@ -541,6 +582,7 @@ struct rocket_plan {
     int n_cu = 0;
     bool direct = false;
     bool clamp = false;      // rows staged with one-zero margins, indices clamped
+    bool mpv = false;        // third feature per kernel: mean of positive values
     int32_t halo_lo = 0;     // staged layout actually used (floats)
     int32_t row_stride = 0;
     int32_t tail_pad = 0;
@@ -579,7 +621,7 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
                                                rocket_plan **out) {
     if (!out) return ROCKET_ERR_INVALID_ARG;
     *out = nullptr;
-    if ((flags & ~(ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED)) ||
+    if ((flags & ~(ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED | ROCKET_PLAN_MPV)) ||
         ((flags & ROCKET_PLAN_DIRECT) && (flags & ROCKET_PLAN_CLAMPED)))
         return ROCKET_ERR_INVALID_ARG;
     rocket_status st = rocket::validate_kernels(k, L);
@@ -599,6 +641,7 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         return ROCKET_ERR_HIP;
     }
     p->n_cu = prop.multiProcessorCount;
+    p->mpv = (flags & ROCKET_PLAN_MPV) != 0;
     // Staged layout: rows with zero margins wide enough for every padded tap
     // if that fits one workgroup's LDS, else rows with one zero on each side
     // and clamped indices, else the direct kernel.  Rows per workgroup: as
@@ -643,10 +686,14 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
         if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
         if (e == hipSuccess && lds > 64 * 1024) {
-            const void *fns[] = {(const void *)rocket_fused_kernel<kBlock, false>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, false>,
-                                 (const void *)rocket_fused_kernel<kBlock, true>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, true>};
+            const void *fns[] = {(const void *)rocket_fused_kernel<kBlock, false, false>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, false, false>,
+                                 (const void *)rocket_fused_kernel<kBlock, true, false>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, true, false>,
+                                 (const void *)rocket_fused_kernel<kBlock, false, true>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, false, true>,
+                                 (const void *)rocket_fused_kernel<kBlock, true, true>,
+                                 (const void *)rocket_fused_kernel<kBigBlock, true, true>};
             for (const void *f : fns)
                 if (e == hipSuccess)
                     e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -671,16 +718,16 @@ extern "C" void rocket_plan_destroy(rocket_plan *p) {
     delete p;
 }
 
-extern "C" rocket_status rocket_plan_info(const rocket_plan *p, int64_t *n_items, int64_t *n_buckets,
-                                          int64_t *mfma_per_row, int64_t *lds_bytes,
-                                          int32_t *direct, int32_t *clamped) {
-    if (!p) return ROCKET_ERR_INVALID_ARG;
-    if (n_items) *n_items = (int64_t)p->host.items.size();
-    if (n_buckets) *n_buckets = p->host.n_buckets;
-    if (mfma_per_row) *mfma_per_row = p->host.mfma_per_row;
-    if (lds_bytes) *lds_bytes = p->lds_bytes;
-    if (direct) *direct = p->direct ? 1 : 0;
-    if (clamped) *clamped = p->clamp ? 1 : 0;
+extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out) {
+    if (!p || !out) return ROCKET_ERR_INVALID_ARG;
+    out->n_items = (int64_t)p->host.items.size();
+    out->n_buckets = p->host.n_buckets;
+    out->mfma_per_row = p->host.mfma_per_row;
+    out->lds_bytes = p->lds_bytes;
+    out->direct = p->direct ? 1 : 0;
+    out->clamped = p->clamp ? 1 : 0;
+    out->features_per_kernel = p->mpv ? 3 : 2;
+    out->rows_per_block = p->direct ? 0 : p->rows_per_block;
     return ROCKET_OK;
 }
 
@@ -697,7 +744,7 @@ static rocket_status launch_direct(const rocket_plan *p, const float *X, int64_t
             dim3 grid((unsigned)nr, (unsigned)((nk + per_block - 1) / per_block));
             hipLaunchKernelGGL(rocket_direct_kernel, grid, dim3(kBlock), 0, s, X, r0, p->host.L, K,
                                (int32_t)k0, p->d_len, p->d_dil, p->d_pad, p->d_b, p->d_w,
-                               p->max_len, F);
+                               p->max_len, p->mpv ? 3 : 2, F);
             if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
         }
     }
@@ -720,6 +767,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.F = F;
     a.L = p->host.L;
     a.K = p->host.n_kernels;
+    a.nf = p->mpv ? 3 : 2;
     a.items = p->d_items;
     a.lanes = p->d_lanes;
     a.wpk = p->d_wpk;
@@ -747,14 +795,21 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)p->lds_bytes;
         const bool big = row_bytes > kBigLds;
-        if (p->clamp && big)
-            hipLaunchKernelGGL((rocket_fused_kernel<kBigBlock, true>), dim3(nb), dim3(kBigBlock), lds, s, a);
-        else if (p->clamp)
-            hipLaunchKernelGGL((rocket_fused_kernel<kBlock, true>), dim3(nb), dim3(kBlock), lds, s, a);
-        else if (big)
-            hipLaunchKernelGGL((rocket_fused_kernel<kBigBlock, false>), dim3(nb), dim3(kBigBlock), lds, s, a);
-        else
-            hipLaunchKernelGGL((rocket_fused_kernel<kBlock, false>), dim3(nb), dim3(kBlock), lds, s, a);
+        // one instance per (block size, layout, feature count)
+        auto go = [&](auto kern, int block) {
+            hipLaunchKernelGGL(kern, dim3(nb), dim3(block), lds, s, a);
+        };
+        const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0);
+        switch (sel) {
+            case 0: go(rocket_fused_kernel<kBlock, false, false>, kBlock); break;
+            case 1: go(rocket_fused_kernel<kBigBlock, false, false>, kBigBlock); break;
+            case 2: go(rocket_fused_kernel<kBlock, true, false>, kBlock); break;
+            case 3: go(rocket_fused_kernel<kBigBlock, true, false>, kBigBlock); break;
+            case 4: go(rocket_fused_kernel<kBlock, false, true>, kBlock); break;
+            case 5: go(rocket_fused_kernel<kBigBlock, false, true>, kBigBlock); break;
+            case 6: go(rocket_fused_kernel<kBlock, true, true>, kBlock); break;
+            default: go(rocket_fused_kernel<kBigBlock, true, true>, kBigBlock); break;
+        }
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
     }
     return ROCKET_OK;
@@ -780,7 +835,7 @@ extern "C" rocket_status rocket_transform_host(const rocket_plan *p, const float
     if (!p || n < 0 || batch_rows < 0) return ROCKET_ERR_INVALID_ARG;
     if (n == 0) return ROCKET_OK;
     if (!X_host || !F_host) return ROCKET_ERR_INVALID_ARG;
-    const int64_t L = p->host.L, K2 = 2 * (int64_t)p->host.n_kernels;
+    const int64_t L = p->host.L, K2 = (int64_t)(p->mpv ? 3 : 2) * p->host.n_kernels;
     int64_t B = batch_rows;
     // default: about 8 batches, so copies have neighbours to overlap with,
     // each within 256 MiB of staging

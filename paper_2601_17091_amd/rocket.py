@@ -24,6 +24,7 @@ ROCKET_ERR_INTERNAL = -5
 ROCKET_PLAN_DEFAULT = 0
 ROCKET_PLAN_DIRECT = 1
 ROCKET_PLAN_CLAMPED = 2
+ROCKET_PLAN_MPV = 4
 MAX_KERNEL_LENGTH = 11
 
 # every symbol include/rocket.h declares
@@ -59,6 +60,15 @@ class CKernels(ctypes.Structure):
         ("padding", ctypes.POINTER(ctypes.c_int32)),
         ("bias", ctypes.POINTER(ctypes.c_float)),
         ("weights", ctypes.POINTER(ctypes.c_float)),
+    ]
+
+
+class CPlanFacts(ctypes.Structure):
+    _fields_ = [
+        ("n_items", ctypes.c_int64), ("n_buckets", ctypes.c_int64),
+        ("mfma_per_row", ctypes.c_int64), ("lds_bytes", ctypes.c_int64),
+        ("direct", ctypes.c_int32), ("clamped", ctypes.c_int32),
+        ("features_per_kernel", ctypes.c_int32), ("rows_per_block", ctypes.c_int32),
     ]
 
 
@@ -107,7 +117,7 @@ def library() -> ctypes.CDLL:
     lib.rocket_transform.restype = ctypes.c_int
     lib.rocket_transform_host.argtypes = [vp, vp, i64, vp, i64, vp]
     lib.rocket_transform_host.restype = ctypes.c_int
-    lib.rocket_plan_info.argtypes = [vp] + [ctypes.POINTER(i64)] * 4 + [ctypes.POINTER(i32)] * 2
+    lib.rocket_plan_info.argtypes = [vp, ctypes.POINTER(CPlanFacts)]
     lib.rocket_plan_info.restype = ctypes.c_int
     lib.rocket_plan_tables_build.argtypes = [kp, i32, ctypes.POINTER(CPlanTables)]
     lib.rocket_plan_tables_build.restype = ctypes.c_int
@@ -217,34 +227,41 @@ def _check_series(X, L: int):
 class Plan:
     """rocket_plan: a kernel set planned for series of length L on the current device."""
 
-    def __init__(self, kernels: dict, L: int, direct: bool = False, clamped: bool = False):
+    def __init__(self, kernels: dict, L: int, direct: bool = False, clamped: bool = False,
+                 mpv: bool = False):
         lib = library()
         self._c, self._keep = as_c_kernels(kernels)
         self.n_kernels = int(self._c.n_kernels)
         self.L = int(L)
         h = ctypes.c_void_p()
-        flags = (ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT) | (ROCKET_PLAN_CLAMPED if clamped else 0)
+        flags = ((ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT)
+                 | (ROCKET_PLAN_CLAMPED if clamped else 0) | (ROCKET_PLAN_MPV if mpv else 0))
         _check(lib.rocket_plan_create_ex(ctypes.byref(self._c), self.L, flags, ctypes.byref(h)),
                "rocket_plan_create")
         self._h = h
+        self.features_per_kernel = 3 if mpv else 2
 
     def info(self) -> dict:
-        vals = [ctypes.c_int64() for _ in range(4)]
-        direct, clamped = ctypes.c_int32(), ctypes.c_int32()
-        _check(library().rocket_plan_info(self._h, *[ctypes.byref(v) for v in vals], ctypes.byref(direct),
-                                          ctypes.byref(clamped)),
-               "rocket_plan_info")
-        return dict(n_items=vals[0].value, n_buckets=vals[1].value, mfma_per_row=vals[2].value,
-                    lds_bytes=vals[3].value, direct=bool(direct.value), clamped=bool(clamped.value))
+        f = CPlanFacts()
+        _check(library().rocket_plan_info(self._h, ctypes.byref(f)), "rocket_plan_info")
+        return dict(n_items=f.n_items, n_buckets=f.n_buckets, mfma_per_row=f.mfma_per_row,
+                    lds_bytes=f.lds_bytes, direct=bool(f.direct), clamped=bool(f.clamped),
+                    features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block)
+
+    @property
+    def n_features(self) -> int:
+        """Columns of F: features_per_kernel * n_kernels."""
+        return self.features_per_kernel * self.n_kernels
 
     def transform_into(self, X, F, stream=None):
-        """F[n, 2K] <- features of X[n, L]; asynchronous on `stream`."""
+        """F[n, fK] <- features of X[n, L] (f = 2, or 3 with MPV);
+        asynchronous on `stream`."""
         import torch
         _check_series(X, self.L)
         n = X.shape[0]
         if (not isinstance(F, torch.Tensor) or not F.is_cuda or F.dtype != torch.float32
-                or tuple(F.shape) != (n, 2 * self.n_kernels) or not F.is_contiguous()):
-            raise ValueError("F must be contiguous float32 [n, 2*n_kernels] on the GPU")
+                or tuple(F.shape) != (n, self.n_features) or not F.is_contiguous()):
+            raise ValueError("F must be contiguous float32 [n, %d] on the GPU" % self.n_features)
         if X.device != F.device:
             raise ValueError("X and F must be on the same device")
         _check(library().rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), n,
@@ -254,11 +271,11 @@ class Plan:
 
     def transform(self, X, stream=None):
         import torch
-        F = torch.empty((X.shape[0], 2 * self.n_kernels), dtype=torch.float32, device=X.device)
+        F = torch.empty((X.shape[0], self.n_features), dtype=torch.float32, device=X.device)
         return self.transform_into(X, F, stream)
 
     def transform_host(self, X_host, F_host, batch_rows: int = 0, stream=None):
-        """F_host[n, 2K] <- features of X_host[n, L], both in host memory
+        """F_host[n, fK] <- features of X_host[n, L], both in host memory
         (CPU torch tensors, pinned for overlap, or numpy arrays); copies and
         transforms of successive row batches overlap.  Blocks until done."""
         import torch
@@ -270,8 +287,8 @@ class Plan:
             raise ValueError("X_host must be a contiguous float32 [n, %d] array" % self.L)
         n = X_t.shape[0]
         if (F_t.dtype != torch.float32 or not F_t.is_contiguous()
-                or tuple(F_t.shape) != (n, 2 * self.n_kernels)):
-            raise ValueError("F_host must be a contiguous float32 [%d, %d] array" % (n, 2 * self.n_kernels))
+                or tuple(F_t.shape) != (n, self.n_features)):
+            raise ValueError("F_host must be a contiguous float32 [%d, %d] array" % (n, self.n_features))
         if stream is None:
             stream = torch.cuda.current_stream()
         _check(library().rocket_transform_host(self._h, ctypes.c_void_p(X_t.data_ptr()), n,

@@ -206,3 +206,44 @@ def assert_parity(F_gpu, ref, what=""):
     assert r["outside_count_interval"] == 0, (what, r)
     assert r["max_beyond_bound"] == 0, (what, r)
     return r
+
+
+# ---------------------------------------------------------------------------
+# MPV parity (the optional third feature)
+# ---------------------------------------------------------------------------
+MPV_REL_TOL = 1e-4   # |MPV_gpu - MPV_oracle| <= MPV_REL_TOL * MPV_oracle + beta
+                     # where the GPU's count equals the oracle's
+
+
+def split_mpv(F3):
+    """[m, 3K] (PPV, MAX, MPV per kernel) -> ([m, 2K] (PPV, MAX), [m, K] MPV)."""
+    F3 = np.asarray(F3)
+    m, K3 = F3.shape
+    K = K3 // 3
+    F2 = np.empty((m, 2 * K), dtype=F3.dtype)
+    F2[:, 0::2] = F3[:, 0::3]
+    F2[:, 1::2] = F3[:, 1::3]
+    return F2, F3[:, 2::3]
+
+
+def assert_mpv_parity(F3, ref, what=""):
+    """PPV and MAX under the usual rule; MPV inside the oracle's certified
+    fp32 range and, where the GPU counted the same positives as the oracle,
+    within MPV_REL_TOL * MPV + beta of it.  beta (the oracle's bound on any
+    one dot product's fp32 error) covers the error the averaged values carry;
+    the relative part covers the kernel's own summation: each lane adds at
+    most ceil(O/64) values in sequence and a 64-lane tree adds 6 more
+    roundings, (O/64 + 6) * 2^-24 < 1e-4 for every O below 2^24 / 100."""
+    F2, mpv = split_mpv(F3)
+    r = assert_parity(F2, ref, what)
+    mpv = np.asarray(mpv, dtype=np.float64)
+    assert np.all(np.isfinite(mpv)), what
+    inside = (mpv >= ref["mpv_lo"]) & (mpv <= ref["mpv_hi"])
+    assert inside.all(), (what, int((~inside).sum()))
+    cnt = np.rint(F2[:, 0::2].astype(np.float64) * ref["O"][None, :]).astype(np.int64)
+    same = cnt == ref["cnt"]
+    err = np.abs(mpv - ref["mpv"])[same]
+    lim = (MPV_REL_TOL * np.abs(ref["mpv"]) + ref["beta"])[same]
+    assert np.all(err <= lim), (what, float((err - lim).max()))
+    r["mpv_max_rel_err"] = float((err / np.maximum(np.abs(ref["mpv"][same]), 1e-30)).max()) if err.size else 0.0
+    return r

@@ -108,7 +108,7 @@ def test_plan_validation_null_and_flags(lib):
     k = _kernels()
     c, keep = rb.as_c_kernels(k)
     assert lib.rocket_plan_create(ctypes.byref(c), 100, None) == rb.ROCKET_ERR_INVALID_ARG
-    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, 4, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, 8, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
     both = rb.ROCKET_PLAN_DIRECT | rb.ROCKET_PLAN_CLAMPED
     assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, both, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
     bad = rb.CKernels(2, 0, 11, c.length, c.dilation, c.padding, c.bias, None)
@@ -134,7 +134,7 @@ def test_transform_validation(lib):
     # n == 0 is a no-op that never touches memory
     assert lib.rocket_transform(None, 0, 100, ctypes.byref(c), None, None) == rb.ROCKET_OK
     assert lib.rocket_transform_plan(None, dummy, 1, dummy, None) == rb.ROCKET_ERR_INVALID_ARG
-    assert lib.rocket_plan_info(None, None, None, None, None, None, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_info(None, None) == rb.ROCKET_ERR_INVALID_ARG
     assert lib.rocket_transform_host(None, dummy, 1, dummy, 0, None) == rb.ROCKET_ERR_INVALID_ARG
 
 
