@@ -49,8 +49,19 @@
  * with c = cnt_hi; when cnt_lo = 0 the range is [0, max_maybe 2 beta_t
  * (1 + gamma_c)(1 + u)].
  *
- * Plain loops: rows -> kernels -> t -> j.  No SIMD intrinsics, no fast-math.
- * OpenMP only splits rows across threads (for timing the CPU baseline).
+ * Multivariate series (Sec. 3.3): a series has C channels, x_c[0..L-1].
+ * Each kernel reads its own subset of channels, channel_count[k] of them
+ * with ids channel_index[k*C + s], s < channel_count[k], and has one row
+ * of weights per channel it reads; its dot product sums over those channels
+ * and taps:
+ *       y_t = b + sum_s sum_j w[s][j] * xz_{c_s}[t - p + j d]
+ * (a univariate set is the case C = 1, every kernel reading channel 0).
+ * beta_t then counts all channel_count * l products:
+ *       beta_t = gamma_{m+1} (|b| + sum |w x|) + (m+1) 2^-126,  m = count * l.
+ *
+ * Plain loops: rows -> kernels -> t -> channels -> j.  No SIMD intrinsics,
+ * no fast-math.  OpenMP only splits rows across threads (for timing the CPU
+ * baseline).
  */
 #include <math.h>
 #include <stddef.h>
@@ -72,27 +83,39 @@ int64_t oracle_output_length(int32_t L, int32_t length, int32_t dilation, int32_
 }
 
 /*
- * X        : fp32 [n_rows_total, L] row-major.
+ * X        : fp32 [n_rows_total, C, L] row-major (C = n_channels; C = 1 for
+ *            univariate series, [n_rows_total, L]).
  * rows     : optional list of n_out row indices into X (NULL: rows 0..n_out-1).
- * kernels  : SoA arrays of K kernels; weights row stride wstride (>= length).
+ * kernels  : SoA arrays of K kernels; weights of kernel k, channel slot s,
+ *            tap j at weights[(k*C + s)*wstride + j] (wstride >= length).
+ * channel_count, channel_index : per kernel, the channels it reads (see
+ *            above); both may be NULL when C == 1.
  * F        : fp64 [n_out, 2K]  (PPV, MAX interleaved per kernel).
  * cnt, cnt_lo, cnt_hi : int64 [n_out, K] (may be NULL).
  * beta_max : fp64 [n_out, K] (may be NULL).
  * mpv, mpv_lo, mpv_hi : fp64 [n_out, K] (may be NULL).
  * nthreads : OpenMP threads (<= 0: runtime default).
  */
-int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, int64_t n_out,
-                     int32_t L, int32_t K, const int32_t *length, const int32_t *dilation,
-                     const int32_t *padding, const float *bias, const float *weights,
-                     int32_t wstride, double *F, int64_t *cnt, int64_t *cnt_lo,
-                     int64_t *cnt_hi, double *beta_max, double *mpv, double *mpv_lo,
-                     double *mpv_hi, int nthreads) {
+int oracle_transform_mc(const float *X, int64_t n_rows_total, const int64_t *rows, int64_t n_out,
+                        int32_t C, int32_t L, int32_t K, const int32_t *length,
+                        const int32_t *dilation, const int32_t *padding, const float *bias,
+                        const float *weights, int32_t wstride, const int32_t *channel_count,
+                        const int32_t *channel_index, double *F, int64_t *cnt, int64_t *cnt_lo,
+                        int64_t *cnt_hi, double *beta_max, double *mpv, double *mpv_lo,
+                        double *mpv_hi, int nthreads) {
     if (!X || !length || !dilation || !padding || !bias || !weights || !F) return ORACLE_ERR_ARG;
-    if (L < 1 || K < 1 || n_out < 0 || wstride < 1) return ORACLE_ERR_ARG;
+    if (C < 1 || L < 1 || K < 1 || n_out < 0 || wstride < 1) return ORACLE_ERR_ARG;
+    if (C > 1 && (!channel_count || !channel_index)) return ORACLE_ERR_ARG;
     for (int32_t k = 0; k < K; ++k) {
         if (length[k] < 1 || length[k] > wstride || dilation[k] < 1 || padding[k] < 0)
             return ORACLE_ERR_ARG;
         if (oracle_output_length(L, length[k], dilation[k], padding[k]) < 1) return ORACLE_ERR_LENGTH;
+        if (C > 1) {
+            if (channel_count[k] < 1 || channel_count[k] > C) return ORACLE_ERR_ARG;
+            for (int32_t s = 0; s < channel_count[k]; ++s)
+                if (channel_index[(int64_t)k * C + s] < 0 || channel_index[(int64_t)k * C + s] >= C)
+                    return ORACLE_ERR_ARG;
+        }
     }
     if (rows) {
         for (int64_t r = 0; r < n_out; ++r)
@@ -109,25 +132,30 @@ int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, 
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t r = 0; r < n_out; ++r) {
         const int64_t row = rows ? rows[r] : r;
-        const float *x = X + row * (int64_t)L;
+        const float *xrow = X + row * (int64_t)C * L;
         for (int32_t k = 0; k < K; ++k) {
             const int32_t len = length[k], d = dilation[k], p = padding[k];
-            const float *w = weights + (int64_t)k * wstride;
+            const int32_t nch = C > 1 ? channel_count[k] : 1;
             const double b = (double)bias[k];
             const int64_t O = oracle_output_length(L, len, d, p);
-            const double g = gamma_m(len + 1);
-            const double tiny = (len + 1) * ldexp(1.0, -126);
+            const double g = gamma_m(nch * len + 1);
+            const double tiny = (nch * len + 1) * ldexp(1.0, -126);
             int64_t positive = 0, lo = 0, hi = 0;
             double mx = -INFINITY, bmax = 0.0;
             double pos_sum = 0.0, sure_lo = 0.0, sure_hi = 0.0, maybe = 0.0, maybe_max = 0.0;
             for (int64_t t = 0; t < O; ++t) {
                 double y = b;
                 double mag = fabs(b);
-                for (int32_t j = 0; j < len; ++j) {
-                    const int64_t m = t - p + (int64_t)j * d;
-                    const double xv = (m >= 0 && m < L) ? (double)x[m] : 0.0;
-                    y += (double)w[j] * xv;
-                    mag += fabs((double)w[j] * xv);
+                for (int32_t s = 0; s < nch; ++s) {
+                    const int32_t c = C > 1 ? channel_index[(int64_t)k * C + s] : 0;
+                    const float *x = xrow + (int64_t)c * L;
+                    const float *w = weights + ((int64_t)k * C + s) * wstride;
+                    for (int32_t j = 0; j < len; ++j) {
+                        const int64_t m = t - p + (int64_t)j * d;
+                        const double xv = (m >= 0 && m < L) ? (double)x[m] : 0.0;
+                        y += (double)w[j] * xv;
+                        mag += fabs((double)w[j] * xv);
+                    }
                 }
                 const double beta = g * mag + tiny;
                 if (y > 0.0) {
@@ -170,6 +198,18 @@ int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, 
         }
     }
     return ORACLE_OK;
+}
+
+/* Univariate series [n_rows_total, L]: the multichannel loop with C = 1. */
+int oracle_transform(const float *X, int64_t n_rows_total, const int64_t *rows, int64_t n_out,
+                     int32_t L, int32_t K, const int32_t *length, const int32_t *dilation,
+                     const int32_t *padding, const float *bias, const float *weights,
+                     int32_t wstride, double *F, int64_t *cnt, int64_t *cnt_lo,
+                     int64_t *cnt_hi, double *beta_max, double *mpv, double *mpv_lo,
+                     double *mpv_hi, int nthreads) {
+    return oracle_transform_mc(X, n_rows_total, rows, n_out, 1, L, K, length, dilation, padding,
+                               bias, weights, wstride, NULL, NULL, F, cnt, cnt_lo, cnt_hi, beta_max,
+                               mpv, mpv_lo, mpv_hi, nthreads);
 }
 
 /* Threads the OpenMP runtime would use (reported with the CPU baseline). */
