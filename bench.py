@@ -34,18 +34,21 @@ def log(msg):
 
 def valid_taps(kernels, L):
     """Products whose series index lands inside [0, L) (padding zeros excluded),
-    summed over kernels: the algorithmic FMA count of one series."""
+    summed over kernels (and, for multivariate sets, over the channels each
+    kernel reads): the algorithmic FMA count of one series."""
     ln = kernels["length"].astype(np.int64)
     d = kernels["dilation"].astype(np.int64)
     p = kernels["padding"].astype(np.int64)
+    ch = (kernels["channel_count"].astype(np.int64) if int(kernels.get("n_channels", 1)) > 1
+          else np.ones_like(ln))
     O = L + 2 * p - (ln - 1) * d
     total = 0
     for j in range(11):
         on = j < ln
         lo = np.maximum(0, p - j * d)
         hi = np.minimum(O, p - j * d + L)
-        total += int(np.where(on, np.maximum(0, hi - lo), 0).sum())
-    nominal = int((ln * O).sum())
+        total += int((np.where(on, np.maximum(0, hi - lo), 0) * ch).sum())
+    nominal = int((ln * O * ch).sum())
     return total, nominal
 
 
@@ -117,7 +120,10 @@ def main():
     props = torch.cuda.get_device_properties(dev)
 
     log("workload %s: n=%d L=%d K=%d" % (w.name, w.n, w.L, w.n_kernels))
-    ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
+    if w.channels > 1:
+        ks = rk.generate_kernels_multi(w.kernel_seed, w.n_kernels, w.L, w.channels)
+    else:
+        ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
     t0 = time.perf_counter()
     X_np = workload_series(w.name)
     log("series generated in %.1f s" % (time.perf_counter() - t0))
@@ -242,7 +248,7 @@ def main():
         "vs_baseline": None,
         "dtype": "fp32",
         "data": "synthetic (seeded %s series, z-normalised; seeded ROCKET kernels)" % w.kind,
-        "config": {"workload": w.name, "n_series": w.n, "series_length": w.L,
+        "config": {"workload": w.name, "n_series": w.n, "series_length": w.L, "channels": w.channels,
                    "n_kernels": w.n_kernels, "features": K2, "f_batch_rows": batch,
                    "kernel_seed": w.kernel_seed, "data_seed": w.data_seed,
                    "path": "direct" if info["direct"] else "fused-mfma"},

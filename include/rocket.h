@@ -54,11 +54,17 @@ typedef enum {
  *   dilation[k] >= 1
  *   padding[k]  >= 0             (generated: 0 or (length-1)*dilation/2)
  *   bias[k]     fp32
- *   weights[k*max_len + j], j < length[k]; entries beyond length[k] are
- *               ignored (the generator writes zeros there)
  *   max_len     weights row stride, in [length max, 11]; generated sets use 11
  *   input_length the series length the set was generated for (informational
  *               for hand-built sets; the transform takes L explicitly)
+ * Univariate sets (n_channels 0 or 1; channel_count and channel_index may be
+ * NULL): weights[k*max_len + j], j < length[k]; entries beyond length[k] are
+ * ignored (the generator writes zeros there).
+ * Multivariate sets (Sec. 3.3; series have n_channels = C channels, C in
+ * [2, 32]): kernel k reads channel_count[k] channels (in [1, C]) with ids
+ * channel_index[k*C + s], s < channel_count[k] (distinct, in [0, C)), and
+ * has one weight row per channel it reads: weights[(k*C + s)*max_len + j].
+ * Its dot product sums over those channels and taps.
  */
 typedef struct {
     int32_t n_kernels;
@@ -69,7 +75,12 @@ typedef struct {
     int32_t *padding;
     float *bias;
     float *weights;
+    int32_t n_channels;
+    int32_t *channel_count;
+    int32_t *channel_index;
 } rocket_kernels;
+
+#define ROCKET_MAX_CHANNELS 32
 
 /*
  * Generate n_kernels ROCKET kernels for series of length input_length
@@ -95,7 +106,29 @@ typedef struct {
 rocket_status rocket_generate_kernels(uint64_t seed, int32_t n_kernels, int32_t input_length,
                                       rocket_kernels *out);
 
-/* Release arrays allocated by rocket_generate_kernels and zero *k.
+/*
+ * Generate n_kernels multivariate ROCKET kernels (Sec. 3.3) for series of
+ * n_channels channels (in [1, 32]) and length input_length: length, bias,
+ * dilation and padding as rocket_generate_kernels; each kernel also reads
+ * floor(2^x) channels, x uniform on [0, log2(C + 1)), clamped to [1, C],
+ * chosen uniformly at random (ascending ids), with one weight row per
+ * channel, standard normal and mean-centred over the kernel's taps.
+ * Random numbers: kernel k, slot s reads element k*512 + s of the SplitMix64
+ * sequence started at `seed`: slot 0 length, slot 1 channel count, slots
+ * 2 .. C+1 a partial Fisher-Yates shuffle of 0..C-1 (step i swaps positions
+ * i and i + floor(u (C - i)), computed exactly on the integer), slots 64 ..
+ * Box-Muller pairs for the weights (normal q is channel slot q / 11, tap
+ * q % 11), slot 509 bias, 510 dilation, 511 padding.  The result depends
+ * only on (seed, k, input_length, n_channels).  Host only.
+ * out: library-owned arrays (weights [K * C * 11], channel_index [K * C],
+ *      -1 past each kernel's count); release with rocket_free_kernels.
+ * Errors: ROCKET_ERR_INVALID_ARG (out NULL, n_kernels < 1, input_length < 11,
+ *         n_channels outside [1, 32]); ROCKET_ERR_OOM.
+ */
+rocket_status rocket_generate_kernels_multi(uint64_t seed, int32_t n_kernels, int32_t input_length,
+                                            int32_t n_channels, rocket_kernels *out);
+
+/* Release arrays allocated by rocket_generate_kernels(_multi) and zero *k.
  * NULL-safe and idempotent.  Do not call on caller-built sets. */
 void rocket_free_kernels(rocket_kernels *k);
 
@@ -225,11 +258,14 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  * touched).  rocket_plan_tables_build validates like rocket_plan_create and
  * fills *out with library-owned arrays; free them with
  * rocket_plan_tables_free (NULL-safe, idempotent).
- *   items        n_items x 16 int32, one row per work item:
+ *   items        n_items x item_words (20) int32, one row per work item:
  *                [variant, dilation, padding, outputs O, steps S, rounds,
  *                 lane_off, w_off, k_off, cost, n_long, n_short,
- *                 rounds_long, 0, inv_O (words 14-15: 1/O as an IEEE
- *                 double, little-endian)];
+ *                 rounds_long, n_ch, ch_off, 0, inv_O (words 16-17: 1/O as
+ *                 an IEEE double, little-endian), 0, 0];
+ *                n_ch channels, listed in chan[ch_off .. ch_off + n_ch),
+ *                are the union of the channels the item's kernels read
+ *                (1 and channel 0 for univariate sets);
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
  *                7/9/11 taps, G kernel groups of 4 slots;
  *                every residue class (outputs r, r+d, ...) is split into
@@ -241,7 +277,7 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                lane's chunk has S-1 outputs in a round of S steps (the
  *                last step is computed and discarded); bit 30 set: the lane
  *                has no chunk (every step is discarded)
- *   wpk          packed weights, per item [G][taps][4 slots]
+ *   wpk          packed weights, per item [n_ch][G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in
  *                split_counts[n_layouts]: the items of variant v in split s
@@ -254,7 +290,11 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  */
 typedef struct {
     int64_t n_items;
+    int32_t item_words;
+    int32_t n_channels;
     const int32_t *items;
+    int64_t n_chan;
+    const int32_t *chan;
     int64_t n_lanes;
     const uint32_t *lanes;
     int64_t n_wpk;

@@ -6,5 +6,6 @@ Python-side entry points (argument marshalling over ctypes):
     transform(X, kernels)  one-shot
 The seeded synthetic series live in ``paper_2601_17091_amd.workloads``.
 """
-from .rocket import (EXPORTED, Plan, RocketError, generate_kernels, library, status_string,  # noqa: F401
+from .rocket import (EXPORTED, Plan, RocketError, generate_kernels, generate_kernels_multi, library,  # noqa: F401
+                     status_string,
                      plan_tables, transform, transform_batched)

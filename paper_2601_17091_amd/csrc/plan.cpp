@@ -24,6 +24,21 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
         const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
         if (len < 1 || len > k->max_len || d < 1 || p < 0) return ROCKET_ERR_INVALID_ARG;
     }
+    const int32_t C = k->n_channels < 1 ? 1 : k->n_channels;
+    if (C > ROCKET_MAX_CHANNELS) return ROCKET_ERR_INVALID_ARG;
+    if (C > 1) {
+        if (!k->channel_count || !k->channel_index) return ROCKET_ERR_INVALID_ARG;
+        for (int32_t i = 0; i < k->n_kernels; ++i) {
+            const int32_t cc = k->channel_count[i];
+            if (cc < 1 || cc > C) return ROCKET_ERR_INVALID_ARG;
+            uint64_t seen = 0;
+            for (int32_t s = 0; s < cc; ++s) {
+                const int32_t c = k->channel_index[(int64_t)i * C + s];
+                if (c < 0 || c >= C || (seen >> c) & 1u) return ROCKET_ERR_INVALID_ARG;
+                seen |= (uint64_t)1 << c;
+            }
+        }
+    }
     for (int32_t i = 0; i < k->n_kernels; ++i) {
         const int64_t O = output_length(L, k->length[i], k->dilation[i], k->padding[i]);
         if (O < 1 || O >= kMaxOutputs) return ROCKET_ERR_LENGTH;
@@ -132,6 +147,24 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         HostPlan P;
         P.n_kernels = k->n_kernels;
         P.L = L;
+        const int32_t C = k->n_channels < 1 ? 1 : k->n_channels;
+        P.n_channels = C;
+        // channels kernel i reads, as a bit mask (bit 0 for univariate sets)
+        auto mask_of = [&](int32_t i) -> uint64_t {
+            if (C == 1) return 1u;
+            uint64_t m = 0;
+            for (int32_t s = 0; s < k->channel_count[i]; ++s)
+                m |= (uint64_t)1 << k->channel_index[(int64_t)i * C + s];
+            return m;
+        };
+        // weight row of kernel i for channel c (nullptr if it does not read c)
+        auto row_of = [&](int32_t i, int32_t c) -> const float * {
+            if (C == 1) return k->weights + (int64_t)i * k->max_len;
+            for (int32_t s = 0; s < k->channel_count[i]; ++s)
+                if (k->channel_index[(int64_t)i * C + s] == c)
+                    return k->weights + ((int64_t)i * C + s) * k->max_len;
+            return nullptr;
+        };
         // bucket kernels by (length, dilation, padding); kernels keep their
         // original order inside a bucket
         std::map<std::tuple<int32_t, int32_t, int32_t>, std::vector<int32_t>> buckets;
@@ -161,7 +194,12 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         for (auto &kv : buckets) {
             const int32_t len = std::get<0>(kv.first), d = std::get<1>(kv.first),
                           p = std::get<2>(kv.first);
-            const std::vector<int32_t> &ids = kv.second;
+            std::vector<int32_t> &ids = kv.second;
+            // multivariate: kernels with similar channel sets next to each
+            // other, so that an item's channel union stays small
+            if (C > 1)
+                std::stable_sort(ids.begin(), ids.end(),
+                                 [&](int32_t a, int32_t b) { return mask_of(a) < mask_of(b); });
             const int eidx = ell_index_for(len);
             const int ell = kEllValues[eidx];
             const int64_t O = output_length(L, len, d, p);
@@ -192,22 +230,37 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 it.lane_off = lane_off;
                 it.w_off = (int32_t)P.wpk.size();
                 it.k_off = (int32_t)P.kid.size();
-                it.cost = (int32_t)(ch.steps() * ell * G);
+                uint64_t umask = 0;
+                for (size_t s = 0; s < take; ++s) umask |= mask_of(ids[pos + s]);
+                it.n_ch = 0;
+                it.ch_off = (int32_t)P.chan.size();
+                for (int32_t c = 0; c < C; ++c)
+                    if ((umask >> c) & 1u) {
+                        P.chan.push_back(c);
+                        ++it.n_ch;
+                    }
+                it.cost = (int32_t)(ch.steps() * ell * G * it.n_ch);
                 it.n_long = (int32_t)ch.n_long;
                 it.n_short = (int32_t)ch.n_short;
                 it.rounds_long = (int32_t)ch.rounds_long;
                 it.inv_O = 1.0 / (double)O;
-                // A-operand weights: [g][j][slot i]; zeros for empty slots and
-                // for taps past the kernel's own length
-                for (int g = 0; g < G; ++g)
-                    for (int j = 0; j < ell; ++j)
-                        for (int i = 0; i < 4; ++i) {
-                            const size_t s = (size_t)(4 * g + i);
-                            float w = 0.0f;
-                            if (s < take && j < len)
-                                w = k->weights[(int64_t)ids[pos + s] * k->max_len + j];
-                            P.wpk.push_back(w);
-                        }
+                // A-operand weights: [channel][g][j][slot i]; zeros for empty
+                // slots, for channels a slot's kernel does not read and for
+                // taps past the kernel's own length
+                for (int32_t ci = 0; ci < it.n_ch; ++ci) {
+                    const int32_t c = P.chan[it.ch_off + ci];
+                    for (int g = 0; g < G; ++g)
+                        for (int j = 0; j < ell; ++j)
+                            for (int i = 0; i < 4; ++i) {
+                                const size_t s = (size_t)(4 * g + i);
+                                float w = 0.0f;
+                                if (s < take && j < len) {
+                                    const float *row = row_of(ids[pos + s], c);
+                                    if (row) w = row[j];
+                                }
+                                P.wpk.push_back(w);
+                            }
+                }
                 for (int s = 0; s < 4 * G; ++s) {
                     if ((size_t)s < take) {
                         P.kid.push_back(ids[pos + s]);
@@ -278,6 +331,10 @@ extern "C" rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32
         return st;
     }
     out->n_items = (int64_t)P->items.size();
+    out->item_words = rocket::kItemWords;
+    out->n_chan = (int64_t)P->chan.size();
+    out->chan = P->chan.data();
+    out->n_channels = P->n_channels;
     out->items = reinterpret_cast<const int32_t *>(P->items.data());
     out->n_lanes = (int64_t)P->lanes.size();
     out->lanes = P->lanes.data();

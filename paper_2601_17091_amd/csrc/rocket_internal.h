@@ -42,16 +42,20 @@ struct alignas(16) ItemDesc {
     int32_t S;            // steps of a long chunk (short chunks: S - 1)
     int32_t rounds;       // rounds per series
     int32_t lane_off;     // first lane-table entry (rounds * 64 entries)
-    int32_t w_off;        // first packed weight: [G][ell][4] floats
+    int32_t w_off;        // first packed weight: [n_ch][G][ell][4] floats
     int32_t k_off;        // first slot entry: kernel ids and biases, [4G]
     int32_t cost;         // MFMA instructions per series (scheduling weight)
     int32_t n_long;       // chunks of S outputs
     int32_t n_short;      // chunks of S - 1 outputs
     int32_t rounds_long;  // rounds that run S steps: ceil(n_long / 64)
-    int32_t reserved;
+    int32_t n_ch;         // channels the item's kernels read (their union; 1 if univariate)
+    int32_t ch_off;       // first entry of the item's channel list
+    int32_t reserved0;
     double inv_O;         // 1 / O rounded to double (exact PPV, see transform.hip)
+    int32_t reserved1[2];
 };
-static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
+static_assert(sizeof(ItemDesc) == 80, "ItemDesc must stay 80 bytes");
+constexpr int kItemWords = (int)(sizeof(ItemDesc) / sizeof(int32_t));
 
 // Lane-table entry: the output position of the lane's first step (below
 // 2^24) and two flags.
@@ -75,6 +79,7 @@ struct HostPlan {
     int32_t halo_hi = 0;   // zeros staged after the series in LDS
     int32_t row_stride = 0;  // floats per staged row
     int32_t tail_pad = 0;    // zeros staged after the last row (reads of discarded steps)
+    int32_t n_channels = 1;  // channels per series
     int64_t n_buckets = 0;
     int64_t mfma_per_row = 0;
     std::vector<ItemDesc> items;
@@ -82,6 +87,7 @@ struct HostPlan {
     std::vector<float> wpk;       // packed A-operand weights
     std::vector<float> bias;      // per slot
     std::vector<int32_t> kid;     // per slot, -1 = empty
+    std::vector<int32_t> chan;    // per item, its channel list (ascending)
     std::vector<int32_t> order;   // kNumSplitLayouts concatenated item orders
     std::vector<int32_t> split_begin;  // per layout: kNumVariants*nsplit + 1 offsets into order
     std::vector<int32_t> layout_off;   // per layout: offset into split_begin

@@ -59,6 +59,8 @@ struct FusedArgs {
     int32_t L;
     int32_t K;
     int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV)
+    int32_t C;         // channels per series
+    const int32_t *chan;  // item channel lists
     const ItemDesc *items;
     const uint32_t *lanes;
     const float *wpk;
@@ -97,6 +99,7 @@ struct PaddedRow {
     int d;
     __device__ __forceinline__ float value(int m) const { return xs[m * d]; }
     __device__ __forceinline__ PaddedRow shifted(int k) const { return PaddedRow{xs + k, d}; }
+    __device__ __forceinline__ PaddedRow channel(int off) const { return PaddedRow{xs + off, d}; }
 };
 
 struct ClampedRow {
@@ -108,6 +111,7 @@ struct ClampedRow {
         return row[min(max(i0 + m * d, -1), L)];
     }
     __device__ __forceinline__ ClampedRow shifted(int k) const { return ClampedRow{row, i0 + k, d, L}; }
+    __device__ __forceinline__ ClampedRow channel(int off) const { return ClampedRow{row + off, i0, d, L}; }
 };
 
 // Per-series accumulators of one work item, per lane and kernel slot: the
@@ -120,32 +124,42 @@ struct RowAcc {
     v4f ps[G];
 };
 
+// Multichannel items (Sec. 3.3): where the item's weights and channel rows
+// are.  w is the lane's first packed weight (slot lane & 3); the weights of
+// channel list entry ci, group g, tap j are at w[((ci*G + g)*ELL + j)*4].
+// The row of channel c sits c*cstride floats after the series' first row.
+struct McCtx {
+    const float *w;
+    ConstPtr<int32_t> chan;  // the item's channel list
+    int n_ch;
+    int cstride;
+};
+
 // NS consecutive output steps of one round, as an outer-product contraction
-// over the taps.  The window of series values under the NS outputs
-// (NS + ELL - 1 values spaced d apart) is read from LDS first; then tap j of every step and kernel group is issued before tap j+1,
-// so the wavefront keeps NS*G independent MFMA accumulation chains in
-// flight.  Each chain starts from binit (the slots' biases, or -inf on a
-// lane without a chunk); when LAST is set the block ends the round and its
-// final step starts from -inf on lanes with drop_last set (a chunk one
-// output short, or no chunk).  A chain started at -inf stays -inf, so MAX folds every
-// result (v_max3 over pairs of steps) and the positive count is a ballot of
-// y > 0 popcounted on the scalar unit.
-template <int ELL, int G, int NS, bool LAST, bool MPV, typename Src>
-__device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][ELL],
-                                           const v4f (&binit)[G], bool drop_last, RowAcc<G> &ra) {
-    float xw[NS + ELL - 1];
-#pragma unroll
-    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
-    v4f acc[NS][G];
+// over the taps: tap j of every step and kernel group is issued before tap
+// j+1, so the wavefront keeps NS*G independent MFMA accumulation chains in
+// flight.  With FIRST set each chain starts from binit (the slots' biases,
+// or -inf on a lane without a chunk) and, when LAST is also set (the block
+// ends the round), the final step starts from -inf on lanes with drop_last
+// set (a chunk one output short, or no chunk); without FIRST the chains
+// continue from acc (the next channel of a multichannel item).
+template <int ELL, int G, int NS, bool LAST, bool FIRST>
+__device__ __forceinline__ void block_mfma(const float (&xw)[NS + ELL - 1], const float (&wa)[G][ELL],
+                                           const v4f (&binit)[G], bool drop_last,
+                                           v4f (&acc)[NS][G]) {
 #pragma unroll
     for (int u = 0; u < NS; ++u)
 #pragma unroll
-        for (int g = 0; g < G; ++g)
-        {
-            v4f c = binit[g];
-            if (LAST && u == NS - 1) {
+        for (int g = 0; g < G; ++g) {
+            v4f c;
+            if (FIRST) {
+                c = binit[g];
+                if (LAST && u == NS - 1) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
+                    for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
+                }
+            } else {
+                c = acc[u][g];
             }
             acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], c, 0, 0, 0);
         }
@@ -156,6 +170,14 @@ __device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][
 #pragma unroll
             for (int g = 0; g < G; ++g)
                 acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[u + j], acc[u][g], 0, 0, 0);
+}
+
+// Fold NS steps of finished dot products into the row accumulators.  A chain
+// started at -inf stays -inf, so MAX folds every result (v_max3 over pairs of
+// steps), the positive count is a ballot of y > 0 popcounted on the scalar
+// unit, and the MPV numerator adds max(y, 0).
+template <int G, int NS, bool MPV>
+__device__ __forceinline__ void block_reduce(const v4f (&acc)[NS][G], RowAcc<G> &ra) {
 #pragma unroll
     for (int u = 0; u < NS; ++u)
 #pragma unroll
@@ -164,7 +186,6 @@ __device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][
             for (int v = 0; v < 4; ++v)
                 ra.cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][g][v] > 0.0f));
     if (MPV) {
-        // sum of the positive values (-inf and non-positive results add 0)
 #pragma unroll
         for (int u = 0; u < NS; ++u)
 #pragma unroll
@@ -187,23 +208,78 @@ __device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][
     }
 }
 
+// The window under NS steps: NS + ELL - 1 values spaced d apart.
+template <int ELL, int NS, typename Src>
+__device__ __forceinline__ void load_window(const Src &src, float (&xw)[NS + ELL - 1]) {
+#pragma unroll
+    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
+}
+
+// One block of NS steps.  Univariate items keep their weights in registers
+// (wa); multichannel items (MC) run the MFMA chains over every channel of
+// their list, reading each channel's window and weights in turn.
+template <int ELL, int G, int NS, bool LAST, bool MPV, bool MC, typename Src>
+__device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][ELL], const McCtx &mc,
+                                           const v4f (&binit)[G], bool drop_last, RowAcc<G> &ra) {
+    float xw[NS + ELL - 1];
+    v4f acc[NS][G];
+    if constexpr (!MC) {
+#pragma unroll
+        for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
+#pragma unroll
+        for (int u = 0; u < NS; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                v4f c = binit[g];
+                if (LAST && u == NS - 1) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
+                }
+                acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], c, 0, 0, 0);
+            }
+#pragma unroll
+        for (int j = 1; j < ELL; ++j)
+#pragma unroll
+            for (int u = 0; u < NS; ++u)
+#pragma unroll
+                for (int g = 0; g < G; ++g)
+                    acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[u + j], acc[u][g], 0, 0, 0);
+    } else {
+        float wc[G][ELL];
+        for (int ci = 0; ci < mc.n_ch; ++ci) {
+            load_window<ELL, NS>(src.channel(mc.chan[ci] * mc.cstride), xw);
+            const float *wp = mc.w + ci * (G * ELL * 4);
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int j = 0; j < ELL; ++j) wc[g][j] = wp[(g * ELL + j) * 4];
+            if (ci == 0)
+                block_mfma<ELL, G, NS, LAST, true>(xw, wc, binit, drop_last, acc);
+            else
+                block_mfma<ELL, G, NS, LAST, false>(xw, wc, binit, drop_last, acc);
+        }
+    }
+    block_reduce<G, NS, MPV>(acc, ra);
+}
+
 // The last block of a round: its length nv (1..N) selects a code copy.
-template <int ELL, int G, int N, bool MPV, typename Src>
+template <int ELL, int G, int N, bool MPV, bool MC, typename Src>
 struct TailBlock {
     __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
-                                               const v4f (&binit)[G], bool drop_last,
-                                               RowAcc<G> &ra) {
+                                               const McCtx &mc, const v4f (&binit)[G],
+                                               bool drop_last, RowAcc<G> &ra) {
         if (nv == N)
-            step_block<ELL, G, N, true, MPV>(src, wa, binit, drop_last, ra);
+            step_block<ELL, G, N, true, MPV, MC>(src, wa, mc, binit, drop_last, ra);
         else
-            TailBlock<ELL, G, N - 1, MPV, Src>::run(nv, src, wa, binit, drop_last, ra);
+            TailBlock<ELL, G, N - 1, MPV, MC, Src>::run(nv, src, wa, mc, binit, drop_last, ra);
     }
 };
 
-template <int ELL, int G, bool MPV, typename Src>
-struct TailBlock<ELL, G, 0, MPV, Src> {
+template <int ELL, int G, bool MPV, bool MC, typename Src>
+struct TailBlock<ELL, G, 0, MPV, MC, Src> {
     __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL],
-                                               const v4f (&)[G], bool, RowAcc<G> &) {}
+                                               const McCtx &, const v4f (&)[G], bool,
+                                               RowAcc<G> &) {}
 };
 
 // Combining operations of the wavefront reductions: max for MAX, sum for
@@ -291,19 +367,20 @@ __device__ __forceinline__ void setup_round(const ItemDesc &it, int rd, const Fu
 
 // All steps of one round for one series; src.value(m) is the zero-padded
 // series value under tap m of the lane's step-0 output.
-template <int ELL, int G, int T, bool MPV, typename Src>
+template <int ELL, int G, int T, bool MPV, bool MC, typename Src>
 __device__ __forceinline__ void run_round(const Src &src, int d, const RoundState<G> &st,
-                                          const float (&wa)[G][ELL], RowAcc<G> &ra) {
+                                          const float (&wa)[G][ELL], const McCtx &mc,
+                                          RowAcc<G> &ra) {
     const int nfull = (st.len - 1) / T;  // full blocks before the last block
     const int nv = st.len - nfull * T;   // length of the last block, 1..T
     // block b starts b*T*d positions along the row: a wavefront-uniform
     // offset, so each load is one lane address plus a scalar
     for (int blk = 0; blk < nfull; ++blk) {
         const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
-        step_block<ELL, G, T, false, MPV>(src.shifted(off), wa, st.binit, st.drop_last, ra);
+        step_block<ELL, G, T, false, MPV, MC>(src.shifted(off), wa, mc, st.binit, st.drop_last, ra);
     }
-    TailBlock<ELL, G, T, MPV, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
-                                        wa, st.binit, st.drop_last, ra);
+    TailBlock<ELL, G, T, MPV, MC, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
+                                            wa, mc, st.binit, st.drop_last, ra);
 }
 
 template <int G, bool MPV>
@@ -321,7 +398,7 @@ __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 // scalar), then per kernel {PPV, MAX} (or {PPV, MAX, MPV}), written by lanes
 // 0, 16, 32 and 48.
 template <int G, bool MPV>
-__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&out_kernel)[G],
+__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int32_t *kid_row,
                                           double inv_O, int lane, float *Frow) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -338,7 +415,9 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&out_k
         c = lane >= 16 ? c2 : c;
         c = lane >= 32 ? c1 : c;
         c = lane >= 48 ? c3 : c;
-        if (out_kernel[g] >= 0) {
+        const bool writer = (lane & 15) == 0;
+        const int ok = writer ? kid_row[4 * g + slot_of_row(lane >> 4)] : -1;
+        if (ok >= 0) {
             // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
             // quotient is never a float midpoint and lies at least 2^-49
             // (relative) from one, while c * fl64(1/O) is within 2^-52 of
@@ -347,7 +426,7 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&out_k
             const float ppv = (float)((double)c * inv_O);
             if (MPV) {
                 // rows of 3 floats: 4-byte aligned only
-                float *f = Frow + 3 * (int64_t)out_kernel[g];
+                float *f = Frow + 3 * (int64_t)ok;
                 f[0] = ppv;
                 f[1] = m;
                 f[2] = c > 0 ? psum / (float)c : 0.0f;
@@ -355,39 +434,47 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&out_k
                 float2 res;
                 res.x = ppv;
                 res.y = m;
-                *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)out_kernel[g]) = res;
+                *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)ok) = res;
             }
         }
     }
 }
 
 // One round over the series whose index 0 sits at `row` in LDS.
-template <int ELL, int G, int T, bool CLAMP, bool MPV>
+template <int ELL, int G, int T, bool CLAMP, bool MPV, bool MC>
 __device__ __forceinline__ void run_row_round(const float *row, const ItemDesc &it, int L,
                                               const RoundState<G> &st, const float (&wa)[G][ELL],
-                                              RowAcc<G> &ra) {
+                                              const McCtx &mc, RowAcc<G> &ra) {
     const int i0 = (int)st.pos - it.p;  // series index under tap 0 of step 0
     if (CLAMP)
-        run_round<ELL, G, T, MPV>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, ra);
+        run_round<ELL, G, T, MPV, MC>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, mc, ra);
     else
-        run_round<ELL, G, T, MPV>(PaddedRow{row + i0, it.d}, it.d, st, wa, ra);
+        run_round<ELL, G, T, MPV, MC>(PaddedRow{row + i0, it.d}, it.d, st, wa, mc, ra);
 }
 
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.
-template <int ELL, int G, bool CLAMP, bool MPV>
+template <int ELL, int G, bool CLAMP, bool MPV, bool MC>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
     // steps per block: 8 (G = 1) or 6 (G = 2) independent accumulation
     // chains per wavefront; T = 3 for G = 2 keeps the kernel within 96 VGPRs
     // (5 wavefronts per SIMD)
     constexpr int T = G == 1 ? 8 : 3;
-    // A operand: lane holds the weight of kernel slot (lane & 3) for every tap
+    // A operand: lane holds the weight of kernel slot (lane & 3) for every
+    // tap; univariate items keep them in registers for the whole item,
+    // multichannel ones read each channel's weights per block (McCtx)
     float wa[G][ELL];
+    if constexpr (!MC) {
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+        for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
+            for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
+    }
+    McCtx mc{};
+    if constexpr (MC) mc = McCtx{a.wpk + it.w_off + (lane & 3), as_const(a.chan) + it.ch_off, it.n_ch,
+                                 a.row_stride};
+    const int row_pitch = a.C * a.row_stride;  // floats per staged series (LDS offsets fit 32 bits)
     // C operand of the first tap: the bias of block row v (kernel slot v)
     // (wavefront-uniform: scalar registers)
     float bias[G][4];
@@ -396,12 +483,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
         for (int v = 0; v < 4; ++v) bias[g][v] = as_const(a.bias)[it.k_off + 4 * g + v];
     // after the reduction, lane 16q writes slot slot_of_row(q) of each group
-    const int row_of_lane = lane >> 4;
-    const bool writer = (lane & 15) == 0;  // lanes 0, 16, 32, 48
-    int out_kernel[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-        out_kernel[g] = writer ? a.kid[it.k_off + 4 * g + slot_of_row(row_of_lane)] : -1;
+    const int32_t *kid_row = a.kid + it.k_off;
     const int64_t f_stride = (int64_t)a.nf * a.K;
     RoundState<G> st;
     if (it.rounds == 1) {
@@ -410,8 +492,8 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         for (int r = 0; r < nrows; ++r) {
             RowAcc<G> ra;
             init_row<G, MPV>(ra);
-            run_row_round<ELL, G, T, CLAMP, MPV>(rows0 + r * a.row_stride, it, a.L, st, wa, ra);
-            write_row<G, MPV>(ra, out_kernel, it.inv_O, lane, F0 + r * f_stride);
+            run_row_round<ELL, G, T, CLAMP, MPV, MC>(rows0 + r * row_pitch, it, a.L, st, wa, mc, ra);
+            write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
         }
     } else {
         for (int r = 0; r < nrows; ++r) {
@@ -419,9 +501,9 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
             init_row<G, MPV>(ra);
             for (int rd = 0; rd < it.rounds; ++rd) {
                 setup_round<G>(it, rd, a, bias, lane, st);
-                run_row_round<ELL, G, T, CLAMP, MPV>(rows0 + r * a.row_stride, it, a.L, st, wa, ra);
+                run_row_round<ELL, G, T, CLAMP, MPV, MC>(rows0 + r * row_pitch, it, a.L, st, wa, mc, ra);
             }
-            write_row<G, MPV>(ra, out_kernel, it.inv_O, lane, F0 + r * f_stride);
+            write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
         }
     }
 }
@@ -442,11 +524,13 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
     it.n_short = p->n_short;
     it.rounds_long = p->rounds_long;
     it.inv_O = p->inv_O;
+    it.n_ch = p->n_ch;
+    it.ch_off = p->ch_off;
     return it;
 }
 
 // Items of one variant, taken one at a time from the workgroup's counter.
-template <int ELL, int G, bool CLAMP, bool MPV>
+template <int ELL, int G, bool CLAMP, bool MPV, bool MC>
 __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items,
                                           const float *rows0, int nrows, const FusedArgs &a,
                                           float *F0, int lane) {
@@ -456,13 +540,13 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
         idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
         if (idx >= cnt_items) break;
         const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
-        run_item<ELL, G, CLAMP, MPV>(it, rows0, nrows, a, F0, lane);
+        run_item<ELL, G, CLAMP, MPV, MC>(it, rows0, nrows, a, F0, lane);
     }
 }
 
 // Workgroup = (variant, row tile, split); each workgroup stages its row tile
 // in LDS and runs the items of one variant over it.
-template <int BLOCK, bool CLAMP, bool MPV>
+template <int BLOCK, bool CLAMP, bool MPV, bool MC>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
@@ -485,10 +569,11 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     const int nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
     const int64_t grow = a.row0 + first;
 
-    // stage the tile's series with their zero margins, coalesced
-    for (int r = 0; r < nrows; ++r) {
-        const float *x = a.X + (grow + r) * (int64_t)a.L;
-        float *dst = smem + r * a.row_stride;
+    // stage the tile's series (every channel) with their zero margins,
+    // coalesced; channel c of row r at (r*C + c)*row_stride
+    for (int rc = 0; rc < nrows * a.C; ++rc) {
+        const float *x = a.X + ((grow * a.C) + rc) * (int64_t)a.L;
+        float *dst = smem + rc * a.row_stride;
         for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
             const int m = e - a.halo_lo;
             dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
@@ -496,7 +581,7 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     }
     // zeros after the last row: discarded extra steps may read up to
     // tail_pad floats past it
-    for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[nrows * a.row_stride + e] = 0.0f;
+    for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[nrows * a.C * a.row_stride + e] = 0.0f;
     if (threadIdx.x == 0) next_item = 0;
     __syncthreads();
 
@@ -504,12 +589,12 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     float *F0 = a.F + grow * (int64_t)a.nf * a.K;
     const float *rows0 = smem + a.halo_lo;
     switch (variant) {
-        case 0: run_items<7, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 1: run_items<7, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 2: run_items<9, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 3: run_items<9, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 4: run_items<11, 1, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        default: run_items<11, 2, CLAMP, MPV>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 1: run_items<7, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+        default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
     }
 }
 
@@ -520,24 +605,30 @@ __global__ __launch_bounds__(kBlock) void rocket_direct_kernel(
     const float *__restrict__ X, int64_t row0, int32_t L, int32_t K, int32_t k0,
     const int32_t *__restrict__ len, const int32_t *__restrict__ dil,
     const int32_t *__restrict__ pad, const float *__restrict__ bias,
-    const float *__restrict__ w, int32_t max_len, int32_t nf, float *__restrict__ F) {
+    const float *__restrict__ w, int32_t max_len, int32_t nf, int32_t C,
+    const int32_t *__restrict__ ccount, const int32_t *__restrict__ cindex,
+    float *__restrict__ F) {
     const int64_t row = row0 + blockIdx.x;
     const int k = k0 + (int)blockIdx.y * (kBlock / 64) + (int)(threadIdx.x >> 6);
     if (k >= K) return;
     const int lane = threadIdx.x & 63;
     const int ell = len[k], d = dil[k], p = pad[k];
+    const int nch = C > 1 ? ccount[k] : 1;
     const float b = bias[k];
-    const float *wk = w + (int64_t)k * max_len;
     const int64_t O = (int64_t)L + 2 * (int64_t)p - (int64_t)(ell - 1) * d;
-    const float *x = X + row * (int64_t)L;
     float mx = -INFINITY, ps = 0.0f;
     uint32_t c = 0;
     for (int64_t t = lane; t < O; t += 64) {
         float acc = b;
-        for (int j = 0; j < ell; ++j) {
-            const int64_t m = t - p + (int64_t)j * d;
-            const float xv = (m >= 0 && m < L) ? x[m] : 0.0f;
-            acc = fmaf(wk[j], xv, acc);
+        for (int s = 0; s < nch; ++s) {
+            const int ch = C > 1 ? cindex[(int64_t)k * C + s] : 0;
+            const float *x = X + (row * C + ch) * (int64_t)L;
+            const float *wk = w + ((int64_t)k * C + s) * max_len;
+            for (int j = 0; j < ell; ++j) {
+                const int64_t m = t - p + (int64_t)j * d;
+                const float xv = (m >= 0 && m < L) ? x[m] : 0.0f;
+                acc = fmaf(wk[j], xv, acc);
+            }
         }
         c += acc > 0.0f ? 1u : 0u;
         ps += acc > 0.0f ? acc : 0.0f;
@@ -576,6 +667,31 @@ hipError_t upload_raw(const T *h, size_t n, T **d) {
 
 }  // namespace
 
+// The fused kernel's instances: bit 0 the 1024-thread block (rows above
+// kBigLds), bit 1 clamped indices, bit 2 MPV, bit 3 multichannel items.
+constexpr int kFusedInstances = 16;
+static const void *fused_fn(int sel) {
+    static const void *const fns[kFusedInstances] = {
+        (const void *)rocket_fused_kernel<kBlock, false, false, false>,
+        (const void *)rocket_fused_kernel<kBigBlock, false, false, false>,
+        (const void *)rocket_fused_kernel<kBlock, true, false, false>,
+        (const void *)rocket_fused_kernel<kBigBlock, true, false, false>,
+        (const void *)rocket_fused_kernel<kBlock, false, true, false>,
+        (const void *)rocket_fused_kernel<kBigBlock, false, true, false>,
+        (const void *)rocket_fused_kernel<kBlock, true, true, false>,
+        (const void *)rocket_fused_kernel<kBigBlock, true, true, false>,
+        (const void *)rocket_fused_kernel<kBlock, false, false, true>,
+        (const void *)rocket_fused_kernel<kBigBlock, false, false, true>,
+        (const void *)rocket_fused_kernel<kBlock, true, false, true>,
+        (const void *)rocket_fused_kernel<kBigBlock, true, false, true>,
+        (const void *)rocket_fused_kernel<kBlock, false, true, true>,
+        (const void *)rocket_fused_kernel<kBigBlock, false, true, true>,
+        (const void *)rocket_fused_kernel<kBlock, true, true, true>,
+        (const void *)rocket_fused_kernel<kBigBlock, true, true, true>,
+    };
+    return fns[sel];
+}
+
 struct rocket_plan {
     rocket::HostPlan host;
     int device = 0;
@@ -583,6 +699,7 @@ struct rocket_plan {
     bool direct = false;
     bool clamp = false;      // rows staged with one-zero margins, indices clamped
     bool mpv = false;        // third feature per kernel: mean of positive values
+    int32_t C = 1;           // channels per series
     int32_t halo_lo = 0;     // staged layout actually used (floats)
     int32_t row_stride = 0;
     int32_t tail_pad = 0;
@@ -595,8 +712,11 @@ struct rocket_plan {
     int32_t *d_kid = nullptr;
     int32_t *d_order = nullptr;
     int32_t *d_split_begin = nullptr;
+    int32_t *d_chan = nullptr;
     // the kernel set as given, for the direct kernel
     int32_t max_len = 0;
+    int32_t *d_cc = nullptr;  // channel counts and indices (multichannel sets)
+    int32_t *d_ci = nullptr;
     int32_t *d_len = nullptr;
     int32_t *d_dil = nullptr;
     int32_t *d_pad = nullptr;
@@ -606,7 +726,8 @@ struct rocket_plan {
 
 static void plan_free_device(rocket_plan *p) {
     void *ptrs[] = {p->d_items, p->d_lanes, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
-                    p->d_split_begin, p->d_len, p->d_dil, p->d_pad, p->d_b, p->d_w};
+                    p->d_split_begin, p->d_chan, p->d_len, p->d_dil, p->d_pad, p->d_b,
+                    p->d_w, p->d_cc, p->d_ci};
     for (void *q : ptrs)
         if (q) (void)hipFree(q);
 }
@@ -642,13 +763,14 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     }
     p->n_cu = prop.multiProcessorCount;
     p->mpv = (flags & ROCKET_PLAN_MPV) != 0;
+    p->C = p->host.n_channels;
     // Staged layout: rows with zero margins wide enough for every padded tap
     // if that fits one workgroup's LDS, else rows with one zero on each side
     // and clamped indices, else the direct kernel.  Rows per workgroup: as
     // many as fit the LDS budget (at least one).
     const int64_t limit = (int64_t)prop.sharedMemPerBlock;
     auto layout = [&](int64_t stride, int64_t pad, int *rows) {
-        const int64_t row_bytes = stride * (int64_t)sizeof(float);
+        const int64_t row_bytes = stride * p->C * (int64_t)sizeof(float);  // every channel
         const int64_t pad_bytes = pad * (int64_t)sizeof(float);
         *rows = (int)std::max<int64_t>(
             1, std::min<int64_t>(kMaxRowsPerBlock, (kRowsLdsBudget - pad_bytes) / row_bytes));
@@ -676,7 +798,9 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     if (e == hipSuccess) e = upload_raw(k->dilation, (size_t)K, &p->d_dil);
     if (e == hipSuccess) e = upload_raw(k->padding, (size_t)K, &p->d_pad);
     if (e == hipSuccess) e = upload_raw(k->bias, (size_t)K, &p->d_b);
-    if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * k->max_len, &p->d_w);
+    if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * p->C * k->max_len, &p->d_w);
+    if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_count, (size_t)K, &p->d_cc);
+    if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_index, (size_t)K * p->C, &p->d_ci);
     if (!p->direct) {
         if (e == hipSuccess) e = upload(p->host.items, &p->d_items);
         if (e == hipSuccess) e = upload(p->host.lanes, &p->d_lanes);
@@ -685,19 +809,11 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
         if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
         if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
-        if (e == hipSuccess && lds > 64 * 1024) {
-            const void *fns[] = {(const void *)rocket_fused_kernel<kBlock, false, false>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, false, false>,
-                                 (const void *)rocket_fused_kernel<kBlock, true, false>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, true, false>,
-                                 (const void *)rocket_fused_kernel<kBlock, false, true>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, false, true>,
-                                 (const void *)rocket_fused_kernel<kBlock, true, true>,
-                                 (const void *)rocket_fused_kernel<kBigBlock, true, true>};
-            for (const void *f : fns)
-                if (e == hipSuccess)
-                    e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        }
+        if (e == hipSuccess) e = upload(p->host.chan, &p->d_chan);
+        if (e == hipSuccess && lds > 64 * 1024)
+            for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
+                e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                        (int)lds);
     }
     if (e != hipSuccess) {
         plan_free_device(p);
@@ -744,7 +860,7 @@ static rocket_status launch_direct(const rocket_plan *p, const float *X, int64_t
             dim3 grid((unsigned)nr, (unsigned)((nk + per_block - 1) / per_block));
             hipLaunchKernelGGL(rocket_direct_kernel, grid, dim3(kBlock), 0, s, X, r0, p->host.L, K,
                                (int32_t)k0, p->d_len, p->d_dil, p->d_pad, p->d_b, p->d_w,
-                               p->max_len, p->mpv ? 3 : 2, F);
+                               p->max_len, p->mpv ? 3 : 2, p->C, p->d_cc, p->d_ci, F);
             if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
         }
     }
@@ -756,7 +872,7 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     // enough workgroups to fill the chip several times over: split the work
     // items of a series across workgroups when there are few series
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
-    const int64_t row_bytes = (int64_t)p->row_stride * (int64_t)sizeof(float);
+    const int64_t row_bytes = (int64_t)p->row_stride * (int64_t)sizeof(float);  // one channel
     const int R = p->rows_per_block;
     const int64_t tiles = (n + R - 1) / R;
     int li = 0;
@@ -768,6 +884,8 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.L = p->host.L;
     a.K = p->host.n_kernels;
     a.nf = p->mpv ? 3 : 2;
+    a.C = p->C;
+    a.chan = p->d_chan;
     a.items = p->d_items;
     a.lanes = p->d_lanes;
     a.wpk = p->d_wpk;
@@ -794,22 +912,12 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         a.tiles_per_xcd = (tiles_now + kXcds - 1) / kXcds;
         const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)p->lds_bytes;
-        const bool big = row_bytes > kBigLds;
-        // one instance per (block size, layout, feature count)
-        auto go = [&](auto kern, int block) {
-            hipLaunchKernelGGL(kern, dim3(nb), dim3(block), lds, s, a);
-        };
-        const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0);
-        switch (sel) {
-            case 0: go(rocket_fused_kernel<kBlock, false, false>, kBlock); break;
-            case 1: go(rocket_fused_kernel<kBigBlock, false, false>, kBigBlock); break;
-            case 2: go(rocket_fused_kernel<kBlock, true, false>, kBlock); break;
-            case 3: go(rocket_fused_kernel<kBigBlock, true, false>, kBigBlock); break;
-            case 4: go(rocket_fused_kernel<kBlock, false, true>, kBlock); break;
-            case 5: go(rocket_fused_kernel<kBigBlock, false, true>, kBigBlock); break;
-            case 6: go(rocket_fused_kernel<kBlock, true, true>, kBlock); break;
-            default: go(rocket_fused_kernel<kBigBlock, true, true>, kBigBlock); break;
-        }
+        const bool big = row_bytes * p->C > kBigLds;
+        const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
+        void *args[] = {&a};
+        if (hipLaunchKernel(fused_fn(sel), dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) !=
+            hipSuccess)
+            return ROCKET_ERR_HIP;
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
     }
     return ROCKET_OK;
@@ -835,7 +943,8 @@ extern "C" rocket_status rocket_transform_host(const rocket_plan *p, const float
     if (!p || n < 0 || batch_rows < 0) return ROCKET_ERR_INVALID_ARG;
     if (n == 0) return ROCKET_OK;
     if (!X_host || !F_host) return ROCKET_ERR_INVALID_ARG;
-    const int64_t L = p->host.L, K2 = (int64_t)(p->mpv ? 3 : 2) * p->host.n_kernels;
+    const int64_t L = (int64_t)p->host.L * p->C;  // floats per series (every channel)
+    const int64_t K2 = (int64_t)(p->mpv ? 3 : 2) * p->host.n_kernels;
     int64_t B = batch_rows;
     // default: about 8 batches, so copies have neighbours to overlap with,
     // each within 256 MiB of staging

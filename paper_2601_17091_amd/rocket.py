@@ -30,6 +30,7 @@ MAX_KERNEL_LENGTH = 11
 # every symbol include/rocket.h declares
 EXPORTED = (
     "rocket_generate_kernels",
+    "rocket_generate_kernels_multi",
     "rocket_free_kernels",
     "rocket_plan_create",
     "rocket_plan_create_ex",
@@ -60,6 +61,9 @@ class CKernels(ctypes.Structure):
         ("padding", ctypes.POINTER(ctypes.c_int32)),
         ("bias", ctypes.POINTER(ctypes.c_float)),
         ("weights", ctypes.POINTER(ctypes.c_float)),
+        ("n_channels", ctypes.c_int32),
+        ("channel_count", ctypes.POINTER(ctypes.c_int32)),
+        ("channel_index", ctypes.POINTER(ctypes.c_int32)),
     ]
 
 
@@ -74,7 +78,9 @@ class CPlanFacts(ctypes.Structure):
 
 class CPlanTables(ctypes.Structure):
     _fields_ = [
-        ("n_items", ctypes.c_int64), ("items", ctypes.POINTER(ctypes.c_int32)),
+        ("n_items", ctypes.c_int64), ("item_words", ctypes.c_int32), ("n_channels", ctypes.c_int32),
+        ("items", ctypes.POINTER(ctypes.c_int32)),
+        ("n_chan", ctypes.c_int64), ("chan", ctypes.POINTER(ctypes.c_int32)),
         ("n_lanes", ctypes.c_int64), ("lanes", ctypes.POINTER(ctypes.c_uint32)),
         ("n_wpk", ctypes.c_int64), ("wpk", ctypes.POINTER(ctypes.c_float)),
         ("n_slots", ctypes.c_int64), ("slot_bias", ctypes.POINTER(ctypes.c_float)),
@@ -103,6 +109,8 @@ def library() -> ctypes.CDLL:
     kp = ctypes.POINTER(CKernels)
     lib.rocket_generate_kernels.argtypes = [ctypes.c_uint64, i32, i32, kp]
     lib.rocket_generate_kernels.restype = ctypes.c_int
+    lib.rocket_generate_kernels_multi.argtypes = [ctypes.c_uint64, i32, i32, i32, kp]
+    lib.rocket_generate_kernels_multi.restype = ctypes.c_int
     lib.rocket_free_kernels.argtypes = [kp]
     lib.rocket_free_kernels.restype = None
     lib.rocket_plan_create.argtypes = [kp, i32, ctypes.POINTER(vp)]
@@ -143,19 +151,56 @@ def _ptr(a: np.ndarray, ctype):
 
 
 def as_c_kernels(kernels: dict):
-    """A CKernels view of numpy kernel arrays (kept alive by the returned tuple)."""
+    """A CKernels view of numpy kernel arrays (kept alive by the returned
+    tuple).  Univariate sets: weights [K, max_len].  Multivariate sets carry
+    n_channels C > 1, channel_count [K], channel_index [K, C] and weights
+    [K, C, max_len]."""
     length = np.ascontiguousarray(kernels["length"], dtype=np.int32)
     dilation = np.ascontiguousarray(kernels["dilation"], dtype=np.int32)
     padding = np.ascontiguousarray(kernels["padding"], dtype=np.int32)
     bias = np.ascontiguousarray(kernels["bias"], dtype=np.float32)
     weights = np.ascontiguousarray(kernels["weights"], dtype=np.float32)
-    if weights.ndim != 2 or weights.shape[0] != length.shape[0]:
-        raise ValueError("weights must be [n_kernels, max_len]")
-    c = CKernels(int(length.shape[0]), int(kernels.get("input_length", 0)), int(weights.shape[1]),
+    K = length.shape[0]
+    C = int(kernels.get("n_channels", 1))
+    if C > 1:
+        if weights.ndim != 3 or weights.shape[:2] != (K, C):
+            raise ValueError("multivariate weights must be [n_kernels, n_channels, max_len]")
+        count = np.ascontiguousarray(kernels["channel_count"], dtype=np.int32)
+        index = np.ascontiguousarray(kernels["channel_index"], dtype=np.int32)
+        if count.shape != (K,) or index.shape != (K, C):
+            raise ValueError("channel_count must be [n_kernels], channel_index [n_kernels, n_channels]")
+        count_p, index_p = _ptr(count, ctypes.c_int32), _ptr(index, ctypes.c_int32)
+        max_len = weights.shape[2]
+    else:
+        if weights.ndim != 2 or weights.shape[0] != K:
+            raise ValueError("weights must be [n_kernels, max_len]")
+        count = index = None
+        count_p = index_p = ctypes.POINTER(ctypes.c_int32)()
+        max_len = weights.shape[1]
+    c = CKernels(int(K), int(kernels.get("input_length", 0)), int(max_len),
                  _ptr(length, ctypes.c_int32), _ptr(dilation, ctypes.c_int32),
                  _ptr(padding, ctypes.c_int32), _ptr(bias, ctypes.c_float),
-                 _ptr(weights, ctypes.c_float))
-    return c, (length, dilation, padding, bias, weights)
+                 _ptr(weights, ctypes.c_float), C, count_p, index_p)
+    return c, (length, dilation, padding, bias, weights, count, index)
+
+
+def _kernels_to_numpy(ck) -> dict:
+    K, M, C = ck.n_kernels, ck.max_len, max(1, ck.n_channels)
+    out = dict(
+        length=np.ctypeslib.as_array(ck.length, (K,)).copy(),
+        dilation=np.ctypeslib.as_array(ck.dilation, (K,)).copy(),
+        padding=np.ctypeslib.as_array(ck.padding, (K,)).copy(),
+        bias=np.ctypeslib.as_array(ck.bias, (K,)).copy(),
+        input_length=ck.input_length,
+    )
+    if C > 1:
+        out["weights"] = np.ctypeslib.as_array(ck.weights, (K * C * M,)).copy().reshape(K, C, M)
+        out["n_channels"] = C
+        out["channel_count"] = np.ctypeslib.as_array(ck.channel_count, (K,)).copy()
+        out["channel_index"] = np.ctypeslib.as_array(ck.channel_index, (K * C,)).copy().reshape(K, C)
+    else:
+        out["weights"] = np.ctypeslib.as_array(ck.weights, (K * M,)).copy().reshape(K, M)
+    return out
 
 
 def generate_kernels(seed: int, n_kernels: int, input_length: int) -> dict:
@@ -165,18 +210,25 @@ def generate_kernels(seed: int, n_kernels: int, input_length: int) -> dict:
     _check(lib.rocket_generate_kernels(ctypes.c_uint64(seed & (2 ** 64 - 1)), n_kernels, input_length,
                                        ctypes.byref(ck)), "rocket_generate_kernels")
     try:
-        K, M = ck.n_kernels, ck.max_len
-        out = dict(
-            length=np.ctypeslib.as_array(ck.length, (K,)).copy(),
-            dilation=np.ctypeslib.as_array(ck.dilation, (K,)).copy(),
-            padding=np.ctypeslib.as_array(ck.padding, (K,)).copy(),
-            bias=np.ctypeslib.as_array(ck.bias, (K,)).copy(),
-            weights=np.ctypeslib.as_array(ck.weights, (K * M,)).copy().reshape(K, M),
-            input_length=ck.input_length,
-        )
+        return _kernels_to_numpy(ck)
     finally:
         lib.rocket_free_kernels(ctypes.byref(ck))
-    return out
+
+
+def generate_kernels_multi(seed: int, n_kernels: int, input_length: int, n_channels: int) -> dict:
+    """rocket_generate_kernels_multi (multivariate kernels, Sec. 3.3), copied
+    into numpy arrays: weights [K, C, 11], channel_count [K], channel_index
+    [K, C] (-1 past each kernel's count); for C = 1 the univariate form."""
+    lib = library()
+    ck = CKernels()
+    _check(lib.rocket_generate_kernels_multi(ctypes.c_uint64(seed & (2 ** 64 - 1)), n_kernels,
+                                             input_length, n_channels, ctypes.byref(ck)),
+           "rocket_generate_kernels_multi")
+    try:
+        # a one-channel set comes back in the univariate form (weights [K, 11])
+        return _kernels_to_numpy(ck)
+    finally:
+        lib.rocket_free_kernels(ctypes.byref(ck))
 
 
 def plan_tables(kernels: dict, L: int) -> dict:
@@ -191,7 +243,9 @@ def plan_tables(kernels: dict, L: int) -> dict:
             a = np.ctypeslib.as_array(ptr, (int(n),)).copy() if n > 0 else np.zeros(0)
             return a.reshape(shape) if shape is not None else a
         out = dict(
-            items=arr(t.items, t.n_items * 16, (int(t.n_items), 16)),
+            items=arr(t.items, t.n_items * t.item_words, (int(t.n_items), int(t.item_words))),
+            chan=arr(t.chan, t.n_chan),
+            n_channels=t.n_channels,
             lanes=arr(t.lanes, t.n_lanes),
             wpk=arr(t.wpk, t.n_wpk),
             slot_bias=arr(t.slot_bias, t.n_slots),
@@ -216,12 +270,18 @@ def _stream_handle(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _check_series(X, L: int):
+def _series_shape_ok(X, L: int, C: int) -> bool:
+    if C > 1:
+        return X.dim() == 3 and X.shape[1] == C and X.shape[2] == L
+    return X.dim() == 2 and X.shape[1] == L
+
+
+def _check_series(X, L: int, C: int = 1):
     import torch
     if not isinstance(X, torch.Tensor) or not X.is_cuda:
         raise TypeError("X must be a torch tensor on the GPU")
-    if X.dtype != torch.float32 or X.dim() != 2 or X.shape[1] != L or not X.is_contiguous():
-        raise ValueError("X must be contiguous float32 [n, %d]" % L)
+    if X.dtype != torch.float32 or not _series_shape_ok(X, L, C) or not X.is_contiguous():
+        raise ValueError("X must be contiguous float32 %s" % ("[n, %d, %d]" % (C, L) if C > 1 else "[n, %d]" % L))
 
 
 class Plan:
@@ -240,6 +300,7 @@ class Plan:
                "rocket_plan_create")
         self._h = h
         self.features_per_kernel = 3 if mpv else 2
+        self.n_channels = max(1, int(self._c.n_channels))
 
     def info(self) -> dict:
         f = CPlanFacts()
@@ -257,7 +318,7 @@ class Plan:
         """F[n, fK] <- features of X[n, L] (f = 2, or 3 with MPV);
         asynchronous on `stream`."""
         import torch
-        _check_series(X, self.L)
+        _check_series(X, self.L, self.n_channels)
         n = X.shape[0]
         if (not isinstance(F, torch.Tensor) or not F.is_cuda or F.dtype != torch.float32
                 or tuple(F.shape) != (n, self.n_features) or not F.is_contiguous()):
@@ -283,8 +344,8 @@ class Plan:
         F_t = F_host if isinstance(F_host, torch.Tensor) else torch.from_numpy(F_host)
         if X_t.is_cuda or F_t.is_cuda:
             raise ValueError("transform_host takes host tensors")
-        if X_t.dtype != torch.float32 or not X_t.is_contiguous() or X_t.dim() != 2 or X_t.shape[1] != self.L:
-            raise ValueError("X_host must be a contiguous float32 [n, %d] array" % self.L)
+        if X_t.dtype != torch.float32 or not X_t.is_contiguous() or not _series_shape_ok(X_t, self.L, self.n_channels):
+            raise ValueError("X_host must be a contiguous float32 series array for this plan")
         n = X_t.shape[0]
         if (F_t.dtype != torch.float32 or not F_t.is_contiguous()
                 or tuple(F_t.shape) != (n, self.n_features)):
@@ -313,8 +374,9 @@ def transform(X, kernels: dict, stream=None):
     """One-shot rocket_transform: returns F[n, 2K] (blocks until done)."""
     import torch
     c, keep = as_c_kernels(kernels)
-    L = int(X.shape[1])
-    _check_series(X, L)
+    C = max(1, int(c.n_channels))
+    L = int(X.shape[-1]) if C > 1 else int(X.shape[1])
+    _check_series(X, L, C)
     F = torch.empty((X.shape[0], 2 * c.n_kernels), dtype=torch.float32, device=X.device)
     _check(library().rocket_transform(ctypes.c_void_p(X.data_ptr()), X.shape[0], L, ctypes.byref(c),
                                       ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),

@@ -21,6 +21,10 @@ row in fp64 (population standard deviation) and stored as fp32, row-major.
                   trend of slope U(-0.05, 0.05)
   paper_sweep     1,000 x 10,000, 10,000 kernels: Gaussian random walk (the
                   default point of the paper's timing sweep, Sec. 4)
+  multivariate    10,000 series x 6 channels x 500, 10,000 multivariate
+                  kernels (Sec. 3.3): per series, 3 latent random walks mixed
+                  into the 6 channels with random weights plus N(0, 0.3)
+                  noise; every channel z-normalised
 
 Kernel seed 200 + i and data seed 100 + i for workload i = 1 .. 5.
 """
@@ -40,6 +44,7 @@ class Workload:
     kernel_seed: int
     data_seed: int
     kind: str
+    channels: int = 1
 
 
 WORKLOADS = {
@@ -49,6 +54,7 @@ WORKLOADS = {
     "long": Workload("long", 1000, 16384, 10000, 204, 104, "walk_steps"),
     "many_short": Workload("many_short", 1000000, 64, 10000, 205, 105, "trend"),
     "paper_sweep": Workload("paper_sweep", 1000, 10000, 10000, 206, 106, "random_walk"),
+    "multivariate": Workload("multivariate", 10000, 500, 10000, 208, 108, "mixed_walks", 6),
 }
 
 
@@ -112,6 +118,21 @@ def _trend(rng, n, L, chunk=1 << 18):
     return out
 
 
+def make_multichannel(n: int, C: int, L: int, seed: int, chunk: int = 4096) -> np.ndarray:
+    """fp32 [n, C, L]: per series, 3 latent Gaussian random walks mixed into
+    C channels with N(0, 1) weights plus N(0, 0.3) noise, each channel
+    z-normalised in fp64."""
+    rng = np.random.default_rng(seed)
+    out = np.empty((n, C, L), dtype=np.float32)
+    for s0 in range(0, n, chunk):
+        m = min(chunk, n - s0)
+        lat = np.cumsum(rng.standard_normal((m, 3, L)), axis=2)
+        mix = rng.standard_normal((m, C, 3))
+        x = np.einsum("mcl,mlt->mct", mix, lat) + rng.normal(0.0, 0.3, size=(m, C, L))
+        out[s0:s0 + m] = znorm_rows(x.reshape(m * C, L)).reshape(m, C, L)
+    return out
+
+
 def make_series(kind: str, n: int, L: int, seed: int) -> np.ndarray:
     """fp32 [n, L] z-normalised series of the given kind."""
     rng = np.random.default_rng(seed)
@@ -131,8 +152,11 @@ def make_series(kind: str, n: int, L: int, seed: int) -> np.ndarray:
 
 
 def workload_series(name: str, n: int | None = None) -> np.ndarray:
-    """Series of a named workload (optionally only its first n rows)."""
+    """Series of a named workload (optionally only its first n rows):
+    [n, L], or [n, C, L] for multichannel workloads."""
     w = WORKLOADS[name]
+    if w.channels > 1:
+        return make_multichannel(w.n if n is None else n, w.channels, w.L, w.data_seed)
     return make_series(w.kind, w.n if n is None else n, w.L, w.data_seed)
 
 

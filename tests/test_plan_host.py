@@ -27,17 +27,29 @@ IDLE = 1 << 30
 
 def item_fields(row):
     (variant, d, p, O, S, rounds, lane_off, w_off, k_off, cost, n_long, n_short,
-     rounds_long) = (int(v) for v in row[:13])
-    inv_O = row[14:16].astype(np.int32).view(np.float64)[0]
+     rounds_long, n_ch, ch_off) = (int(v) for v in row[:15])
+    inv_O = row[16:18].astype(np.int32).view(np.float64)[0]
     return dict(variant=variant, d=d, p=p, O=O, S=S, rounds=rounds, lane_off=lane_off,
                 w_off=w_off, k_off=k_off, cost=cost, n_long=n_long, n_short=n_short,
-                rounds_long=rounds_long, inv_O=inv_O)
+                rounds_long=rounds_long, n_ch=n_ch, ch_off=ch_off, inv_O=inv_O)
+
+
+def kernel_row(kernels, k, c):
+    """Weights of kernel k for channel c (None if it does not read c)."""
+    C = int(kernels.get("n_channels", 1))
+    if C == 1:
+        return kernels["weights"][k] if c == 0 else None
+    for s_ in range(int(kernels["channel_count"][k])):
+        if int(kernels["channel_index"][k][s_]) == c:
+            return kernels["weights"][k][s_]
+    return None
 
 
 def walk(tables, kernels, L, X=None):
     """Replay the fused kernel's schedule; returns per-kernel coverage and,
     if X is given, fp32 features [n, 2K]."""
     K = len(kernels["length"])
+    C = int(kernels.get("n_channels", 1))
     lanes = tables["lanes"].astype(np.int64)
     halo_lo, stride, pad = tables["halo_lo"], tables["row_stride"], tables["tail_pad"]
     cover = [np.zeros(0, np.int64)] * K
@@ -45,8 +57,9 @@ def walk(tables, kernels, L, X=None):
     if X is not None:
         n = X.shape[0]
         F = np.full((n, 2 * K), np.nan, dtype=np.float64)
-        rows = np.zeros((n, stride), dtype=np.float32)
-        rows[:, halo_lo:halo_lo + L] = X
+        Xc = X.reshape(n, C, L)
+        rows = np.zeros((n, C, stride), dtype=np.float32)
+        rows[:, :, halo_lo:halo_lo + L] = Xc
     for row in tables["items"]:
         f = item_fields(row)
         d, p, O, S, ell = f["d"], f["p"], f["O"], f["S"], ELLS[f["variant"] // 2]
@@ -54,21 +67,33 @@ def walk(tables, kernels, L, X=None):
         nslot = 4 * G
         kid = tables["slot_kernel"][f["k_off"]:f["k_off"] + nslot]
         bias = tables["slot_bias"][f["k_off"]:f["k_off"] + nslot]
-        W = tables["wpk"][f["w_off"]:f["w_off"] + G * ell * 4].reshape(G, ell, 4)
-        Wslot = np.concatenate([W[g].T for g in range(G)], axis=0)  # [slot, tap]
+        nch = f["n_ch"]
+        chans = tables["chan"][f["ch_off"]:f["ch_off"] + nch].astype(np.int64)
+        assert nch >= 1 and np.all(np.diff(chans) > 0) and chans.min() >= 0 and chans.max() < C
+        W = tables["wpk"][f["w_off"]:f["w_off"] + nch * G * ell * 4].reshape(nch, G, ell, 4)
+        # [channel, slot, tap]
+        Wslot = np.stack([np.concatenate([W[ci, g].T for g in range(G)], axis=0) for ci in range(nch)])
+        used = np.zeros(nch, bool)
         for s_, k in enumerate(kid):
             if k >= 0:
                 ln = int(kernels["length"][k])
-                assert np.array_equal(Wslot[s_, :ln], kernels["weights"][k, :ln])
-                assert np.all(Wslot[s_, ln:] == 0)
+                for ci, c in enumerate(chans):
+                    row = kernel_row(kernels, k, c)
+                    if row is None:
+                        assert np.all(Wslot[ci, s_] == 0)
+                    else:
+                        used[ci] = True
+                        assert np.array_equal(Wslot[ci, s_, :ln], row[:ln])
+                        assert np.all(Wslot[ci, s_, ln:] == 0)
                 assert bias[s_] == np.float32(kernels["bias"][k])
                 assert (int(kernels["dilation"][k]), int(kernels["padding"][k])) == (d, p)
             else:
-                assert np.all(Wslot[s_] == 0)
+                assert np.all(Wslot[:, s_] == 0)
+        assert used.all()     # the channel list is exactly the union
         n_chunks = f["n_long"] + f["n_short"]
         assert f["rounds"] == -(-n_chunks // 64) and f["rounds_long"] == -(-f["n_long"] // 64)
         steps = f["rounds_long"] * S + (f["rounds"] - f["rounds_long"]) * (S - 1)
-        assert f["cost"] == steps * ell * G
+        assert f["cost"] == steps * ell * G * nch
         assert f["inv_O"] == 1.0 / O
         kept = []
         ys = [] if X is not None else None
@@ -103,10 +128,12 @@ def walk(tables, kernels, L, X=None):
             if X is not None:
                 qa = np.concatenate([q0[l] + np.arange(keep_steps[l]) * d for l in range(64)])
                 tap_idx = halo_lo - p + qa[:, None] + np.arange(ell)[None, :] * d
-                xv = rows[:, tap_idx]                                 # [n, output, tap]
-                acc = np.broadcast_to(bias.astype(np.float32), xv.shape[:2] + (nslot,)).copy()
-                for j in range(ell):
-                    acc = (acc + xv[..., j, None] * Wslot[None, None, :, j]).astype(np.float32)
+                acc = np.broadcast_to(bias.astype(np.float32), (n, qa.shape[0], nslot)).copy()
+                # channel by channel, tap by tap, in the kernel's order
+                for ci, c in enumerate(chans):
+                    xv = rows[:, c][:, tap_idx]                       # [n, output, tap]
+                    for j in range(ell):
+                        acc = (acc + xv[..., j, None] * Wslot[ci][None, None, :, j]).astype(np.float32)
                 ys.append(acc)
         allq = np.concatenate(kept)
         for k in kid[kid >= 0]:
@@ -196,7 +223,7 @@ def test_item_cost_and_groups():
     ell = np.array(ELLS)[items[:, 0] // 2]
     S, rounds, rounds_long = items[:, 4], items[:, 5], items[:, 12]
     steps = rounds_long * S + (rounds - rounds_long) * (S - 1)
-    np.testing.assert_array_equal(items[:, 9], steps * ell * G)
+    np.testing.assert_array_equal(items[:, 9], steps * ell * G * items[:, 13])
     # a bucket is split into groups of 8 with at most one smaller group
     assert (G == 2).sum() > (G == 1).sum()
     # small dilations need one round of long chunks per series
@@ -224,3 +251,25 @@ def test_ppv_through_double_reciprocal():
     want = c_all.astype(np.float32) / O_all.astype(np.float32)
     got = (c_all.astype(np.float64) * (1.0 / O_all.astype(np.float64))).astype(np.float32)
     assert np.array_equal(want, got)
+
+
+@pytest.mark.parametrize("seed,K,L,C", [(21, 200, 60, 3), (22, 300, 150, 6)])
+def test_multichannel_walk_matches_oracle(oracle, seed, K, L, C):
+    """Multivariate sets: every item's channel list is the union of its
+    kernels' channels, the packed weights are each kernel's row for each
+    channel (zero for channels it does not read), and the replay over
+    channels then taps lands inside the oracle's bounds."""
+    rng = np.random.default_rng(seed)
+    ks = rk.generate_kernels_multi(seed, K, L, C)
+    X = rng.standard_normal((3, C, L)).cumsum(axis=2)
+    X = ((X - X.mean(2, keepdims=True)) / X.std(2, keepdims=True)).astype(np.float32)
+    check_tables(ks, L, X, oracle)
+
+
+def test_multichannel_generator_matches_oracle():
+    from oracle import rocket_oracle as o
+    for C in (2, 5, 32):
+        a = rk.generate_kernels_multi(77, 300, 500, C)
+        b = o.generate_kernels_multi(77, 300, 500, C)
+        for key in ("length", "dilation", "padding", "bias", "channel_count", "channel_index", "weights"):
+            assert np.array_equal(a[key], b[key]), (C, key)
