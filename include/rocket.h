@@ -153,7 +153,7 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
 /* Plan flags for rocket_plan_create_ex. */
 #define ROCKET_PLAN_DEFAULT 0u
 #define ROCKET_PLAN_DIRECT 1u  /* use the plain one-wavefront-per-pair kernel */
-#define ROCKET_PLAN_CLAMPED 2u /* fused kernel with clamped indices (one-zero margins) */
+#define ROCKET_PLAN_CLAMPED 2u /* fused kernel with the long-series row layout */
 #define ROCKET_PLAN_MPV 4u     /* a third feature per kernel: mean of positive values */
 
 /*
@@ -161,11 +161,12 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
  * kernel: one wavefront per (series, kernel) pair reading the series from
  * global memory.  It is slower and serves as a second GPU reference; the
  * default plan also falls back to it when a series does not fit one
- * workgroup's LDS even with clamped indices.  ROCKET_PLAN_CLAMPED forces the
- * layout the default plan picks for long series: rows staged with a single
- * zero on each side and every series index clamped into [-1, L] (same
- * results; two more instructions per load).  ROCKET_PLAN_DIRECT together
- * with ROCKET_PLAN_CLAMPED is ROCKET_ERR_INVALID_ARG.
+ * workgroup's LDS even in the long-series layout.  ROCKET_PLAN_CLAMPED
+ * forces the layout the default plan picks for long series: rows staged with
+ * 512 zeros on each side, and the series offset of each block of tiles
+ * clamped into those margins on the scalar unit (same results).
+ * ROCKET_PLAN_DIRECT together with ROCKET_PLAN_CLAMPED is
+ * ROCKET_ERR_INVALID_ARG.
  * ROCKET_PLAN_MPV adds a third feature per kernel, the mean of the positive
  * values (MPV; the CUROCKET paper, Sec. 5, names it as a feature that does
  * not depend on time positions and so fuses into the same pass):
@@ -231,10 +232,11 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks)
  *   lds_bytes    LDS one workgroup uses (0 for the direct kernel)
  *   direct       1 if the plan runs the direct kernel, else 0
- *   clamped      1 if the fused kernel stages rows with a single zero on
- *                each side and clamps series indices (chosen when the full
- *                zero margins of the padded kernels would not fit in LDS,
- *                or forced by ROCKET_PLAN_CLAMPED), else 0
+ *   clamped      1 if the fused kernel stages rows with 512 zeros on each
+ *                side and clamps each block's series offset into them
+ *                (chosen when the full zero margins of the padded kernels
+ *                would not fit in LDS, or forced by ROCKET_PLAN_CLAMPED),
+ *                else 0
  *   features_per_kernel  2 (PPV, MAX) or 3 (PPV, MAX, MPV)
  *   rows_per_block       series staged per workgroup (0 for the direct kernel)
  */
@@ -258,25 +260,19 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  * touched).  rocket_plan_tables_build validates like rocket_plan_create and
  * fills *out with library-owned arrays; free them with
  * rocket_plan_tables_free (NULL-safe, idempotent).
- *   items        n_items x item_words (20) int32, one row per work item:
- *                [variant, dilation, padding, outputs O, steps S, rounds,
- *                 lane_off, w_off, k_off, cost, n_long, n_short,
- *                 rounds_long, n_ch, ch_off, 0, inv_O (words 16-17: 1/O as
- *                 an IEEE double, little-endian), 0, 0];
+ *   items        n_items x item_words (16) int32, one row per work item:
+ *                [variant, dilation, padding, outputs O, tiles, w_off,
+ *                 k_off, cost, n_ch, ch_off, 0, 0, 0, 0, inv_O (words
+ *                 14-15: 1/O as an IEEE double, little-endian)];
  *                n_ch channels, listed in chan[ch_off .. ch_off + n_ch),
  *                are the union of the channels the item's kernels read
  *                (1 and channel 0 for univariate sets);
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
  *                7/9/11 taps, G kernel groups of 4 slots;
- *                every residue class (outputs r, r+d, ...) is split into
- *                chunks of S or S-1 outputs, the n_long chunks of S outputs
- *                first; each round hands the next 64 chunks to the 64 lanes;
- *                the first rounds_long rounds run S steps, the rest S-1
- *   lanes        lane table: per item and round, 64 entries: bits 0-23 the
- *                output position of the lane's first step; bit 31 set: the
- *                lane's chunk has S-1 outputs in a round of S steps (the
- *                last step is computed and discarded); bit 30 set: the lane
- *                has no chunk (every step is discarded)
+ *                the O outputs are computed in tiles = ceil(O / 64) tiles
+ *                of 64 consecutive positions (lane l of tile k computes
+ *                output 64k + l; lanes past O compute nothing that counts);
+ *                cost = MFMA instructions per series (tiles x taps x G x n_ch)
  *   wpk          packed weights, per item [n_ch][G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in
@@ -285,8 +281,11 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                order[split_begin[layout_off[i] + v*ns + s] ..
  *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..5
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
+ *                of the padded layout (every tap of every real output lands
+ *                inside the row)
  *   tail_pad     zeros staged after the last row of a workgroup, so that
- *                the discarded extra steps read inside the staged memory
+ *                the lanes past O of an item's last tile read inside the
+ *                staged memory
  */
 typedef struct {
     int64_t n_items;
@@ -295,8 +294,6 @@ typedef struct {
     const int32_t *items;
     int64_t n_chan;
     const int32_t *chan;
-    int64_t n_lanes;
-    const uint32_t *lanes;
     int64_t n_wpk;
     const float *wpk;
     int64_t n_slots;

@@ -1,7 +1,8 @@
 // Host-side planning: validation, bucketing of kernels by (length, dilation,
-// padding), work items, lane tables and packed weights for the fused MFMA
+// padding), work items, packed weights and item orders for the fused MFMA
 // kernel.  Pure host code; no HIP calls.
 #include <algorithm>
+#include <climits>
 #include <cstring>
 #include <map>
 #include <new>
@@ -48,100 +49,6 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Outputs of residue class r (positions r, r+d, ...) for r < d.
-static int64_t residue_count(int64_t O, int64_t d, int64_t r) { return r < O ? ceil_div(O - r, d) : 0; }
-
-// Chunk counts of the balanced split of every residue class into nc chunks.
-static Chunking split_counts(int64_t O, int64_t d, int64_t nc) {
-    Chunking c;
-    c.nc = nc;
-    const int64_t C = ceil_div(O, d);          // longest residue class
-    c.S = ceil_div(C, nc);
-    // residue classes hold C or C-1 outputs (or none when O < d)
-    const int64_t n_big = std::min(d, O - (C - 1) * d);
-    const int64_t n_small = std::min(d, O) - n_big;
-    auto add = [&](int64_t cr, int64_t count) {
-        if (cr <= 0 || count <= 0) return;
-        const int64_t q = cr / nc, r = cr % nc;  // r chunks of q+1, nc-r of q
-        auto put = [&](int64_t len, int64_t n) {
-            if (len <= 0 || n <= 0) return;
-            if (len == c.S) c.n_long += n;
-            else c.n_short += n;  // len == S - 1
-        };
-        put(q + 1, r * count);
-        put(q, (nc - r) * count);
-    };
-    add(C, n_big);
-    add(C - 1, n_small);
-    c.rounds = ceil_div(c.n_long + c.n_short, kWave);
-    c.rounds_long = ceil_div(c.n_long, kWave);
-    return c;
-}
-
-// Estimated cycles of one series for one group of 4 kernels: a step costs
-// `ell` MFMAs plus the count and max reductions and its share of the window
-// loads; a round costs its lane-table load, address and bias set-up.
-static int64_t chunking_cost(const Chunking &c, int ell) {
-    return c.steps() * (10 * ell + 30) + c.rounds * (4 * ell + 100);
-}
-
-Chunking choose_chunking(int64_t O, int64_t d, int ell) {
-    const int64_t C = ceil_div(O, d);
-    Chunking best;
-    int64_t best_cost = -1;
-    const int64_t nc_max = std::min<int64_t>(C, 4096);
-    for (int64_t nc = 1; nc <= nc_max; ++nc) {
-        const Chunking c = split_counts(O, d, nc);
-        const int64_t cost = chunking_cost(c, ell);
-        if (best_cost < 0 || cost < best_cost) {
-            best_cost = cost;
-            best = c;
-        }
-    }
-    return best;
-}
-
-// Lane table of one bucket: the long chunks, then the short ones, each
-// numbered residue-fastest so neighbouring lanes work on neighbouring
-// positions, cut into rounds of 64.  Short chunks in a round of S steps get
-// kLaneShort; lanes past the last chunk get kLaneIdle and the position of
-// the round's first chunk.  Returns how far (in floats) the discarded
-// extra step of a short chunk reads past the end of the staged row
-// (`row_end` = L + halo_hi, relative to series index 0).
-static int64_t build_lane_table(int64_t O, int64_t d, int64_t p, int ell, const Chunking &c,
-                                int64_t row_end, std::vector<uint32_t> &lanes) {
-    std::vector<uint32_t> longs, shorts;
-    for (int64_t k = 0; k < c.nc; ++k)
-        for (int64_t r = 0; r < std::min(d, O); ++r) {
-            const int64_t cr = residue_count(O, d, r);
-            const int64_t st = k * cr / c.nc, en = (k + 1) * cr / c.nc;
-            const int64_t len = en - st;
-            if (len <= 0) continue;
-            (len == c.S ? longs : shorts).push_back((uint32_t)(r + st * d));
-        }
-    std::vector<uint32_t> all(longs);
-    all.insert(all.end(), shorts.begin(), shorts.end());
-    const int64_t n = (int64_t)all.size();
-    int64_t overflow = 0;
-    for (int64_t rd = 0; rd < c.rounds; ++rd) {
-        const bool long_round = rd < c.rounds_long;
-        for (int64_t i = rd * kWave; i < (rd + 1) * kWave; ++i) {
-            if (i >= n) {
-                lanes.push_back(all[rd * kWave] | kLaneIdle);
-            } else if (long_round && i >= (int64_t)longs.size()) {
-                lanes.push_back(all[i] | kLaneShort);
-                // the extra step sits at q + (S-1) d; its last tap reads
-                // series index q + (S-1) d - p + (ell-1) d
-                const int64_t last = (int64_t)all[i] + (c.S - 1 + ell - 1) * d - p;
-                overflow = std::max<int64_t>(overflow, last + 1 - row_end);
-            } else {
-                lanes.push_back(all[i]);
-            }
-        }
-    }
-    return overflow;
-}
-
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
     try {
         HostPlan P;
@@ -168,9 +75,10 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         // bucket kernels by (length, dilation, padding); kernels keep their
         // original order inside a bucket
         std::map<std::tuple<int32_t, int32_t, int32_t>, std::vector<int32_t>> buckets;
-        // every computed output is a real one, so the taps reach from
-        // position -p to L-1+p, plus (ell - length) taps of zero weight for
-        // kernels run at a longer code length
+        // the taps of real outputs reach from position -p to L-1+p, plus
+        // (ell - length) taps of zero weight for kernels run at a longer
+        // code length; lanes past O in an item's last tile read up to 63
+        // positions further (tail_pad, below)
         int64_t halo_lo = 0, halo_hi = 0;
         for (int32_t i = 0; i < k->n_kernels; ++i) {
             const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
@@ -190,7 +98,6 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             P.row_stride = (int32_t)stride;
         }
 
-        int64_t tail_pad = 0;
         for (auto &kv : buckets) {
             const int32_t len = std::get<0>(kv.first), d = std::get<1>(kv.first),
                           p = std::get<2>(kv.first);
@@ -203,31 +110,19 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             const int eidx = ell_index_for(len);
             const int ell = kEllValues[eidx];
             const int64_t O = output_length(L, len, d, p);
-            const Chunking ch = choose_chunking(O, d, ell);
-            const int32_t S = (int32_t)ch.S;
-            const int32_t rounds = (int32_t)ch.rounds;
+            const int64_t n_tiles = ceil_div(O, kTile);
             size_t pos = 0;
-            bool table_built = false;
-            int32_t lane_off = 0;
             while (pos < ids.size()) {
                 const size_t rem = ids.size() - pos;
                 const int G = rem > 4 ? 2 : 1;
                 const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
-                if (!table_built) {
-                    lane_off = (int32_t)P.lanes.size();
-                    tail_pad = std::max(tail_pad, build_lane_table(O, d, p, ell, ch,
-                                                                   (int64_t)L + halo_hi, P.lanes));
-                    table_built = true;
-                }
                 ItemDesc it;
                 std::memset(&it, 0, sizeof(it));
                 it.variant = eidx * 2 + (G - 1);
                 it.d = d;
                 it.p = p;
                 it.O = (int32_t)O;
-                it.S = S;
-                it.rounds = rounds;
-                it.lane_off = lane_off;
+                it.n_tiles = (int32_t)n_tiles;
                 it.w_off = (int32_t)P.wpk.size();
                 it.k_off = (int32_t)P.kid.size();
                 uint64_t umask = 0;
@@ -239,10 +134,9 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                         P.chan.push_back(c);
                         ++it.n_ch;
                     }
-                it.cost = (int32_t)(ch.steps() * ell * G * it.n_ch);
-                it.n_long = (int32_t)ch.n_long;
-                it.n_short = (int32_t)ch.n_short;
-                it.rounds_long = (int32_t)ch.rounds_long;
+                // MFMA instructions per series: ell taps per tile and group,
+                // for every channel of the item (capped: it only orders work)
+                it.cost = (int32_t)std::min<int64_t>(n_tiles * ell * G * it.n_ch, INT32_MAX);
                 it.inv_O = 1.0 / (double)O;
                 // A-operand weights: [channel][g][j][slot i]; zeros for empty
                 // slots, for channels a slot's kernel does not read and for
@@ -271,12 +165,12 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                     }
                 }
                 P.items.push_back(it);
-                P.mfma_per_row += it.cost;
+                P.mfma_per_row += n_tiles * ell * G * it.n_ch;
                 pos += take;
             }
         }
 
-        P.tail_pad = P.row_stride > 0 ? (int32_t)tail_pad : 0;
+        P.tail_pad = kTile;
 
         // item orders: per variant, largest cost first (longest-processing-
         // time first), dealt to splits greedily by accumulated cost
@@ -336,8 +230,6 @@ extern "C" rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32
     out->chan = P->chan.data();
     out->n_channels = P->n_channels;
     out->items = reinterpret_cast<const int32_t *>(P->items.data());
-    out->n_lanes = (int64_t)P->lanes.size();
-    out->lanes = P->lanes.data();
     out->n_wpk = (int64_t)P->wpk.size();
     out->wpk = P->wpk.data();
     out->n_slots = (int64_t)P->kid.size();

@@ -23,46 +23,42 @@ constexpr int kWave = 64;
 constexpr int kSlotsPerGroup = 4;
 constexpr int kMaxGroups = 2;  // a work item holds 4 or 8 kernels of one bucket
 
-// One work item: up to 4*G kernels that share (length, dilation, padding).
-// The 64 lanes of a wavefront each own a chunk of consecutive outputs along
-// one dilation residue class (positions q, q+d, q+2d, ...).  Each residue
-// class is split into nc chunks of balanced length, S or S-1 outputs.  A
-// "round" hands 64 chunks to the 64 lanes and runs a fixed number of steps
-// for all of them: the chunks of S outputs come first, so the first
-// rounds_long rounds run S steps and the rest S-1.  In a round of S steps a
-// lane holding an (S-1)-output chunk computes one extra output past its
-// chunk, and a lane without a chunk computes junk; both start those
-// accumulations from -inf (lane-table flags), so they change neither the
-// count nor the max.  Every real output is computed by exactly one lane.
-struct alignas(16) ItemDesc {
-    int32_t variant;      // ell_index * 2 + (G - 1)
-    int32_t d;            // dilation
-    int32_t p;            // padding
-    int32_t O;            // number of dot products (outputs)
-    int32_t S;            // steps of a long chunk (short chunks: S - 1)
-    int32_t rounds;       // rounds per series
-    int32_t lane_off;     // first lane-table entry (rounds * 64 entries)
-    int32_t w_off;        // first packed weight: [n_ch][G][ell][4] floats
-    int32_t k_off;        // first slot entry: kernel ids and biases, [4G]
-    int32_t cost;         // MFMA instructions per series (scheduling weight)
-    int32_t n_long;       // chunks of S outputs
-    int32_t n_short;      // chunks of S - 1 outputs
-    int32_t rounds_long;  // rounds that run S steps: ceil(n_long / 64)
-    int32_t n_ch;         // channels the item's kernels read (their union; 1 if univariate)
-    int32_t ch_off;       // first entry of the item's channel list
-    int32_t reserved0;
-    double inv_O;         // 1 / O rounded to double (exact PPV, see transform.hip)
-    int32_t reserved1[2];
-};
-static_assert(sizeof(ItemDesc) == 80, "ItemDesc must stay 80 bytes");
-constexpr int kItemWords = (int)(sizeof(ItemDesc) / sizeof(int32_t));
+// Outputs are computed in tiles of 64 consecutive positions: lane l of a
+// wavefront computes output 64*k + l of tile k for every kernel slot of the
+// item.  A block runs kTilesPerBlock[G-1] tiles at once (the independent
+// MFMA accumulation chains of a wavefront: tiles x groups = 8).
+constexpr int kTile = kWave;
+constexpr int kTilesPerBlock[kMaxGroups] = {8, 4};
+constexpr int kMaxTilesPerBlock = 8;
 
-// Lane-table entry: the output position of the lane's first step (below
-// 2^24) and two flags.
+// Clamped row layout (long series): each staged row carries this many zeros
+// on each side; the series index of a block's first lane is clamped into
+// [-kClampMargin, L] on the scalar unit, so a block whose 64*NT positions all
+// fall outside the series reads zeros from a margin.
+constexpr int kClampMargin = kTile * kMaxTilesPerBlock;
+
+// Every output of an item is computed by exactly one lane of one tile; lanes
+// of the last tile past O start from -inf and change no feature.
 constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
-constexpr uint32_t kLanePosMask = 0x00FFFFFFu;
-constexpr uint32_t kLaneShort = 1u << 31;  // chunk is one output short: last step discarded
-constexpr uint32_t kLaneIdle = 1u << 30;   // no chunk: every step discarded
+
+// One work item: up to 4*G kernels that share (length, dilation, padding),
+// so every slot has the same O outputs and reads the same series values.
+struct alignas(16) ItemDesc {
+    int32_t variant;   // ell_index * 2 + (G - 1)
+    int32_t d;         // dilation
+    int32_t p;         // padding
+    int32_t O;         // number of dot products (outputs)
+    int32_t n_tiles;   // ceil(O / 64)
+    int32_t w_off;     // first packed weight: [n_ch][G][ell][4] floats
+    int32_t k_off;     // first slot entry: kernel ids and biases, [4G]
+    int32_t cost;      // MFMA instructions per series (scheduling weight)
+    int32_t n_ch;      // channels the item's kernels read (their union; 1 if univariate)
+    int32_t ch_off;    // first entry of the item's channel list
+    int32_t reserved[4];
+    double inv_O;      // 1 / O rounded to double (exact PPV, see transform.hip)
+};
+static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
+constexpr int kItemWords = (int)(sizeof(ItemDesc) / sizeof(int32_t));
 
 // Item orders for a few split counts.  Within a layout with `nsplit` splits
 // the items are grouped by variant, so that every workgroup runs one code
@@ -75,15 +71,14 @@ constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 struct HostPlan {
     int32_t n_kernels = 0;
     int32_t L = 0;
-    int32_t halo_lo = 0;   // zeros staged before the series in LDS
-    int32_t halo_hi = 0;   // zeros staged after the series in LDS
-    int32_t row_stride = 0;  // floats per staged row
-    int32_t tail_pad = 0;    // zeros staged after the last row (reads of discarded steps)
+    int32_t halo_lo = 0;     // padded layout: zeros staged before the series
+    int32_t halo_hi = 0;     // padded layout: zeros staged after the series
+    int32_t row_stride = 0;  // padded layout: floats per staged row (0: does not fit 32 bits)
+    int32_t tail_pad = 0;    // zeros staged after the last row (reads of lanes past O)
     int32_t n_channels = 1;  // channels per series
     int64_t n_buckets = 0;
     int64_t mfma_per_row = 0;
     std::vector<ItemDesc> items;
-    std::vector<uint32_t> lanes;
     std::vector<float> wpk;       // packed A-operand weights
     std::vector<float> bias;      // per slot
     std::vector<int32_t> kid;     // per slot, -1 = empty
@@ -98,15 +93,5 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L);
 
 // Build the host-side tables of a plan.  Assumes validate_kernels passed.
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out);
-
-// Chunking of one bucket: nc chunks per residue class, chunk lengths S and
-// S-1, with n_long / n_short chunks of each; rounds of 64 chunks, the first
-// rounds_long of them running S steps.  Chosen to minimise an estimate of
-// the cycles one series costs (MFMA steps, reductions, round set-up).
-struct Chunking {
-    int64_t nc = 1, S = 1, n_long = 0, n_short = 0, rounds = 0, rounds_long = 0;
-    int64_t steps() const { return rounds_long * S + (rounds - rounds_long) * (S - 1); }
-};
-Chunking choose_chunking(int64_t O, int64_t d, int ell);
 
 }  // namespace rocket

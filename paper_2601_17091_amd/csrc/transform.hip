@@ -1,23 +1,25 @@
 // ROCKET transform on CDNA4 (gfx950): fused MFMA kernel, plain direct
 // kernel, and the HIP-facing half of the C ABI.
 //
-// Fused kernel (one workgroup = one series x one split of the work items):
-//   1. the series is staged HBM -> LDS with coalesced loads, with zero
+// Fused kernel (one workgroup = a few series x one split of the work items
+// of one code variant):
+//   1. the series are staged HBM -> LDS with coalesced loads, with zero
 //      margins on both sides that stand in for the zero padding (Sec. 2.1);
 //   2. each wavefront takes work items from an LDS counter; an item holds 4
-//      or 8 kernels of one (length, dilation, padding) bucket;
-//   3. the dot products of a bucket are an outer-product contraction over the
+//      or 8 kernels of one (length, dilation, padding) bucket, which share
+//      their outputs' positions and the series values under every tap;
+//   3. outputs are computed in tiles of 64 consecutive positions, lane l
+//      taking position 64k + l of tile k; for tap j the 64 lanes read 64
+//      consecutive series values (index 64k - p + j*d + l), so a tile's
+//      loads are conflict-free and share one address register per tap;
+//   4. the dot products of a tile are an outer-product contraction over the
 //      taps: v_mfma_f32_4x4x1_16b_f32 multiplies the 4 kernels' weights (A,
-//      one kernel per block row) by 64 series values (B, one output position
-//      per lane), one tap per instruction, accumulating onto the bias;
-//   4. every lane walks a chunk of outputs along one dilation residue class,
-//      so successive outputs share all but one series value: a register
-//      window slides along the decimated series and each step loads one new
-//      value from LDS;
-//   5. MAX is a per-lane running max reduced across the wavefront at the end;
-//      the positive count is a ballot of y > 0 popcounted on the scalar unit;
-//      no dot product is written to memory (Sec. 3.2 keeps only the two
-//      counters per pair as well);
+//      one kernel per block row) by the 64 lanes' series values (B), one tap
+//      per instruction, accumulating onto the bias;
+//   5. MAX is a per-lane running max reduced across the wavefront at the end
+//      of a series; the positive count is a ballot of y > 0 popcounted on
+//      the scalar unit; no dot product is written to memory (Sec. 3.2 keeps
+//      only the two counters per pair as well);
 //   6. PPV = count / O and MAX are written to F in the original kernel order.
 #include <hip/hip_runtime.h>
 
@@ -50,6 +52,7 @@ constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
 constexpr int64_t kRowsLdsBudget = 30 * 1024;  // LDS for the series of one workgroup (5 per CU)
 constexpr int kMaxRowsPerBlock = 8;
 constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dealt round-robin
+constexpr int kTile = rocket::kTile;
 
 struct FusedArgs {
     const float *X;
@@ -62,7 +65,6 @@ struct FusedArgs {
     int32_t C;         // channels per series
     const int32_t *chan;  // item channel lists
     const ItemDesc *items;
-    const uint32_t *lanes;
     const float *wpk;
     const float *bias;
     const int32_t *kid;
@@ -71,7 +73,7 @@ struct FusedArgs {
     int32_t nsplit;
     int32_t n_variants;          // variants that have items, launched variant-major
     int32_t variants[rocket::kNumVariants];
-    int64_t tiles_per_xcd;       // row tiles (of rows_per_block series) per XCD
+    int64_t groups_per_xcd;      // row groups (of rows_per_block series) per XCD
     int32_t halo_lo;
     int32_t row_stride;
     int32_t tail_pad;        // zero floats staged after the last row
@@ -84,34 +86,40 @@ constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
 
-// Where a lane's window values come from.  value(m) is the zero-padded
-// series value under tap m of the lane's current step-0 output (positions
-// m*d apart); shifted(k) moves the window k positions along the row (k is
-// wavefront-uniform).
-//   PaddedRow:  the row sits in LDS with zero margins wide enough for every
-//               padded tap, so value(m) is one load at xs + m*d.
-//   ClampedRow: the row sits in LDS with one zero on each side (index -1 and
-//               L); value(m) clamps the series index into [-1, L] first.
-//               Used when the margins would not fit in LDS (long series);
-//               it costs two more VALU instructions per load.
-struct PaddedRow {
-    const float *xs;
+// Where a block's series values come from.  tap(j) is the lane's LDS
+// pointer for tap j of the block's first tile; tile u of the block reads
+// 64*u floats further.  channel(off) moves to another channel's row.
+//   PaddedTiles:  the row sits in LDS with zero margins wide enough for
+//                 every tap of every real output (and the tail pad after
+//                 the last row for the lanes past O), so tap j is at
+//                 x + j*d.
+//   ClampedTiles: the row sits in LDS with kClampMargin zeros on each side
+//                 (long series, whose full margins would not fit).  The
+//                 series index of lane 0 of tap j is clamped into
+//                 [-kClampMargin, L] on the scalar unit: a block whose
+//                 positions all lie left (right) of the series then reads
+//                 zeros from the left (right) margin, and a block that
+//                 overlaps the series is not moved, so every read stays in
+//                 the margins and yields the zero-padded value.
+struct PaddedTiles {
+    const float *x;  // the lane's value at series index t0 - p (t0: first output of the block)
     int d;
-    __device__ __forceinline__ float value(int m) const { return xs[m * d]; }
-    __device__ __forceinline__ PaddedRow shifted(int k) const { return PaddedRow{xs + k, d}; }
-    __device__ __forceinline__ PaddedRow channel(int off) const { return PaddedRow{xs + off, d}; }
+    __device__ __forceinline__ const float *tap(int j) const { return x + j * d; }
+    __device__ __forceinline__ PaddedTiles channel(int off) const { return PaddedTiles{x + off, d}; }
 };
 
-struct ClampedRow {
-    const float *row;  // series index 0
-    int i0;            // series index under tap 0 of the lane's step-0 output
+struct ClampedTiles {
+    const float *row;  // series index 0 of the row, plus the lane number
+    int b0;            // series index under tap 0 of lane 0 (wavefront-uniform)
     int d;
     int L;
-    __device__ __forceinline__ float value(int m) const {
-        return row[min(max(i0 + m * d, -1), L)];
+    __device__ __forceinline__ const float *tap(int j) const {
+        const int b = min(max(b0 + j * d, -rocket::kClampMargin), L);
+        return row + b;
     }
-    __device__ __forceinline__ ClampedRow shifted(int k) const { return ClampedRow{row, i0 + k, d, L}; }
-    __device__ __forceinline__ ClampedRow channel(int off) const { return ClampedRow{row + off, i0, d, L}; }
+    __device__ __forceinline__ ClampedTiles channel(int off) const {
+        return ClampedTiles{row + off, b0, d, L};
+    }
 };
 
 // Per-series accumulators of one work item, per lane and kernel slot: the
@@ -135,51 +143,41 @@ struct McCtx {
     int cstride;
 };
 
-// NS consecutive output steps of one round, as an outer-product contraction
-// over the taps: tap j of every step and kernel group is issued before tap
-// j+1, so the wavefront keeps NS*G independent MFMA accumulation chains in
-// flight.  With FIRST set each chain starts from binit (the slots' biases,
-// or -inf on a lane without a chunk) and, when LAST is also set (the block
-// ends the round), the final step starts from -inf on lanes with drop_last
-// set (a chunk one output short, or no chunk); without FIRST the chains
-// continue from acc (the next channel of a multichannel item).
-template <int ELL, int G, int NS, bool LAST, bool FIRST>
-__device__ __forceinline__ void block_mfma(const float (&xw)[NS + ELL - 1], const float (&wa)[G][ELL],
-                                           const v4f (&binit)[G], bool drop_last,
-                                           v4f (&acc)[NS][G]) {
+// The contraction of one block of NT tiles over the taps of one channel:
+// tap j of every tile and kernel group is issued before tap j+1, so the
+// wavefront keeps NT*G independent MFMA accumulation chains in flight.  With
+// FIRST set each chain starts from its start value (the slots' biases, or,
+// in the last tile of a row, -inf on lanes past the last output); without
+// it the chains continue from acc (the next channel of a multichannel item).
+template <int ELL, int G, int NT, bool LAST, bool FIRST, typename Src>
+__device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][ELL],
+                                          const v4f (&binit)[G], const v4f (&blast)[G],
+                                          v4f (&acc)[NT][G]) {
 #pragma unroll
-    for (int u = 0; u < NS; ++u)
+    for (int j = 0; j < ELL; ++j) {
+        const float *pj = src.tap(j);
+        float xv[NT];
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            v4f c;
-            if (FIRST) {
-                c = binit[g];
-                if (LAST && u == NS - 1) {
+        for (int u = 0; u < NT; ++u) xv[u] = pj[u * kTile];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
-                }
-            } else {
-                c = acc[u][g];
+        for (int u = 0; u < NT; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const v4f c = (FIRST && j == 0) ? ((LAST && u == NT - 1) ? blast[g] : binit[g])
+                                                : acc[u][g];
+                acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xv[u], c, 0, 0, 0);
             }
-            acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], c, 0, 0, 0);
-        }
-#pragma unroll
-    for (int j = 1; j < ELL; ++j)
-#pragma unroll
-        for (int u = 0; u < NS; ++u)
-#pragma unroll
-            for (int g = 0; g < G; ++g)
-                acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[u + j], acc[u][g], 0, 0, 0);
+    }
 }
 
-// Fold NS steps of finished dot products into the row accumulators.  A chain
+// Fold NT tiles of finished dot products into the row accumulators.  A chain
 // started at -inf stays -inf, so MAX folds every result (v_max3 over pairs of
-// steps), the positive count is a ballot of y > 0 popcounted on the scalar
+// tiles), the positive count is a ballot of y > 0 popcounted on the scalar
 // unit, and the MPV numerator adds max(y, 0).
-template <int G, int NS, bool MPV>
-__device__ __forceinline__ void block_reduce(const v4f (&acc)[NS][G], RowAcc<G> &ra) {
+template <int G, int NT, bool MPV>
+__device__ __forceinline__ void block_reduce(const v4f (&acc)[NT][G], RowAcc<G> &ra) {
 #pragma unroll
-    for (int u = 0; u < NS; ++u)
+    for (int u = 0; u < NT; ++u)
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
@@ -187,98 +185,77 @@ __device__ __forceinline__ void block_reduce(const v4f (&acc)[NS][G], RowAcc<G> 
                 ra.cnt[g][v] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][g][v] > 0.0f));
     if (MPV) {
 #pragma unroll
-        for (int u = 0; u < NS; ++u)
+        for (int u = 0; u < NT; ++u)
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) ra.ps[g][v] += fmaxf(acc[u][g][v], 0.0f);
     }
 #pragma unroll
-    for (int u = 0; u + 1 < NS; u += 2)
+    for (int u = 0; u + 1 < NT; u += 2)
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 ra.mx[g][v] = fmaxf(fmaxf(ra.mx[g][v], acc[u][g][v]), acc[u + 1][g][v]);
-    if (NS % 2 == 1) {
+    if (NT % 2 == 1) {
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int v = 0; v < 4; ++v) ra.mx[g][v] = fmaxf(ra.mx[g][v], acc[NS - 1][g][v]);
+            for (int v = 0; v < 4; ++v) ra.mx[g][v] = fmaxf(ra.mx[g][v], acc[NT - 1][g][v]);
     }
 }
 
-// The window under NS steps: NS + ELL - 1 values spaced d apart.
-template <int ELL, int NS, typename Src>
-__device__ __forceinline__ void load_window(const Src &src, float (&xw)[NS + ELL - 1]) {
-#pragma unroll
-    for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
-}
-
-// One block of NS steps.  Univariate items keep their weights in registers
+// One block of NT tiles.  Univariate items keep their weights in registers
 // (wa); multichannel items (MC) run the MFMA chains over every channel of
-// their list, reading each channel's window and weights in turn.
-template <int ELL, int G, int NS, bool LAST, bool MPV, bool MC, typename Src>
-__device__ __forceinline__ void step_block(const Src &src, const float (&wa)[G][ELL], const McCtx &mc,
-                                           const v4f (&binit)[G], bool drop_last, RowAcc<G> &ra) {
-    float xw[NS + ELL - 1];
-    v4f acc[NS][G];
+// their list, reading each channel's weights in turn.  The scheduling
+// barriers keep the block's MFMAs in one run and its reduction in another:
+// on gfx950 fp32 MFMA and VALU instructions of a SIMD do not execute at the
+// same time, and a VALU instruction placed between two MFMAs of a wavefront
+// costs more than the same instruction in a run of VALU work.
+template <int ELL, int G, int NT, bool LAST, bool MPV, bool MC, typename Src>
+__device__ __forceinline__ void tile_block(const Src &src, const float (&wa)[G][ELL],
+                                           const McCtx &mc, const v4f (&binit)[G],
+                                           const v4f (&blast)[G], RowAcc<G> &ra) {
+    v4f acc[NT][G];
     if constexpr (!MC) {
-#pragma unroll
-        for (int m = 0; m < NS + ELL - 1; ++m) xw[m] = src.value(m);
-#pragma unroll
-        for (int u = 0; u < NS; ++u)
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                v4f c = binit[g];
-                if (LAST && u == NS - 1) {
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) c[v] = drop_last ? -INFINITY : c[v];
-                }
-                acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][0], xw[u], c, 0, 0, 0);
-            }
-#pragma unroll
-        for (int j = 1; j < ELL; ++j)
-#pragma unroll
-            for (int u = 0; u < NS; ++u)
-#pragma unroll
-                for (int g = 0; g < G; ++g)
-                    acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xw[u + j], acc[u][g], 0, 0, 0);
+        tile_mfma<ELL, G, NT, LAST, true>(src, wa, binit, blast, acc);
     } else {
         float wc[G][ELL];
         for (int ci = 0; ci < mc.n_ch; ++ci) {
-            load_window<ELL, NS>(src.channel(mc.chan[ci] * mc.cstride), xw);
             const float *wp = mc.w + ci * (G * ELL * 4);
 #pragma unroll
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int j = 0; j < ELL; ++j) wc[g][j] = wp[(g * ELL + j) * 4];
+            const Src s = src.channel(mc.chan[ci] * mc.cstride);
             if (ci == 0)
-                block_mfma<ELL, G, NS, LAST, true>(xw, wc, binit, drop_last, acc);
+                tile_mfma<ELL, G, NT, LAST, true>(s, wc, binit, blast, acc);
             else
-                block_mfma<ELL, G, NS, LAST, false>(xw, wc, binit, drop_last, acc);
+                tile_mfma<ELL, G, NT, LAST, false>(s, wc, binit, blast, acc);
         }
     }
-    block_reduce<G, NS, MPV>(acc, ra);
+    __builtin_amdgcn_sched_barrier(0);
+    block_reduce<G, NT, MPV>(acc, ra);
 }
 
-// The last block of a round: its length nv (1..N) selects a code copy.
+// The last block of a row: its tile count nv (1..N) selects a code copy.
 template <int ELL, int G, int N, bool MPV, bool MC, typename Src>
-struct TailBlock {
+struct TailTiles {
     __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
                                                const McCtx &mc, const v4f (&binit)[G],
-                                               bool drop_last, RowAcc<G> &ra) {
+                                               const v4f (&blast)[G], RowAcc<G> &ra) {
         if (nv == N)
-            step_block<ELL, G, N, true, MPV, MC>(src, wa, mc, binit, drop_last, ra);
+            tile_block<ELL, G, N, true, MPV, MC>(src, wa, mc, binit, blast, ra);
         else
-            TailBlock<ELL, G, N - 1, MPV, MC, Src>::run(nv, src, wa, mc, binit, drop_last, ra);
+            TailTiles<ELL, G, N - 1, MPV, MC, Src>::run(nv, src, wa, mc, binit, blast, ra);
     }
 };
 
 template <int ELL, int G, bool MPV, bool MC, typename Src>
-struct TailBlock<ELL, G, 0, MPV, MC, Src> {
+struct TailTiles<ELL, G, 0, MPV, MC, Src> {
     __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL],
-                                               const McCtx &, const v4f (&)[G], bool,
+                                               const McCtx &, const v4f (&)[G], const v4f (&)[G],
                                                RowAcc<G> &) {}
 };
 
@@ -339,50 +316,6 @@ __device__ __forceinline__ float reduce4(const v4f &m) {
 // row 3 slot 3.
 __device__ __forceinline__ int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
 
-// Lane state of one round: where the lane's chunk starts, the start values
-// of its accumulations, and whether its last step is discarded.
-template <int G>
-struct RoundState {
-    v4f binit[G];
-    uint32_t pos;
-    int len;
-    bool drop_last;
-};
-
-template <int G>
-__device__ __forceinline__ void setup_round(const ItemDesc &it, int rd, const FusedArgs &a,
-                                            const float (&bias)[G][4], int lane,
-                                            RoundState<G> &st) {
-    // rounds of S steps first, then of S-1 steps
-    st.len = rd < it.rounds_long ? it.S : it.S - 1;
-    const uint32_t e = a.lanes[it.lane_off + rd * rocket::kWave + lane];
-    st.pos = e & rocket::kLanePosMask;
-    const bool idle = (e & rocket::kLaneIdle) != 0;
-    st.drop_last = (e & (rocket::kLaneShort | rocket::kLaneIdle)) != 0;
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) st.binit[g][v] = idle ? -INFINITY : bias[g][v];
-}
-
-// All steps of one round for one series; src.value(m) is the zero-padded
-// series value under tap m of the lane's step-0 output.
-template <int ELL, int G, int T, bool MPV, bool MC, typename Src>
-__device__ __forceinline__ void run_round(const Src &src, int d, const RoundState<G> &st,
-                                          const float (&wa)[G][ELL], const McCtx &mc,
-                                          RowAcc<G> &ra) {
-    const int nfull = (st.len - 1) / T;  // full blocks before the last block
-    const int nv = st.len - nfull * T;   // length of the last block, 1..T
-    // block b starts b*T*d positions along the row: a wavefront-uniform
-    // offset, so each load is one lane address plus a scalar
-    for (int blk = 0; blk < nfull; ++blk) {
-        const int off = __builtin_amdgcn_readfirstlane(blk * T * d);
-        step_block<ELL, G, T, false, MPV, MC>(src.shifted(off), wa, mc, st.binit, st.drop_last, ra);
-    }
-    TailBlock<ELL, G, T, MPV, MC, Src>::run(nv, src.shifted(__builtin_amdgcn_readfirstlane(nfull * T * d)),
-                                            wa, mc, st.binit, st.drop_last, ra);
-}
-
 template <int G, bool MPV>
 __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 #pragma unroll
@@ -440,27 +373,13 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int32_t *ki
     }
 }
 
-// One round over the series whose index 0 sits at `row` in LDS.
-template <int ELL, int G, int T, bool CLAMP, bool MPV, bool MC>
-__device__ __forceinline__ void run_row_round(const float *row, const ItemDesc &it, int L,
-                                              const RoundState<G> &st, const float (&wa)[G][ELL],
-                                              const McCtx &mc, RowAcc<G> &ra) {
-    const int i0 = (int)st.pos - it.p;  // series index under tap 0 of step 0
-    if (CLAMP)
-        run_round<ELL, G, T, MPV, MC>(ClampedRow{row, i0, it.d, L}, it.d, st, wa, mc, ra);
-    else
-        run_round<ELL, G, T, MPV, MC>(PaddedRow{row + i0, it.d}, it.d, st, wa, mc, ra);
-}
-
 // One work item over the `nrows` series staged in LDS: the item's weights
-// are loaded once and reused for every series.
+// are loaded once and reused for every series.  Each series runs the item's
+// tiles in blocks of NT (the last block holds the remaining 1..NT tiles).
 template <int ELL, int G, bool CLAMP, bool MPV, bool MC>
 __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0, int nrows,
                                          const FusedArgs &a, float *F0, int lane) {
-    // steps per block: 8 (G = 1) or 6 (G = 2) independent accumulation
-    // chains per wavefront; T = 3 for G = 2 keeps the kernel within 96 VGPRs
-    // (5 wavefronts per SIMD)
-    constexpr int T = G == 1 ? 8 : 3;
+    constexpr int NT = rocket::kTilesPerBlock[G - 1];
     // A operand: lane holds the weight of kernel slot (lane & 3) for every
     // tap; univariate items keep them in registers for the whole item,
     // multichannel ones read each channel's weights per block (McCtx)
@@ -475,36 +394,47 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
     if constexpr (MC) mc = McCtx{a.wpk + it.w_off + (lane & 3), as_const(a.chan) + it.ch_off, it.n_ch,
                                  a.row_stride};
     const int row_pitch = a.C * a.row_stride;  // floats per staged series (LDS offsets fit 32 bits)
-    // C operand of the first tap: the bias of block row v (kernel slot v)
-    // (wavefront-uniform: scalar registers)
-    float bias[G][4];
+    // C operand of the first tap: the bias of block row v (kernel slot v),
+    // and in the last tile of a series -inf on the lanes past the last
+    // output, so that they change no feature
+    const int rem = it.O - (it.n_tiles - 1) * kTile;  // real outputs in the last tile, 1..64
+    v4f binit[G], blast[G];
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) bias[g][v] = as_const(a.bias)[it.k_off + 4 * g + v];
+        for (int v = 0; v < 4; ++v) {
+            const float b = as_const(a.bias)[it.k_off + 4 * g + v];
+            binit[g][v] = b;
+            blast[g][v] = lane < rem ? b : -INFINITY;
+        }
+    const int nfull = (it.n_tiles - 1) / NT;  // full blocks before the last block
+    const int nv = it.n_tiles - nfull * NT;   // tiles in the last block, 1..NT
     // after the reduction, lane 16q writes slot slot_of_row(q) of each group
     const int32_t *kid_row = a.kid + it.k_off;
     const int64_t f_stride = (int64_t)a.nf * a.K;
-    RoundState<G> st;
-    if (it.rounds == 1) {
-        // one round (small dilations): its lane state serves every series
-        setup_round<G>(it, 0, a, bias, lane, st);
-        for (int r = 0; r < nrows; ++r) {
-            RowAcc<G> ra;
-            init_row<G, MPV>(ra);
-            run_row_round<ELL, G, T, CLAMP, MPV, MC>(rows0 + r * row_pitch, it, a.L, st, wa, mc, ra);
-            write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
+    for (int r = 0; r < nrows; ++r) {
+        RowAcc<G> ra;
+        init_row<G, MPV>(ra);
+        const float *row = rows0 + r * row_pitch + lane;
+        // block b starts at output b*NT*64; its lane 0 reads series index
+        // b*NT*64 - p under tap 0 (a wavefront-uniform offset)
+        for (int blk = 0; blk < nfull; ++blk) {
+            const int b0 = blk * (NT * kTile) - it.p;
+            if constexpr (CLAMP)
+                tile_block<ELL, G, NT, false, MPV, MC>(ClampedTiles{row, b0, it.d, a.L}, wa, mc, binit,
+                                                       blast, ra);
+            else
+                tile_block<ELL, G, NT, false, MPV, MC>(PaddedTiles{row + b0, it.d}, wa, mc, binit, blast,
+                                                       ra);
         }
-    } else {
-        for (int r = 0; r < nrows; ++r) {
-            RowAcc<G> ra;
-            init_row<G, MPV>(ra);
-            for (int rd = 0; rd < it.rounds; ++rd) {
-                setup_round<G>(it, rd, a, bias, lane, st);
-                run_row_round<ELL, G, T, CLAMP, MPV, MC>(rows0 + r * row_pitch, it, a.L, st, wa, mc, ra);
-            }
-            write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
-        }
+        const int b0 = nfull * (NT * kTile) - it.p;
+        if constexpr (CLAMP)
+            TailTiles<ELL, G, NT, MPV, MC, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, mc,
+                                                              binit, blast, ra);
+        else
+            TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(nv, PaddedTiles{row + b0, it.d}, wa, mc, binit,
+                                                             blast, ra);
+        write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
     }
 }
 
@@ -514,18 +444,13 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
     it.d = p->d;
     it.p = p->p;
     it.O = p->O;
-    it.S = p->S;
-    it.rounds = p->rounds;
-    it.lane_off = p->lane_off;
+    it.n_tiles = p->n_tiles;
     it.w_off = p->w_off;
     it.k_off = p->k_off;
     it.cost = p->cost;
-    it.n_long = p->n_long;
-    it.n_short = p->n_short;
-    it.rounds_long = p->rounds_long;
-    it.inv_O = p->inv_O;
     it.n_ch = p->n_ch;
     it.ch_off = p->ch_off;
+    it.inv_O = p->inv_O;
     return it;
 }
 
@@ -544,32 +469,32 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
     }
 }
 
-// Workgroup = (variant, row tile, split); each workgroup stages its row tile
-// in LDS and runs the items of one variant over it.
+// Workgroup = (variant, row group, split); each workgroup stages its row
+// group in LDS and runs the items of one variant over it.
 template <int BLOCK, bool CLAMP, bool MPV, bool MC>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     extern __shared__ float smem[];
     __shared__ int next_item;
     // Workgroup b runs on XCD b % 8.  Every XCD takes its own share of the
-    // row tiles and walks them variant by variant, so all XCDs get the same
+    // row groups and walks them variant by variant, so all XCDs get the same
     // mix of work while the CUs of an XCD run one code variant at a time.
     const int64_t b = blockIdx.x;
     const int xcd = (int)(b % kXcds);
     const int64_t local = b / kXcds;
-    const int64_t per_variant = a.tiles_per_xcd * a.nsplit;
+    const int64_t per_variant = a.groups_per_xcd * a.nsplit;
     const int vi = (int)(local / per_variant);
     const int64_t rest = local % per_variant;
-    const int64_t tile = xcd * a.tiles_per_xcd + rest / a.nsplit;
+    const int64_t group = xcd * a.groups_per_xcd + rest / a.nsplit;
     const int split = (int)(rest % a.nsplit);
     const int variant = a.variants[vi];
     const int beg = as_const(a.split_begin)[variant * a.nsplit + split];
     const int cnt_items = as_const(a.split_begin)[variant * a.nsplit + split + 1] - beg;
-    const int64_t first = tile * a.rows_per_block;
+    const int64_t first = group * a.rows_per_block;
     if (cnt_items == 0 || first >= a.n_rows) return;
     const int nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
     const int64_t grow = a.row0 + first;
 
-    // stage the tile's series (every channel) with their zero margins,
+    // stage the group's series (every channel) with their zero margins,
     // coalesced; channel c of row r at (r*C + c)*row_stride
     for (int rc = 0; rc < nrows * a.C; ++rc) {
         const float *x = a.X + ((grow * a.C) + rc) * (int64_t)a.L;
@@ -579,8 +504,8 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
             dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
         }
     }
-    // zeros after the last row: discarded extra steps may read up to
-    // tail_pad floats past it
+    // zeros after the last row: lanes past the last output of an item read
+    // up to tail_pad floats past it
     for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[nrows * a.C * a.row_stride + e] = 0.0f;
     if (threadIdx.x == 0) next_item = 0;
     __syncthreads();
@@ -697,7 +622,7 @@ struct rocket_plan {
     int device = 0;
     int n_cu = 0;
     bool direct = false;
-    bool clamp = false;      // rows staged with one-zero margins, indices clamped
+    bool clamp = false;      // rows staged with kClampMargin zeros on each side, tap offsets clamped
     bool mpv = false;        // third feature per kernel: mean of positive values
     int32_t C = 1;           // channels per series
     int32_t halo_lo = 0;     // staged layout actually used (floats)
@@ -706,7 +631,6 @@ struct rocket_plan {
     int rows_per_block = 1;  // series staged per workgroup
     int64_t lds_bytes = 0;   // per workgroup: the rows plus the tail pad
     ItemDesc *d_items = nullptr;
-    uint32_t *d_lanes = nullptr;
     float *d_wpk = nullptr;
     float *d_bias = nullptr;
     int32_t *d_kid = nullptr;
@@ -725,7 +649,7 @@ struct rocket_plan {
 };
 
 static void plan_free_device(rocket_plan *p) {
-    void *ptrs[] = {p->d_items, p->d_lanes, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
+    void *ptrs[] = {p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
                     p->d_split_begin, p->d_chan, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
     for (void *q : ptrs)
@@ -764,10 +688,11 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     p->n_cu = prop.multiProcessorCount;
     p->mpv = (flags & ROCKET_PLAN_MPV) != 0;
     p->C = p->host.n_channels;
-    // Staged layout: rows with zero margins wide enough for every padded tap
-    // if that fits one workgroup's LDS, else rows with one zero on each side
-    // and clamped indices, else the direct kernel.  Rows per workgroup: as
-    // many as fit the LDS budget (at least one).
+    // Staged layout: rows with zero margins wide enough for every tap of
+    // every real output if that fits one workgroup's LDS, else rows with
+    // kClampMargin zeros on each side and clamped tap offsets, else the
+    // direct kernel.  Rows per workgroup: as many as fit the LDS budget (at
+    // least one).
     const int64_t limit = (int64_t)prop.sharedMemPerBlock;
     auto layout = [&](int64_t stride, int64_t pad, int *rows) {
         const int64_t row_bytes = stride * p->C * (int64_t)sizeof(float);  // every channel
@@ -783,11 +708,13 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         p->halo_lo = p->host.halo_lo;
         p->row_stride = p->host.row_stride;
         p->tail_pad = p->host.tail_pad;
-    } else if (!p->direct && (lds = layout((int64_t)L + 2, 0, &p->rows_per_block)) <= limit) {
+    } else if (!p->direct &&
+               (lds = layout((int64_t)L + 2 * rocket::kClampMargin, p->host.tail_pad, &p->rows_per_block)) <=
+                   limit) {
         p->clamp = true;
-        p->halo_lo = 1;
-        p->row_stride = L + 2;
-        p->tail_pad = 0;
+        p->halo_lo = rocket::kClampMargin;
+        p->row_stride = L + 2 * rocket::kClampMargin;
+        p->tail_pad = p->host.tail_pad;
     } else {
         p->direct = true;
     }
@@ -803,7 +730,6 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_index, (size_t)K * p->C, &p->d_ci);
     if (!p->direct) {
         if (e == hipSuccess) e = upload(p->host.items, &p->d_items);
-        if (e == hipSuccess) e = upload(p->host.lanes, &p->d_lanes);
         if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
         if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
         if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
@@ -874,9 +800,9 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
     const int64_t row_bytes = (int64_t)p->row_stride * (int64_t)sizeof(float);  // one channel
     const int R = p->rows_per_block;
-    const int64_t tiles = (n + R - 1) / R;
+    const int64_t groups = (n + R - 1) / R;
     int li = 0;
-    while (li + 1 < rocket::kNumSplitLayouts && tiles * rocket::kSplitCounts[li] < target) ++li;
+    while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target) ++li;
     const int nsplit = rocket::kSplitCounts[li];
     FusedArgs a;
     a.X = X;
@@ -887,7 +813,6 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.C = p->C;
     a.chan = p->d_chan;
     a.items = p->d_items;
-    a.lanes = p->d_lanes;
     a.wpk = p->d_wpk;
     a.bias = p->d_bias;
     a.kid = p->d_kid;
@@ -908,9 +833,9 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
         a.row0 = r0;
         a.n_rows = std::min<int64_t>(max_rows, n - r0);
-        const int64_t tiles_now = (a.n_rows + R - 1) / R;
-        a.tiles_per_xcd = (tiles_now + kXcds - 1) / kXcds;
-        const unsigned nb = (unsigned)(kXcds * a.tiles_per_xcd * nsplit * a.n_variants);
+        const int64_t groups_now = (a.n_rows + R - 1) / R;
+        a.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
+        const unsigned nb = (unsigned)(kXcds * a.groups_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)p->lds_bytes;
         const bool big = row_bytes * p->C > kBigLds;
         const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);

@@ -81,7 +81,6 @@ class CPlanTables(ctypes.Structure):
         ("n_items", ctypes.c_int64), ("item_words", ctypes.c_int32), ("n_channels", ctypes.c_int32),
         ("items", ctypes.POINTER(ctypes.c_int32)),
         ("n_chan", ctypes.c_int64), ("chan", ctypes.POINTER(ctypes.c_int32)),
-        ("n_lanes", ctypes.c_int64), ("lanes", ctypes.POINTER(ctypes.c_uint32)),
         ("n_wpk", ctypes.c_int64), ("wpk", ctypes.POINTER(ctypes.c_float)),
         ("n_slots", ctypes.c_int64), ("slot_bias", ctypes.POINTER(ctypes.c_float)),
         ("slot_kernel", ctypes.POINTER(ctypes.c_int32)),
@@ -246,7 +245,6 @@ def plan_tables(kernels: dict, L: int) -> dict:
             items=arr(t.items, t.n_items * t.item_words, (int(t.n_items), int(t.item_words))),
             chan=arr(t.chan, t.n_chan),
             n_channels=t.n_channels,
-            lanes=arr(t.lanes, t.n_lanes),
             wpk=arr(t.wpk, t.n_wpk),
             slot_bias=arr(t.slot_bias, t.n_slots),
             slot_kernel=arr(t.slot_kernel, t.n_slots),

@@ -1,17 +1,20 @@
 """Host logic of the fused kernel, checked on the CPU.
 
-The planner's tables (work items, lane tables, packed weights, item orders)
-are read back through rocket_plan_tables_build and walked here exactly the
-way the GPU kernel walks them: every round runs S steps (the first
-rounds_long rounds) or S-1 steps for all 64 lanes; an active lane takes the
-output positions q0, q0+d, ... and loads the series values at
-halo_lo - p + q + j*d from the zero-margined row; a lane flagged "short"
-discards its last step and an idle lane discards every step (both start
-those accumulations from -inf on the GPU).  The checks: every position a
-lane keeps is a real output, every output of every kernel is kept exactly
-once, every load stays inside the staged row (discarded steps: inside the
-row plus the tail pad), the packed weights are the kernels' own, and an
-fp32 replay of the walk lands inside the oracle's certified bounds.
+The planner's tables (work items, packed weights, item orders) are read back
+through rocket_plan_tables_build and walked here the way the GPU kernel walks
+them: an item's O outputs are computed in ceil(O/64) tiles of 64 consecutive
+positions, lane l of tile k computing output 64k + l; tiles run in blocks of
+NT (8 for 4-kernel items, 4 for 8-kernel items); for tap j, lane l of tile u
+of the block that starts at output t0 reads series index t0 - p + j*d +
+64u + l.  In the padded layout that index is used as is (zero margins of
+halo_lo / halo_hi floats around the series, tail_pad zeros after the last
+row); in the clamped layout the block's offset t0 - p + j*d is clamped into
+[-512, L] first (512 zeros on each side of the series).  Lanes past O start
+from -inf on the GPU and change no feature.  The checks: every output of
+every kernel is computed by exactly one lane, every load stays inside the
+staged memory, every load of a real output reads the zero-padded series
+value, the packed weights are the kernels' own, and an fp32 replay of the
+walk lands inside the oracle's certified bounds.
 """
 import numpy as np
 import pytest
@@ -20,18 +23,16 @@ import paper_2601_17091_amd as rk
 from _util import kernel_set
 
 ELLS = (7, 9, 11)
-POS_MASK = 0x00FFFFFF
-SHORT = 1 << 31
-IDLE = 1 << 30
+TILE = 64
+TILES_PER_BLOCK = {1: 8, 2: 4}
+CLAMP_MARGIN = 512
 
 
 def item_fields(row):
-    (variant, d, p, O, S, rounds, lane_off, w_off, k_off, cost, n_long, n_short,
-     rounds_long, n_ch, ch_off) = (int(v) for v in row[:15])
-    inv_O = row[16:18].astype(np.int32).view(np.float64)[0]
-    return dict(variant=variant, d=d, p=p, O=O, S=S, rounds=rounds, lane_off=lane_off,
-                w_off=w_off, k_off=k_off, cost=cost, n_long=n_long, n_short=n_short,
-                rounds_long=rounds_long, n_ch=n_ch, ch_off=ch_off, inv_O=inv_O)
+    (variant, d, p, O, n_tiles, w_off, k_off, cost, n_ch, ch_off) = (int(v) for v in row[:10])
+    inv_O = row[14:16].astype(np.int32).view(np.float64)[0]
+    return dict(variant=variant, d=d, p=p, O=O, n_tiles=n_tiles, w_off=w_off, k_off=k_off,
+                cost=cost, n_ch=n_ch, ch_off=ch_off, inv_O=inv_O)
 
 
 def kernel_row(kernels, k, c):
@@ -45,24 +46,41 @@ def kernel_row(kernels, k, c):
     return None
 
 
-def walk(tables, kernels, L, X=None):
+def tile_reads(f, ell, L, clamped):
+    """Series index every lane reads, [tile, lane, tap], in the given layout."""
+    G = f["variant"] % 2 + 1
+    NT = TILES_PER_BLOCK[G]
+    nt, d, p = f["n_tiles"], f["d"], f["p"]
+    k = np.arange(nt)
+    t0 = (k // NT) * NT * TILE                      # first output of the tile's block
+    u = k % NT                                      # tile within its block
+    off = t0[:, None] - p + np.arange(ell)[None, :] * d   # [tile, tap] block offset of the tap
+    if clamped:
+        off = np.clip(off, -CLAMP_MARGIN, L)
+    return off[:, None, :] + (u * TILE)[:, None, None] + np.arange(TILE)[None, :, None]
+
+
+def walk(tables, kernels, L, X=None, clamped=False):
     """Replay the fused kernel's schedule; returns per-kernel coverage and,
     if X is given, fp32 features [n, 2K]."""
     K = len(kernels["length"])
     C = int(kernels.get("n_channels", 1))
-    lanes = tables["lanes"].astype(np.int64)
-    halo_lo, stride, pad = tables["halo_lo"], tables["row_stride"], tables["tail_pad"]
+    halo_lo, halo_hi, stride, pad = (tables["halo_lo"], tables["halo_hi"], tables["row_stride"],
+                                     tables["tail_pad"])
+    if clamped:
+        halo_lo, halo_hi, stride = CLAMP_MARGIN, CLAMP_MARGIN, L + 2 * CLAMP_MARGIN
+    assert stride == halo_lo + L + halo_hi and pad >= TILE - 1
     cover = [np.zeros(0, np.int64)] * K
     F = None
     if X is not None:
         n = X.shape[0]
         F = np.full((n, 2 * K), np.nan, dtype=np.float64)
         Xc = X.reshape(n, C, L)
-        rows = np.zeros((n, C, stride), dtype=np.float32)
+        rows = np.zeros((n, C, stride + pad), dtype=np.float32)
         rows[:, :, halo_lo:halo_lo + L] = Xc
     for row in tables["items"]:
         f = item_fields(row)
-        d, p, O, S, ell = f["d"], f["p"], f["O"], f["S"], ELLS[f["variant"] // 2]
+        d, p, O, ell = f["d"], f["p"], f["O"], ELLS[f["variant"] // 2]
         G = f["variant"] % 2 + 1
         nslot = 4 * G
         kid = tables["slot_kernel"][f["k_off"]:f["k_off"] + nslot]
@@ -78,70 +96,46 @@ def walk(tables, kernels, L, X=None):
             if k >= 0:
                 ln = int(kernels["length"][k])
                 for ci, c in enumerate(chans):
-                    row = kernel_row(kernels, k, c)
-                    if row is None:
+                    wrow = kernel_row(kernels, k, c)
+                    if wrow is None:
                         assert np.all(Wslot[ci, s_] == 0)
                     else:
                         used[ci] = True
-                        assert np.array_equal(Wslot[ci, s_, :ln], row[:ln])
+                        assert np.array_equal(Wslot[ci, s_, :ln], wrow[:ln])
                         assert np.all(Wslot[ci, s_, ln:] == 0)
                 assert bias[s_] == np.float32(kernels["bias"][k])
                 assert (int(kernels["dilation"][k]), int(kernels["padding"][k])) == (d, p)
             else:
                 assert np.all(Wslot[:, s_] == 0)
         assert used.all()     # the channel list is exactly the union
-        n_chunks = f["n_long"] + f["n_short"]
-        assert f["rounds"] == -(-n_chunks // 64) and f["rounds_long"] == -(-f["n_long"] // 64)
-        steps = f["rounds_long"] * S + (f["rounds"] - f["rounds_long"]) * (S - 1)
-        assert f["cost"] == steps * ell * G * nch
+        assert f["n_tiles"] == -(-O // TILE)
+        assert f["cost"] == f["n_tiles"] * ell * G * nch
         assert f["inv_O"] == 1.0 / O
-        kept = []
-        ys = [] if X is not None else None
-        for rd in range(f["rounds"]):
-            length = S if rd < f["rounds_long"] else S - 1
-            assert length >= 1
-            e = lanes[f["lane_off"] + 64 * rd:f["lane_off"] + 64 * rd + 64]
-            q0 = e & POS_MASK
-            short = (e & SHORT) != 0
-            idle = (e & IDLE) != 0
-            # flags: short chunks only in rounds of S steps, idle lanes only
-            # past the last chunk
-            assert not np.any(short & idle)
-            if length == S - 1:
-                assert not short.any()
-            assert np.array_equal(idle, np.arange(64) + 64 * rd >= n_chunks)
-            # every load of every lane and step, discarded ones included
-            m = np.arange(length + ell - 1)
-            idx = halo_lo - p + q0[:, None] + m[None, :] * d
-            assert idx.min() >= 0 and idx.max() < stride + pad, (d, p, O, S)
-            # steps each lane keeps
-            keep_steps = np.where(idle, 0, np.where(short, length - 1, length))
-            for lane in range(64):
-                ks_ = keep_steps[lane]
-                if ks_ == 0:
-                    continue
-                q = q0[lane] + np.arange(ks_) * d
-                assert q.min() >= 0 and q.max() < O                  # real outputs only
-                last_idx = halo_lo - p + q.max() + (ell - 1) * d
-                assert last_idx < stride                              # kept steps read the row
-                kept.append(q)
-            if X is not None:
-                qa = np.concatenate([q0[l] + np.arange(keep_steps[l]) * d for l in range(64)])
-                tap_idx = halo_lo - p + qa[:, None] + np.arange(ell)[None, :] * d
-                acc = np.broadcast_to(bias.astype(np.float32), (n, qa.shape[0], nslot)).copy()
-                # channel by channel, tap by tap, in the kernel's order
-                for ci, c in enumerate(chans):
-                    xv = rows[:, c][:, tap_idx]                       # [n, output, tap]
-                    for j in range(ell):
-                        acc = (acc + xv[..., j, None] * Wslot[ci][None, None, :, j]).astype(np.float32)
-                ys.append(acc)
-        allq = np.concatenate(kept)
+        # outputs: lane l of tile k computes 64k + l; the real ones are < O
+        t = (np.arange(f["n_tiles"])[:, None] * TILE + np.arange(TILE)[None, :])   # [tile, lane]
+        real = t < O
         for k in kid[kid >= 0]:
-            cover[k] = np.bincount(allq, minlength=O)
+            cover[k] = np.bincount(t[real], minlength=O)
+        idx = tile_reads(f, ell, L, clamped)                                          # [tile, lane, tap]
+        # every load inside the staged memory (lanes past O of the last row:
+        # inside the tail pad)
+        assert (halo_lo + idx).min() >= 0 and (halo_lo + idx).max() < stride + pad, (d, p, O)
+        # loads of real outputs inside the row, at the zero-padded series value
+        true_idx = t[:, :, None] - p + np.arange(ell)[None, None, :] * d
+        ri, ti = idx[real], true_idx[real]
+        assert (halo_lo + ri).max() < stride
+        inside = (ti >= 0) & (ti < L)
+        assert np.array_equal(ri[inside], ti[inside])
+        assert np.all((ri[~inside] < 0) | (ri[~inside] >= L))
         if X is not None:
-            y = np.concatenate(ys, axis=1)                               # [n, outputs, slot]
-            cnt = (y > 0).sum(axis=1)
-            mxv = y.max(axis=1)
+            acc = np.broadcast_to(bias.astype(np.float32), (n, O, nslot)).copy()
+            # channel by channel, tap by tap, in the kernel's order
+            for ci, c in enumerate(chans):
+                xv = rows[:, c][:, halo_lo + ri.reshape(O, ell)]                  # [n, output, tap]
+                for j in range(ell):
+                    acc = (acc + xv[..., j, None] * Wslot[ci][None, None, :, j]).astype(np.float32)
+            cnt = (acc > 0).sum(axis=1)
+            mxv = acc.max(axis=1)
             for s_, k in enumerate(kid):
                 if k >= 0:
                     F[:, 2 * k] = cnt[:, s_] / O
@@ -168,15 +162,16 @@ def check_tables(kernels, L, X=None, oracle=None):
     # every kernel sits in exactly one slot
     kid = t["slot_kernel"]
     assert np.array_equal(np.sort(kid[kid >= 0]), np.arange(K))
-    cover, F = walk(t, kernels, L, X)
-    for k in range(K):
-        O = L + 2 * int(kernels["padding"][k]) - (int(kernels["length"][k]) - 1) * int(kernels["dilation"][k])
-        assert cover[k].shape[0] == O and np.all(cover[k] == 1), k
-    if X is not None:
-        r = oracle.transform(X, kernels)
-        cnt = np.rint(F[:, 0::2] * r["O"][None, :]).astype(np.int64)
-        assert np.all(r["cnt_lo"] <= cnt) and np.all(cnt <= r["cnt_hi"])
-        assert np.all(np.abs(F[:, 1::2] - r["F"][:, 1::2]) <= r["beta"])
+    r = oracle.transform(X, kernels) if X is not None else None
+    for clamped in (False, True):
+        cover, F = walk(t, kernels, L, X, clamped)
+        for k in range(K):
+            O = L + 2 * int(kernels["padding"][k]) - (int(kernels["length"][k]) - 1) * int(kernels["dilation"][k])
+            assert cover[k].shape[0] == O and np.all(cover[k] == 1), k
+        if X is not None:
+            cnt = np.rint(F[:, 0::2] * r["O"][None, :]).astype(np.int64)
+            assert np.all(r["cnt_lo"] <= cnt) and np.all(cnt <= r["cnt_hi"])
+            assert np.all(np.abs(F[:, 1::2] - r["F"][:, 1::2]) <= r["beta"])
     return t
 
 
@@ -221,17 +216,15 @@ def test_item_cost_and_groups():
     items = t["items"]
     G = items[:, 0] % 2 + 1
     ell = np.array(ELLS)[items[:, 0] // 2]
-    S, rounds, rounds_long = items[:, 4], items[:, 5], items[:, 12]
-    steps = rounds_long * S + (rounds - rounds_long) * (S - 1)
-    np.testing.assert_array_equal(items[:, 9], steps * ell * G * items[:, 13])
+    O, n_tiles = items[:, 3], items[:, 4]
+    np.testing.assert_array_equal(n_tiles, (O + TILE - 1) // TILE)
+    np.testing.assert_array_equal(items[:, 7], n_tiles * ell * G * items[:, 8])
     # a bucket is split into groups of 8 with at most one smaller group
     assert (G == 2).sum() > (G == 1).sum()
-    # small dilations need one round of long chunks per series
-    d = items[:, 1]
-    assert np.all(rounds[d == 1] == 1)
-    # MFMA work issued stays within 20% of the nominal taps x outputs
+    # MFMA work issued (256 FMA per instruction: 4 slots x 64 lanes) stays
+    # within 15% of the nominal taps x outputs
     nominal = (ks["length"] * (1000 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
-    assert items[:, 9].sum() * 256 < 1.2 * nominal
+    assert items[:, 7].sum() * 256 < 1.15 * nominal
 
 
 def test_ppv_through_double_reciprocal():
