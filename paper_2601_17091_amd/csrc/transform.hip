@@ -10,8 +10,9 @@
 //      their outputs' positions and the series values under every tap;
 //   3. outputs are computed in tiles of 64 consecutive positions, lane l
 //      taking position 64k + l of tile k; for tap j the 64 lanes read 64
-//      consecutive series values (index 64k - p + j*d + l), so a tile's
-//      loads are conflict-free and share one address register per tap;
+//      consecutive series values (index 64k - p + j*d + l): one
+//      conflict-free ds_read_addtid_b32 per tile and tap, addressed by a
+//      scalar register;
 //   4. the dot products of a tile are an outer-product contraction over the
 //      taps: v_mfma_f32_4x4x1_16b_f32 multiplies the 4 kernels' weights (A,
 //      one kernel per block row) by the 64 lanes' series values (B), one tap
@@ -42,6 +43,77 @@ using ConstPtr = const __attribute__((address_space(4))) T *;
 template <typename T>
 __device__ __forceinline__ ConstPtr<T> as_const(const T *p) {
     return (ConstPtr<T>)(p);
+}
+
+// LDS byte address of a pointer into the kernel's shared memory.
+typedef __attribute__((address_space(3))) const float lds_cfloat;
+__device__ __forceinline__ uint32_t lds_addr(const float *p) {
+    return (uint32_t)(__UINTPTR_TYPE__)(lds_cfloat *)p;
+}
+
+// The series values of up to 4 tiles under one tap: NT reads of 64
+// consecutive floats, 256 bytes apart, the first at LDS byte address m
+// (wavefront-uniform).  ds_read_addtid_b32 reads the dword at
+// M0 + offset + 4 * lane, so the address comes from a scalar register and no
+// vector instruction computes it.  M0 is written right before the reads
+// (one wait state between the write and its first use) and is not used by
+// compiled code in these kernels.  The reads complete before the asm block
+// ends (lgkmcnt(0)), so the outputs are ready when the compiler sees them.
+template <int NT>
+__device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]);
+template <>
+__device__ __forceinline__ void lds_tiles<1>(uint32_t m, float (&xv)[1]) {
+    asm volatile(
+        "s_mov_b32 m0, %1\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=v"(xv[0])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles<2>(uint32_t m, float (&xv)[2]) {
+    asm volatile(
+        "s_mov_b32 m0, %2\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(xv[0]), "=&v"(xv[1])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles<3>(uint32_t m, float (&xv)[3]) {
+    asm volatile(
+        "s_mov_b32 m0, %3\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles<4>(uint32_t m, float (&xv)[4]) {
+    asm volatile(
+        "s_mov_b32 m0, %4\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\tds_read_addtid_b32 %3 offset:768\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3])
+        : "s"(m)
+        : "memory");
+}
+// 5..8 tiles: the first 4, then the rest from 1,024 bytes further
+template <int NT>
+__device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]) {
+    static_assert(NT > 4 && NT <= 8, "1 to 8 tiles per block");
+    float a[4], b[NT - 4];
+    lds_tiles<4>(m, a);
+    lds_tiles<NT - 4>(m + 1024u, b);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) xv[u] = a[u];
+#pragma unroll
+    for (int u = 4; u < NT; ++u) xv[u] = b[u - 4];
 }
 
 namespace {
@@ -86,39 +158,42 @@ constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
 
-// Where a block's series values come from.  tap(j) is the lane's LDS
-// pointer for tap j of the block's first tile; tile u of the block reads
-// 64*u floats further.  channel(off) moves to another channel's row.
+// Where a block's series values come from.  m0(j) is the LDS byte address
+// of lane 0's value under tap j in the block's first tile; lane l reads 4*l
+// bytes further and tile u of the block 256*u bytes further.  channel(off)
+// moves to another channel's row (off floats further).
 //   PaddedTiles:  the row sits in LDS with zero margins wide enough for
 //                 every tap of every real output (and the tail pad after
-//                 the last row for the lanes past O), so tap j is at
-//                 x + j*d.
+//                 the last row for the lanes past O), so tap j is d floats
+//                 after tap j-1.
 //   ClampedTiles: the row sits in LDS with kClampMargin zeros on each side
 //                 (long series, whose full margins would not fit).  The
-//                 series index of lane 0 of tap j is clamped into
+//                 series index of lane 0 under tap j is clamped into
 //                 [-kClampMargin, L] on the scalar unit: a block whose
 //                 positions all lie left (right) of the series then reads
 //                 zeros from the left (right) margin, and a block that
 //                 overlaps the series is not moved, so every read stays in
 //                 the margins and yields the zero-padded value.
 struct PaddedTiles {
-    const float *x;  // the lane's value at series index t0 - p (t0: first output of the block)
+    uint32_t base;  // LDS byte address of lane 0's value under tap 0
     int d;
-    __device__ __forceinline__ const float *tap(int j) const { return x + j * d; }
-    __device__ __forceinline__ PaddedTiles channel(int off) const { return PaddedTiles{x + off, d}; }
+    __device__ __forceinline__ uint32_t m0(int j) const { return base + 4u * (uint32_t)(j * d); }
+    __device__ __forceinline__ PaddedTiles channel(int off) const {
+        return PaddedTiles{base + 4u * (uint32_t)off, d};
+    }
 };
 
 struct ClampedTiles {
-    const float *row;  // series index 0 of the row, plus the lane number
-    int b0;            // series index under tap 0 of lane 0 (wavefront-uniform)
+    uint32_t row;  // LDS byte address of series index 0
+    int b0;        // series index under tap 0 of lane 0
     int d;
     int L;
-    __device__ __forceinline__ const float *tap(int j) const {
+    __device__ __forceinline__ uint32_t m0(int j) const {
         const int b = min(max(b0 + j * d, -rocket::kClampMargin), L);
-        return row + b;
+        return row + 4u * (uint32_t)b;
     }
     __device__ __forceinline__ ClampedTiles channel(int off) const {
-        return ClampedTiles{row + off, b0, d, L};
+        return ClampedTiles{row + 4u * (uint32_t)off, b0, d, L};
     }
 };
 
@@ -155,10 +230,8 @@ __device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][E
                                           v4f (&acc)[NT][G]) {
 #pragma unroll
     for (int j = 0; j < ELL; ++j) {
-        const float *pj = src.tap(j);
         float xv[NT];
-#pragma unroll
-        for (int u = 0; u < NT; ++u) xv[u] = pj[u * kTile];
+        lds_tiles<NT>(src.m0(j), xv);
 #pragma unroll
         for (int u = 0; u < NT; ++u)
 #pragma unroll
@@ -415,7 +488,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
     for (int r = 0; r < nrows; ++r) {
         RowAcc<G> ra;
         init_row<G, MPV>(ra);
-        const float *row = rows0 + r * row_pitch + lane;
+        const uint32_t row = lds_addr(rows0 + r * row_pitch);  // series index 0
         // block b starts at output b*NT*64; its lane 0 reads series index
         // b*NT*64 - p under tap 0 (a wavefront-uniform offset)
         for (int blk = 0; blk < nfull; ++blk) {
@@ -424,16 +497,16 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
                 tile_block<ELL, G, NT, false, MPV, MC>(ClampedTiles{row, b0, it.d, a.L}, wa, mc, binit,
                                                        blast, ra);
             else
-                tile_block<ELL, G, NT, false, MPV, MC>(PaddedTiles{row + b0, it.d}, wa, mc, binit, blast,
-                                                       ra);
+                tile_block<ELL, G, NT, false, MPV, MC>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa,
+                                                       mc, binit, blast, ra);
         }
         const int b0 = nfull * (NT * kTile) - it.p;
         if constexpr (CLAMP)
             TailTiles<ELL, G, NT, MPV, MC, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, mc,
                                                               binit, blast, ra);
         else
-            TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(nv, PaddedTiles{row + b0, it.d}, wa, mc, binit,
-                                                             blast, ra);
+            TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(
+                nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra);
         write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
     }
 }
