@@ -2,11 +2,13 @@
 // padding), work items, packed weights and item orders for the fused MFMA
 // kernel.  Pure host code; no HIP calls.
 #include <algorithm>
+#include <array>
 #include <climits>
 #include <cstring>
 #include <map>
 #include <new>
 #include <tuple>
+#include <utility>
 
 #include "rocket_internal.h"
 
@@ -98,22 +100,88 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             P.row_stride = (int32_t)stride;
         }
 
+        // Frame lists: the kernels one run of items covers, each with the
+        // frame tap its first weight sits on.  A bucket is one list; but
+        // centred kernels (padding (len-1)*d/2) of every length at one
+        // dilation compute the same O = L outputs around the same centre, so
+        // a shorter one also runs in a longer frame with zero weights on the
+        // outer taps.  The empty slots of a bucket's last 4-slot group are
+        // filled that way when it saves a group of a shorter frame
+        // (univariate sets; every group costs frame taps x tiles).
+        struct Frame {
+            int eidx;   // frame length class
+            int32_t d, p;
+            std::vector<std::pair<int32_t, int32_t>> ks;  // (kernel, first frame tap)
+        };
+        std::vector<Frame> frames;
+        std::map<int32_t, std::array<std::vector<int32_t>, kNumEll>> centred;  // by dilation
         for (auto &kv : buckets) {
             const int32_t len = std::get<0>(kv.first), d = std::get<1>(kv.first),
                           p = std::get<2>(kv.first);
-            std::vector<int32_t> &ids = kv.second;
+            const int e = ell_index_for(len);
+            if (C == 1 && len == kEllValues[e] && (int64_t)p * 2 == (int64_t)(len - 1) * d) {
+                centred[d][e] = kv.second;
+                continue;
+            }
+            Frame f{e, d, p, {}};
+            for (int32_t i : kv.second) f.ks.emplace_back(i, 0);
+            frames.push_back(std::move(f));
+        }
+        for (auto &kv : centred) {
+            const int32_t d = kv.first;
+            auto &ids = kv.second;
+            const int64_t n7 = (int64_t)ids[0].size(), n9 = (int64_t)ids[1].size(),
+                          n11 = (int64_t)ids[2].size();
+            auto groups = [](int64_t n) { return ceil_div(n, kSlotsPerGroup); };
+            auto freeslots = [](int64_t n) { return (kSlotsPerGroup - n % kSlotsPerGroup) % kSlotsPerGroup; };
+            // a9 9s and a7 7s ride in the last 11-group, b7 7s in the last 9-group
+            int64_t best = -1, ba9 = 0, ba7 = 0, bb7 = 0;
+            const int64_t f11 = n11 > 0 ? freeslots(n11) : 0;
+            for (int64_t a9 = 0; a9 <= std::min(n9, f11); ++a9)
+                for (int64_t a7 = 0; a7 <= std::min(n7, f11 - a9); ++a7) {
+                    const int64_t m9 = n9 - a9;
+                    const int64_t f9 = m9 > 0 ? freeslots(m9) : 0;
+                    for (int64_t b7 = 0; b7 <= std::min(n7 - a7, f9); ++b7) {
+                        const int64_t cost = 11 * groups(n11 + a9 + a7) + 9 * groups(m9 + b7) +
+                                             7 * groups(n7 - a7 - b7);
+                        if (best < 0 || cost < best) {
+                            best = cost;
+                            ba9 = a9;
+                            ba7 = a7;
+                            bb7 = b7;
+                        }
+                    }
+                }
+            // the fillers are the last kernels of their own lists
+            Frame f11l{2, d, 5 * d, {}}, f9l{1, d, 4 * d, {}}, f7l{0, d, 3 * d, {}};
+            for (int32_t i : ids[2]) f11l.ks.emplace_back(i, 0);
+            for (int64_t q = n9 - ba9; q < n9; ++q) f11l.ks.emplace_back(ids[1][q], 1);
+            for (int64_t q = n7 - ba7; q < n7; ++q) f11l.ks.emplace_back(ids[0][q], 2);
+            for (int64_t q = 0; q < n9 - ba9; ++q) f9l.ks.emplace_back(ids[1][q], 0);
+            for (int64_t q = n7 - ba7 - bb7; q < n7 - ba7; ++q) f9l.ks.emplace_back(ids[0][q], 1);
+            for (int64_t q = 0; q < n7 - ba7 - bb7; ++q) f7l.ks.emplace_back(ids[0][q], 0);
+            for (Frame *f : {&f11l, &f9l, &f7l})
+                if (!f->ks.empty()) frames.push_back(std::move(*f));
+        }
+
+        for (Frame &fr : frames) {
+            const int32_t d = fr.d, p = fr.p;
+            auto &ks = fr.ks;
             // multivariate: kernels with similar channel sets next to each
             // other, so that an item's channel union stays small
             if (C > 1)
-                std::stable_sort(ids.begin(), ids.end(),
-                                 [&](int32_t a, int32_t b) { return mask_of(a) < mask_of(b); });
-            const int eidx = ell_index_for(len);
+                std::stable_sort(ks.begin(), ks.end(), [&](const std::pair<int32_t, int32_t> &a,
+                                                           const std::pair<int32_t, int32_t> &b) {
+                    return mask_of(a.first) < mask_of(b.first);
+                });
+            const int eidx = fr.eidx;
             const int ell = kEllValues[eidx];
-            const int64_t O = output_length(L, len, d, p);
+            // every kernel of a frame list has these outputs
+            const int64_t O = output_length(L, k->length[ks[0].first], d, k->padding[ks[0].first]);
             const int64_t n_tiles = ceil_div(O, kTile);
             size_t pos = 0;
-            while (pos < ids.size()) {
-                const size_t rem = ids.size() - pos;
+            while (pos < ks.size()) {
+                const size_t rem = ks.size() - pos;
                 const int G = rem > 4 ? 2 : 1;
                 const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
                 ItemDesc it;
@@ -126,7 +194,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 it.w_off = (int32_t)P.wpk.size();
                 it.k_off = (int32_t)P.kid.size();
                 uint64_t umask = 0;
-                for (size_t s = 0; s < take; ++s) umask |= mask_of(ids[pos + s]);
+                for (size_t s = 0; s < take; ++s) umask |= mask_of(ks[pos + s].first);
                 it.n_ch = 0;
                 it.ch_off = (int32_t)P.chan.size();
                 for (int32_t c = 0; c < C; ++c)
@@ -140,7 +208,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 it.inv_O = 1.0 / (double)O;
                 // A-operand weights: [channel][g][j][slot i]; zeros for empty
                 // slots, for channels a slot's kernel does not read and for
-                // taps past the kernel's own length
+                // frame taps outside the kernel's own taps
                 for (int32_t ci = 0; ci < it.n_ch; ++ci) {
                     const int32_t c = P.chan[it.ch_off + ci];
                     for (int g = 0; g < G; ++g)
@@ -148,17 +216,18 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                             for (int i = 0; i < 4; ++i) {
                                 const size_t s = (size_t)(4 * g + i);
                                 float w = 0.0f;
-                                if (s < take && j < len) {
-                                    const float *row = row_of(ids[pos + s], c);
-                                    if (row) w = row[j];
+                                if (s < take) {
+                                    const int32_t kk = ks[pos + s].first, off = ks[pos + s].second;
+                                    const float *row = row_of(kk, c);
+                                    if (row && j >= off && j < off + k->length[kk]) w = row[j - off];
                                 }
                                 P.wpk.push_back(w);
                             }
                 }
                 for (int s = 0; s < 4 * G; ++s) {
                     if ((size_t)s < take) {
-                        P.kid.push_back(ids[pos + s]);
-                        P.bias.push_back(k->bias[ids[pos + s]]);
+                        P.kid.push_back(ks[pos + s].first);
+                        P.bias.push_back(k->bias[ks[pos + s].first]);
                     } else {
                         P.kid.push_back(-1);
                         P.bias.push_back(0.0f);
