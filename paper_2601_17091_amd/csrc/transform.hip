@@ -404,8 +404,8 @@ __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 // scalar), then per kernel {PPV, MAX} (or {PPV, MAX, MPV}), written by lanes
 // 0, 16, 32 and 48.
 template <int G, bool MPV>
-__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int32_t *kid_row,
-                                          double inv_O, int lane, float *Frow) {
+__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&okid)[G], double inv_O,
+                                          int lane, float *Frow) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const float m = reduce4<OpMax>(ra.mx[g]);
@@ -421,8 +421,7 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int32_t *ki
         c = lane >= 16 ? c2 : c;
         c = lane >= 32 ? c1 : c;
         c = lane >= 48 ? c3 : c;
-        const bool writer = (lane & 15) == 0;
-        const int ok = writer ? kid_row[4 * g + slot_of_row(lane >> 4)] : -1;
+        const int ok = okid[g];
         if (ok >= 0) {
             // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
             // quotient is never a float midpoint and lies at least 2^-49
@@ -477,13 +476,22 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const float b = as_const(a.bias)[it.k_off + 4 * g + v];
-            binit[g][v] = b;
-            blast[g][v] = lane < rem ? b : -INFINITY;
+            // copied into a vector register once per item (an opaque copy,
+            // so the compiler keeps it there instead of copying the scalar
+            // bias again before every block)
+            float bv;
+            asm volatile("v_mov_b32 %0, %1" : "=v"(bv) : "s"(b));
+            binit[g][v] = bv;
+            blast[g][v] = lane < rem ? bv : -INFINITY;
         }
     const int nfull = (it.n_tiles - 1) / NT;  // full blocks before the last block
     const int nv = it.n_tiles - nfull * NT;   // tiles in the last block, 1..NT
-    // after the reduction, lane 16q writes slot slot_of_row(q) of each group
-    const int32_t *kid_row = a.kid + it.k_off;
+    // after the reduction, lane 16q writes slot slot_of_row(q) of each group:
+    // the kernel ids it writes (-1: not a writer, or an empty slot)
+    int okid[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        okid[g] = (lane & 15) == 0 ? a.kid[it.k_off + 4 * g + slot_of_row(lane >> 4)] : -1;
     const int64_t f_stride = (int64_t)a.nf * a.K;
     for (int r = 0; r < nrows; ++r) {
         RowAcc<G> ra;
@@ -507,7 +515,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         else
             TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(
                 nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra);
-        write_row<G, MPV>(ra, kid_row, it.inv_O, lane, F0 + r * f_stride);
+        write_row<G, MPV>(ra, okid, it.inv_O, lane, F0 + r * f_stride);
     }
 }
 
