@@ -39,6 +39,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "rocket_oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "minirocket_oracle.c")]
 _LIB_PATH = os.path.join(_HERE, "librocket_oracle.so")
 
 MAX_LEN = 11  # weights row stride used by the kernel arrays (longest kernel)
@@ -49,11 +50,14 @@ ORACLE_ERR_LENGTH = -2
 
 
 def build(force: bool = False) -> str:
-    """Compile rocket_oracle.c with gcc (fp64, no fast-math, no FMA contraction)."""
-    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+    """Compile rocket_oracle.c and minirocket_oracle.c with gcc (fp64, no
+    fast-math, no FMA contraction) into one library."""
+    stale = not os.path.exists(_LIB_PATH) or any(
+        os.path.getmtime(_LIB_PATH) < os.path.getmtime(src) for src in _SRCS)
+    if force or stale:
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
         cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
-               "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"]
+               "-fno-fast-math", "-Wall", "-o", tmp] + _SRCS + ["-lm"]
         subprocess.check_call(cmd)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
