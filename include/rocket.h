@@ -237,8 +237,11 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *                (chosen when the full zero margins of the padded kernels
  *                would not fit in LDS, or forced by ROCKET_PLAN_CLAMPED),
  *                else 0
- *   features_per_kernel  2 (PPV, MAX) or 3 (PPV, MAX, MPV)
+ *   features_per_kernel  2 (PPV, MAX) or 3 (PPV, MAX, MPV); 0 for a
+ *                MINIROCKET plan
  *   rows_per_block       series staged per workgroup (0 for the direct kernel)
+ *   n_features   columns of F
+ *   minirocket   1 for a MINIROCKET plan, else 0
  */
 typedef struct {
     int64_t n_items;
@@ -249,6 +252,9 @@ typedef struct {
     int32_t clamped;
     int32_t features_per_kernel;
     int32_t rows_per_block;
+    int64_t n_features;
+    int32_t minirocket;
+    int32_t reserved;
 } rocket_plan_facts;
 
 /* Fill *out with the plan's facts.  Errors: ROCKET_ERR_INVALID_ARG if p or
@@ -315,6 +321,84 @@ typedef struct {
 
 rocket_status rocket_plan_tables_build(const rocket_kernels *k, int32_t L, rocket_plan_tables *out);
 void rocket_plan_tables_free(rocket_plan_tables *t);
+
+/*
+ * MINIROCKET (Dempster, Schmidt and Webb, KDD 2021), the ROCKET variant the
+ * CUROCKET paper (Sec. 5) names as one its principle carries over to:
+ *   - 84 fixed kernels of 9 taps, one per choice of 3 of the 9 taps
+ *     (choices in lexicographic order), weight 2 on the chosen taps and -1
+ *     on the other six;
+ *   - a fitted list of dilations d_i (ascending) and, per dilation, a number
+ *     nf_i of features per kernel;
+ *   - pair (dilation index i, kernel k) is padded (p = 4 d_i, O = L outputs)
+ *     when i + k is even, else unpadded (p = 0, O = L - 8 d_i); its dot
+ *     products are C_t = sum_j w_k[j] * xz[t - p + j d_i];
+ *   - the pair has nf_i fitted biases b; each gives one feature, the
+ *     proportion of positive values of C_t - b:
+ *         PPV = |{t : C_t > b}| / O   (computed as (float)count / (float)O);
+ *   - feature order: dilation index, then kernel, then bias.
+ * Parameters live in HOST memory:
+ *   input_length           L the parameters were fitted for
+ *   n_dilations            number of dilations (>= 1)
+ *   n_features             84 * sum(features_per_dilation)
+ *   dilations[i]           ascending, >= 1, with L - 8 d_i >= 1
+ *   features_per_dilation[i]  >= 0
+ *   biases[f]              fp32, feature order
+ */
+typedef struct {
+    int32_t input_length;
+    int32_t n_dilations;
+    int32_t n_features;
+    int32_t *dilations;
+    int32_t *features_per_dilation;
+    float *biases;
+} rocket_minirocket_params;
+
+/*
+ * Fit MINIROCKET to a training set X_train [n_train, L] (fp32, HOST memory,
+ * row-major), L >= 9, for num_features requested features (>= 84; the fit
+ * keeps 84 * floor(num_features / 84)):
+ *   - dilations: the per-kernel feature count F = num_features / 84 is
+ *     spread over T = min(F, 32) grid points floor(2^e), e evenly spaced on
+ *     [0, log2((L-1)/8)] (e_0 = 0, e_{T-1} = the end point); equal values
+ *     merge, their counts are scaled by F / T and truncated, and what is left
+ *     of F is dealt one by one from the smallest dilation;
+ *   - biases: pair (i, k) draws one training series e = (n_train * (v >> 11))
+ *     >> 53, v = element i*84 + k of the SplitMix64 sequence started at
+ *     `seed`; its padded dot products C_t, t = 0..L-1 (summed in fp64, tap by
+ *     tap) are sorted, and the pair's biases are the quantiles at the
+ *     positions q_m = frac(m * golden ratio) (m = 1, 2, ... over the whole
+ *     feature list, rounded to fp32), by linear interpolation between order
+ *     statistics, rounded to fp32.
+ * Host only; never touches a GPU.
+ * out: library-owned arrays; release with rocket_minirocket_free.  On error
+ *      *out is zeroed.
+ * Errors: ROCKET_ERR_INVALID_ARG (X_train or out NULL, n_train < 1, L < 9,
+ *         num_features < 84); ROCKET_ERR_OOM.
+ */
+rocket_status rocket_minirocket_fit(const float *X_train, int64_t n_train, int32_t L,
+                                    int32_t num_features, uint64_t seed,
+                                    rocket_minirocket_params *out);
+
+/* Release arrays allocated by rocket_minirocket_fit and zero *p.  NULL-safe
+ * and idempotent.  Do not call on caller-built parameters. */
+void rocket_minirocket_free(rocket_minirocket_params *p);
+
+/*
+ * Plan of the MINIROCKET transform for series of length m->input_length on
+ * the current HIP device.  rocket_transform_plan and rocket_transform_host
+ * with this plan write F [n, n_features] (PPV only, feature order above).
+ * The plan groups the 4 kernels of a work item by (dilation, padding) and
+ * computes each pair's dot products once for all of its biases.
+ * flags: ROCKET_PLAN_DEFAULT or ROCKET_PLAN_CLAMPED (the long-series row
+ *        layout, same results); anything else is ROCKET_ERR_INVALID_ARG.
+ * Errors: ROCKET_ERR_INVALID_ARG (null pointers, a field outside the ranges
+ *         above, n_features != 84 * sum(features_per_dilation));
+ *         ROCKET_ERR_LENGTH (L - 8 d_i < 1 for some i, or L >= 2^24);
+ *         ROCKET_ERR_OOM; ROCKET_ERR_HIP.  On error *out is NULL.
+ */
+rocket_status rocket_minirocket_plan_create(const rocket_minirocket_params *m, uint32_t flags,
+                                            rocket_plan **out);
 
 /* Static, human-readable name of a status code ("unknown status" otherwise). */
 const char *rocket_status_string(rocket_status s);

@@ -4,8 +4,10 @@ Python-side entry points (argument marshalling over ctypes):
     generate_kernels(seed, n_kernels, input_length) -> dict of numpy arrays
     Plan(kernels, L)  .transform(X) / .transform_into(X, F) / .info()
     transform(X, kernels)  one-shot
+    minirocket_fit(X_train, num_features, seed) -> MINIROCKET parameters
+    MiniRocketPlan(params)  .transform(X): PPV features [n, n_features]
 The seeded synthetic series live in ``paper_2601_17091_amd.workloads``.
 """
-from .rocket import (EXPORTED, Plan, RocketError, generate_kernels, generate_kernels_multi, library,  # noqa: F401
-                     status_string,
-                     plan_tables, transform, transform_batched)
+from .rocket import (EXPORTED, MiniRocketPlan, Plan, RocketError, generate_kernels,  # noqa: F401
+                     generate_kernels_multi, library, minirocket_fit, plan_tables, status_string,
+                     transform, transform_batched)

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "librocket.so")
-SOURCES = ["transform.hip", "plan.cpp", "generate.cpp"]
+SOURCES = ["transform.hip", "plan.cpp", "generate.cpp", "minirocket.cpp"]
 ARCH = "gfx950"
 
 

@@ -32,6 +32,10 @@ double unit_open_closed(uint64_t v) { return (double)((v >> 11) + 1) * 0x1.0p-53
 
 }  // namespace
 
+uint64_t rocket::splitmix64_at(uint64_t seed, uint64_t index) {
+    return mix64(seed + (index + 1) * kGolden);
+}
+
 extern "C" rocket_status rocket_generate_kernels(uint64_t seed, int32_t n_kernels,
                                                  int32_t input_length, rocket_kernels *out) {
     if (!out) return ROCKET_ERR_INVALID_ARG;

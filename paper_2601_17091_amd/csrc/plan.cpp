@@ -51,6 +51,36 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+void build_item_orders(HostPlan &P) {
+    // per variant, largest cost first (longest-processing-time first), dealt
+    // to splits greedily by accumulated cost
+    std::vector<int32_t> by_cost(P.items.size());
+    for (size_t i = 0; i < by_cost.size(); ++i) by_cost[i] = (int32_t)i;
+    std::stable_sort(by_cost.begin(), by_cost.end(),
+                     [&](int32_t a, int32_t b) { return P.items[a].cost > P.items[b].cost; });
+    for (int li = 0; li < kNumSplitLayouts; ++li) {
+        const int ns = kSplitCounts[li];
+        P.layout_off.push_back((int32_t)P.split_begin.size());
+        for (int v = 0; v < kNumVariants; ++v) {
+            std::vector<std::vector<int32_t>> lists(ns);
+            std::vector<int64_t> load(ns, 0);
+            for (int32_t it : by_cost) {
+                if (P.items[it].variant != v) continue;
+                int best = 0;
+                for (int sp = 1; sp < ns; ++sp)
+                    if (load[sp] < load[best]) best = sp;
+                lists[best].push_back(it);
+                load[best] += P.items[it].cost;
+            }
+            for (int sp = 0; sp < ns; ++sp) {
+                P.split_begin.push_back((int32_t)P.order.size());
+                P.order.insert(P.order.end(), lists[sp].begin(), lists[sp].end());
+            }
+        }
+        P.split_begin.push_back((int32_t)P.order.size());
+    }
+}
+
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
     try {
         HostPlan P;
@@ -241,34 +271,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
 
         P.tail_pad = kTile;
 
-        // item orders: per variant, largest cost first (longest-processing-
-        // time first), dealt to splits greedily by accumulated cost
-        std::vector<int32_t> by_cost(P.items.size());
-        for (size_t i = 0; i < by_cost.size(); ++i) by_cost[i] = (int32_t)i;
-        std::stable_sort(by_cost.begin(), by_cost.end(), [&](int32_t a, int32_t b) {
-            return P.items[a].cost > P.items[b].cost;
-        });
-        for (int li = 0; li < kNumSplitLayouts; ++li) {
-            const int ns = kSplitCounts[li];
-            P.layout_off.push_back((int32_t)P.split_begin.size());
-            for (int v = 0; v < kNumVariants; ++v) {
-                std::vector<std::vector<int32_t>> lists(ns);
-                std::vector<int64_t> load(ns, 0);
-                for (int32_t it : by_cost) {
-                    if (P.items[it].variant != v) continue;
-                    int best = 0;
-                    for (int sp = 1; sp < ns; ++sp)
-                        if (load[sp] < load[best]) best = sp;
-                    lists[best].push_back(it);
-                    load[best] += P.items[it].cost;
-                }
-                for (int sp = 0; sp < ns; ++sp) {
-                    P.split_begin.push_back((int32_t)P.order.size());
-                    P.order.insert(P.order.end(), lists[sp].begin(), lists[sp].end());
-                }
-            }
-            P.split_begin.push_back((int32_t)P.order.size());
-        }
+        build_item_orders(P);
         *out = std::move(P);
         return ROCKET_OK;
     } catch (const std::bad_alloc &) {

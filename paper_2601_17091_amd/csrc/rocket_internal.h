@@ -54,7 +54,9 @@ struct alignas(16) ItemDesc {
     int32_t cost;      // MFMA instructions per series (scheduling weight)
     int32_t n_ch;      // channels the item's kernels read (their union; 1 if univariate)
     int32_t ch_off;    // first entry of the item's channel list
-    int32_t reserved[4];
+    int32_t t_off;     // MINIROCKET: first threshold, [nq][4] floats
+    int32_t nq;        // MINIROCKET: thresholds (features) per slot in this item
+    int32_t reserved[2];
     double inv_O;      // 1 / O rounded to double (exact PPV, see transform.hip)
 };
 static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");
@@ -68,7 +70,16 @@ constexpr int kNumVariants = 2 * kNumEll;
 constexpr int kNumSplitLayouts = 6;  // 1, 2, 4, 8, 16, 32 splits
 constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 
+// MINIROCKET (Sec. 5 names it): 84 kernels of 9 taps; an item holds 4 of
+// them at one (dilation, padding) and up to kMrMaxThresholds of each pair's
+// biases, compared against the pair's dot products computed once.
+constexpr int kMrKernels = 84;
+constexpr int kMrTaps = 9;
+constexpr int kMrMaxThresholds = 4;
+
 struct HostPlan {
+    bool minirocket = false;
+    int64_t n_features = 0;  // columns of F
     int32_t n_kernels = 0;
     int32_t L = 0;
     int32_t halo_lo = 0;     // padded layout: zeros staged before the series
@@ -83,6 +94,7 @@ struct HostPlan {
     std::vector<float> bias;      // per slot
     std::vector<int32_t> kid;     // per slot, -1 = empty
     std::vector<int32_t> chan;    // per item, its channel list (ascending)
+    std::vector<float> thr;       // MINIROCKET: per item [nq][4] thresholds
     std::vector<int32_t> order;   // kNumSplitLayouts concatenated item orders
     std::vector<int32_t> split_begin;  // per layout: kNumVariants*nsplit + 1 offsets into order
     std::vector<int32_t> layout_off;   // per layout: offset into split_begin
@@ -93,5 +105,16 @@ rocket_status validate_kernels(const rocket_kernels *k, int32_t L);
 
 // Build the host-side tables of a plan.  Assumes validate_kernels passed.
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out);
+
+// MINIROCKET parameters: validation and the plan's host tables.
+rocket_status validate_minirocket(const rocket_minirocket_params *m);
+rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan *out);
+
+// Item orders: per variant, longest-processing-time split of the items into
+// every layout's split count (fills order, split_begin, layout_off).
+void build_item_orders(HostPlan &P);
+
+// Element `index` of the SplitMix64 sequence started at `seed`.
+uint64_t splitmix64_at(uint64_t seed, uint64_t index);
 
 }  // namespace rocket

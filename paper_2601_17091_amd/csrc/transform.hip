@@ -136,6 +136,7 @@ struct FusedArgs {
     int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV)
     int32_t C;         // channels per series
     const int32_t *chan;  // item channel lists
+    const float *thr;     // MINIROCKET items: per item [nq][4] thresholds
     const ItemDesc *items;
     const float *wpk;
     const float *bias;
@@ -531,6 +532,8 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
     it.cost = p->cost;
     it.n_ch = p->n_ch;
     it.ch_off = p->ch_off;
+    it.t_off = p->t_off;
+    it.nq = p->nq;
     it.inv_O = p->inv_O;
     return it;
 }
@@ -550,15 +553,25 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
     }
 }
 
-// Workgroup = (variant, row group, split); each workgroup stages its row
-// group in LDS and runs the items of one variant over it.
-template <int BLOCK, bool CLAMP, bool MPV, bool MC>
-__global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
-    extern __shared__ float smem[];
-    __shared__ int next_item;
-    // Workgroup b runs on XCD b % 8.  Every XCD takes its own share of the
-    // row groups and walks them variant by variant, so all XCDs get the same
-    // mix of work while the CUs of an XCD run one code variant at a time.
+// What one workgroup does: a row group, one variant, one split of its items.
+struct GroupWork {
+    int variant;
+    int beg;        // first entry of the items' order
+    int cnt_items;
+    int nrows;      // series staged
+    int64_t grow;   // first series (global row)
+};
+
+// Workgroup = (variant, row group, split).  Workgroup b runs on XCD b % 8.
+// Every XCD takes its own share of the row groups and walks them variant by
+// variant, so all XCDs get the same mix of work while the CUs of an XCD run
+// one code variant at a time.  Stages the group's series (every channel)
+// with their zero margins into smem, coalesced (channel c of row r at
+// (r*C + c)*row_stride), and the tail pad after them.  Returns false when the
+// workgroup has nothing to do (uniformly for the whole workgroup).
+template <int BLOCK>
+__device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int *next_item,
+                                            GroupWork &w) {
     const int64_t b = blockIdx.x;
     const int xcd = (int)(b % kXcds);
     const int64_t local = b / kXcds;
@@ -567,18 +580,15 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     const int64_t rest = local % per_variant;
     const int64_t group = xcd * a.groups_per_xcd + rest / a.nsplit;
     const int split = (int)(rest % a.nsplit);
-    const int variant = a.variants[vi];
-    const int beg = as_const(a.split_begin)[variant * a.nsplit + split];
-    const int cnt_items = as_const(a.split_begin)[variant * a.nsplit + split + 1] - beg;
+    w.variant = a.variants[vi];
+    w.beg = as_const(a.split_begin)[w.variant * a.nsplit + split];
+    w.cnt_items = as_const(a.split_begin)[w.variant * a.nsplit + split + 1] - w.beg;
     const int64_t first = group * a.rows_per_block;
-    if (cnt_items == 0 || first >= a.n_rows) return;
-    const int nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
-    const int64_t grow = a.row0 + first;
-
-    // stage the group's series (every channel) with their zero margins,
-    // coalesced; channel c of row r at (r*C + c)*row_stride
-    for (int rc = 0; rc < nrows * a.C; ++rc) {
-        const float *x = a.X + ((grow * a.C) + rc) * (int64_t)a.L;
+    if (w.cnt_items == 0 || first >= a.n_rows) return false;
+    w.nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
+    w.grow = a.row0 + first;
+    for (int rc = 0; rc < w.nrows * a.C; ++rc) {
+        const float *x = a.X + ((w.grow * a.C) + rc) * (int64_t)a.L;
         float *dst = smem + rc * a.row_stride;
         for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
             const int m = e - a.halo_lo;
@@ -587,20 +597,196 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     }
     // zeros after the last row: lanes past the last output of an item read
     // up to tail_pad floats past it
-    for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[nrows * a.C * a.row_stride + e] = 0.0f;
-    if (threadIdx.x == 0) next_item = 0;
+    for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[w.nrows * a.C * a.row_stride + e] = 0.0f;
+    if (threadIdx.x == 0) *next_item = 0;
     __syncthreads();
+    return true;
+}
 
+// Workgroup = (variant, row group, split); each workgroup stages its row
+// group in LDS and runs the items of one variant over it.
+template <int BLOCK, bool CLAMP, bool MPV, bool MC>
+__global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
+    extern __shared__ float smem[];
+    __shared__ int next_item;
+    GroupWork w;
+    if (!stage_group<BLOCK>(a, smem, &next_item, w)) return;
     const int lane = threadIdx.x & (rocket::kWave - 1);
-    float *F0 = a.F + grow * (int64_t)a.nf * a.K;
+    float *F0 = a.F + w.grow * (int64_t)a.nf * a.K;
     const float *rows0 = smem + a.halo_lo;
-    switch (variant) {
-        case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 1: run_items<7, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
-        default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt_items, rows0, nrows, a, F0, lane); break;
+    const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
+    switch (w.variant) {
+        case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 1: run_items<7, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// MINIROCKET (Dempster, Schmidt and Webb, KDD 2021; Sec. 5 names it as a
+// variant the same principle carries over to).  An item holds 4 of the 84
+// 9-tap kernels at one (dilation, padding) and NQ (1..4) of each pair's
+// biases.  The tiles' dot products are computed once, starting from 0, and
+// compared with each bias: feature (slot v, bias q) counts C_t > b_{v,q}.
+// ---------------------------------------------------------------------------
+
+// Fold NT tiles into the counts: the count of (slot V, bias Q) over the
+// block is a ballot popcount summed on the scalar unit, then written into
+// lane V*NQ + Q of a vector register (the counts of all (slot, bias) pairs
+// would not fit the scalar registers; v_writelane takes a constant lane).
+template <int V, int Q, int NQ, int NT>
+struct MrFold {
+    __device__ __forceinline__ static void run(const v4f (&acc)[NT][1], const float (&thr)[4][NQ],
+                                               uint32_t &part) {
+        uint32_t s = 0;
+#pragma unroll
+        for (int u = 0; u < NT; ++u) s += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][0][V] > thr[V][Q]));
+        asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(part) : "s"(s), "i"(V * NQ + Q));
+        constexpr int V2 = Q + 1 < NQ ? V : V + 1;
+        constexpr int Q2 = Q + 1 < NQ ? Q + 1 : 0;
+        MrFold<V2, Q2, NQ, NT>::run(acc, thr, part);
+    }
+};
+template <int Q, int NQ, int NT>
+struct MrFold<4, Q, NQ, NT> {
+    __device__ __forceinline__ static void run(const v4f (&)[NT][1], const float (&)[4][NQ], uint32_t &) {}
+};
+
+// part: lanes past 4*NQ stay 0 (set once per item), the others are
+// overwritten by every block
+template <int NT, int NQ>
+__device__ __forceinline__ void mr_reduce(const v4f (&acc)[NT][1], const float (&thr)[4][NQ],
+                                          uint32_t &part, uint32_t &cnt) {
+    MrFold<0, 0, NQ, NT>::run(acc, thr, part);
+    cnt += part;
+}
+
+template <int NT, bool LAST, int NQ, typename Src>
+__device__ __forceinline__ void mr_block(const Src &src, const float (&wa)[1][rocket::kMrTaps],
+                                         const v4f (&z)[1], const v4f (&zlast)[1],
+                                         const float (&thr)[4][NQ], uint32_t &part, uint32_t &cnt) {
+    v4f acc[NT][1];
+    tile_mfma<rocket::kMrTaps, 1, NT, LAST, true>(src, wa, z, zlast, acc);
+    __builtin_amdgcn_sched_barrier(0);
+    mr_reduce<NT, NQ>(acc, thr, part, cnt);
+}
+
+// The last block of a series: its tile count nv (1..N) selects a code copy.
+template <int N, int NQ, typename Src>
+struct MrTail {
+    __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[1][rocket::kMrTaps],
+                                               const v4f (&z)[1], const v4f (&zlast)[1],
+                                               const float (&thr)[4][NQ], uint32_t &part, uint32_t &cnt) {
+        if (nv == N)
+            mr_block<N, true, NQ>(src, wa, z, zlast, thr, part, cnt);
+        else
+            MrTail<N - 1, NQ, Src>::run(nv, src, wa, z, zlast, thr, part, cnt);
+    }
+};
+template <int NQ, typename Src>
+struct MrTail<0, NQ, Src> {
+    __device__ __forceinline__ static void run(int, const Src &, const float (&)[1][rocket::kMrTaps],
+                                               const v4f (&)[1], const v4f (&)[1], const float (&)[4][NQ],
+                                               uint32_t &, uint32_t &) {}
+};
+
+template <int NQ, bool CLAMP>
+__device__ __forceinline__ void run_mr_item(const ItemDesc &it, const float *rows0, int nrows,
+                                            const FusedArgs &a, float *F0, int lane) {
+    constexpr int ELL = rocket::kMrTaps;
+    constexpr int NT = rocket::kTilesPerBlock[0];
+    float wa[1][ELL];
+#pragma unroll
+    for (int j = 0; j < ELL; ++j) wa[0][j] = a.wpk[it.w_off + j * 4 + (lane & 3)];
+    // the biases, copied into vector registers once per item (opaque
+    // copies, so the compiler keeps them there rather than in scalar
+    // registers it would have to spill)
+    float thr[4][NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float t = as_const(a.thr)[it.t_off + q * 4 + v];
+            asm volatile("v_mov_b32 %0, %1" : "=v"(thr[v][q]) : "s"(t));
+        }
+    // start values: 0, and -inf on the lanes past the last output in the
+    // last tile of a series
+    const int rem = it.O - (it.n_tiles - 1) * kTile;
+    v4f z[1], zlast[1];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        float zv;
+        asm volatile("v_mov_b32 %0, 0" : "=v"(zv));
+        z[0][v] = zv;
+        zlast[0][v] = lane < rem ? zv : -INFINITY;
+    }
+    // lane v*NQ + q writes feature (slot v, bias q) of the item
+    int myf = -1;
+    if (lane < 4 * NQ) {
+        const int k0 = a.kid[it.k_off + lane / NQ];
+        myf = k0 >= 0 ? k0 + lane % NQ : -1;
+    }
+    const int row_pitch = a.row_stride;
+    const int nfull = (it.n_tiles - 1) / NT;
+    const int nv = it.n_tiles - nfull * NT;
+    const int64_t f_stride = (int64_t)a.nf * a.K;
+    uint32_t part = 0;
+    for (int r = 0; r < nrows; ++r) {
+        // lane v*NQ + q counts the outputs above bias q of slot v
+        uint32_t cnt = 0;
+        const uint32_t row = lds_addr(rows0 + r * row_pitch);
+        for (int blk = 0; blk < nfull; ++blk) {
+            const int b0 = blk * (NT * kTile) - it.p;
+            if constexpr (CLAMP)
+                mr_block<NT, false, NQ>(ClampedTiles{row, b0, it.d, a.L}, wa, z, zlast, thr, part, cnt);
+            else
+                mr_block<NT, false, NQ>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, z, zlast, thr, part,
+                                        cnt);
+        }
+        const int b0 = nfull * (NT * kTile) - it.p;
+        if constexpr (CLAMP)
+            MrTail<NT, NQ, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, z, zlast, thr, part,
+                                              cnt);
+        else
+            MrTail<NT, NQ, PaddedTiles>::run(nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, z, zlast,
+                                             thr, part, cnt);
+        // PPV = count / O, correctly rounded as in write_row
+        if (myf >= 0) F0[r * f_stride + myf] = (float)((double)cnt * it.inv_O);
+    }
+}
+
+template <int NQ, bool CLAMP>
+__device__ __forceinline__ void run_mr_items(int *next_item, int beg, int cnt_items, const float *rows0,
+                                             int nrows, const FusedArgs &a, float *F0, int lane) {
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
+        run_mr_item<NQ, CLAMP>(it, rows0, nrows, a, F0, lane);
+    }
+}
+
+// MINIROCKET workgroup: as rocket_fused_kernel; the variant is NQ - 1.
+template <int BLOCK, bool CLAMP>
+__global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
+    extern __shared__ float smem[];
+    __shared__ int next_item;
+    GroupWork w;
+    if (!stage_group<BLOCK>(a, smem, &next_item, w)) return;
+    const int lane = threadIdx.x & (rocket::kWave - 1);
+    float *F0 = a.F + w.grow * (int64_t)a.nf * a.K;
+    const float *rows0 = smem + a.halo_lo;
+    const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
+    switch (w.variant) {
+        case 0: run_mr_items<1, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 1: run_mr_items<2, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 2: run_mr_items<3, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        default: run_mr_items<4, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
     }
 }
 
@@ -698,6 +884,19 @@ static const void *fused_fn(int sel) {
     return fns[sel];
 }
 
+// The MINIROCKET kernel's instances: bit 0 the 1024-thread block, bit 1
+// clamped indices.
+constexpr int kMrInstances = 4;
+static const void *mr_fn(int sel) {
+    static const void *const fns[kMrInstances] = {
+        (const void *)rocket_minirocket_kernel<kBlock, false>,
+        (const void *)rocket_minirocket_kernel<kBigBlock, false>,
+        (const void *)rocket_minirocket_kernel<kBlock, true>,
+        (const void *)rocket_minirocket_kernel<kBigBlock, true>,
+    };
+    return fns[sel];
+}
+
 struct rocket_plan {
     rocket::HostPlan host;
     int device = 0;
@@ -705,6 +904,8 @@ struct rocket_plan {
     bool direct = false;
     bool clamp = false;      // rows staged with kClampMargin zeros on each side, tap offsets clamped
     bool mpv = false;        // third feature per kernel: mean of positive values
+    bool minirocket = false; // MINIROCKET plan: F [n, n_features], PPV only
+    int64_t f_cols = 0;      // columns of F
     int32_t C = 1;           // channels per series
     int32_t halo_lo = 0;     // staged layout actually used (floats)
     int32_t row_stride = 0;
@@ -718,6 +919,7 @@ struct rocket_plan {
     int32_t *d_order = nullptr;
     int32_t *d_split_begin = nullptr;
     int32_t *d_chan = nullptr;
+    float *d_thr = nullptr;
     // the kernel set as given, for the direct kernel
     int32_t max_len = 0;
     int32_t *d_cc = nullptr;  // channel counts and indices (multichannel sets)
@@ -731,7 +933,7 @@ struct rocket_plan {
 
 static void plan_free_device(rocket_plan *p) {
     void *ptrs[] = {p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
-                    p->d_split_begin, p->d_chan, p->d_len, p->d_dil, p->d_pad, p->d_b,
+                    p->d_split_begin, p->d_chan, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
     for (void *q : ptrs)
         if (q) (void)hipFree(q);
@@ -741,6 +943,57 @@ static rocket_status map_hip(hipError_t e) {
     if (e == hipSuccess) return ROCKET_OK;
     if (e == hipErrorOutOfMemory) return ROCKET_ERR_OOM;
     return ROCKET_ERR_HIP;
+}
+
+// Staged layout: rows with zero margins wide enough for every tap of every
+// real output if that fits one workgroup's LDS (and clamped is not asked
+// for), else rows with kClampMargin zeros on each side and clamped tap
+// offsets.  Rows per workgroup: as many as fit the LDS budget (at least
+// one).  Returns false when neither layout fits; *lds is the workgroup's LDS.
+static bool choose_layout(rocket_plan *p, bool clamped, const hipDeviceProp_t &prop, int64_t *lds) {
+    const int64_t limit = (int64_t)prop.sharedMemPerBlock;
+    const int64_t L = p->host.L;
+    auto layout = [&](int64_t stride, int64_t pad, int *rows) {
+        const int64_t row_bytes = stride * p->C * (int64_t)sizeof(float);  // every channel
+        const int64_t pad_bytes = pad * (int64_t)sizeof(float);
+        *rows = (int)std::max<int64_t>(
+            1, std::min<int64_t>(kMaxRowsPerBlock, (kRowsLdsBudget - pad_bytes) / row_bytes));
+        return *rows * row_bytes + pad_bytes;
+    };
+    if (!clamped && p->host.row_stride > 0 &&
+        (*lds = layout(p->host.row_stride, p->host.tail_pad, &p->rows_per_block)) <= limit) {
+        p->halo_lo = p->host.halo_lo;
+        p->row_stride = p->host.row_stride;
+        p->tail_pad = p->host.tail_pad;
+        return true;
+    }
+    if ((*lds = layout(L + 2 * rocket::kClampMargin, p->host.tail_pad, &p->rows_per_block)) <= limit) {
+        p->clamp = true;
+        p->halo_lo = rocket::kClampMargin;
+        p->row_stride = (int32_t)(L + 2 * rocket::kClampMargin);
+        p->tail_pad = p->host.tail_pad;
+        return true;
+    }
+    return false;
+}
+
+// Upload the work tables and allow the kernels the workgroup's LDS.
+static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
+    hipError_t e = upload(p->host.items, &p->d_items);
+    if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
+    if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
+    if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
+    if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
+    if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
+    if (e == hipSuccess) e = upload(p->host.chan, &p->d_chan);
+    if (e == hipSuccess) e = upload(p->host.thr, &p->d_thr);
+    if (e == hipSuccess && lds > 64 * 1024) {
+        for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
+            e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        for (int sel = 0; sel < kMrInstances && e == hipSuccess; ++sel)
+            e = hipFuncSetAttribute(mr_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    }
+    return e;
 }
 
 extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t L, uint32_t flags,
@@ -769,36 +1022,10 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     p->n_cu = prop.multiProcessorCount;
     p->mpv = (flags & ROCKET_PLAN_MPV) != 0;
     p->C = p->host.n_channels;
-    // Staged layout: rows with zero margins wide enough for every tap of
-    // every real output if that fits one workgroup's LDS, else rows with
-    // kClampMargin zeros on each side and clamped tap offsets, else the
-    // direct kernel.  Rows per workgroup: as many as fit the LDS budget (at
-    // least one).
-    const int64_t limit = (int64_t)prop.sharedMemPerBlock;
-    auto layout = [&](int64_t stride, int64_t pad, int *rows) {
-        const int64_t row_bytes = stride * p->C * (int64_t)sizeof(float);  // every channel
-        const int64_t pad_bytes = pad * (int64_t)sizeof(float);
-        *rows = (int)std::max<int64_t>(
-            1, std::min<int64_t>(kMaxRowsPerBlock, (kRowsLdsBudget - pad_bytes) / row_bytes));
-        return *rows * row_bytes + pad_bytes;
-    };
+    p->f_cols = (int64_t)(p->mpv ? 3 : 2) * k->n_kernels;
     int64_t lds = 0;
     p->direct = (flags & ROCKET_PLAN_DIRECT) != 0;
-    if (!p->direct && !(flags & ROCKET_PLAN_CLAMPED) && p->host.row_stride > 0 &&
-        (lds = layout(p->host.row_stride, p->host.tail_pad, &p->rows_per_block)) <= limit) {
-        p->halo_lo = p->host.halo_lo;
-        p->row_stride = p->host.row_stride;
-        p->tail_pad = p->host.tail_pad;
-    } else if (!p->direct &&
-               (lds = layout((int64_t)L + 2 * rocket::kClampMargin, p->host.tail_pad, &p->rows_per_block)) <=
-                   limit) {
-        p->clamp = true;
-        p->halo_lo = rocket::kClampMargin;
-        p->row_stride = L + 2 * rocket::kClampMargin;
-        p->tail_pad = p->host.tail_pad;
-    } else {
-        p->direct = true;
-    }
+    if (!p->direct && !choose_layout(p, (flags & ROCKET_PLAN_CLAMPED) != 0, prop, &lds)) p->direct = true;
     p->lds_bytes = p->direct ? 0 : lds;
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
@@ -809,19 +1036,49 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * p->C * k->max_len, &p->d_w);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_count, (size_t)K, &p->d_cc);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_index, (size_t)K * p->C, &p->d_ci);
-    if (!p->direct) {
-        if (e == hipSuccess) e = upload(p->host.items, &p->d_items);
-        if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
-        if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
-        if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
-        if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
-        if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
-        if (e == hipSuccess) e = upload(p->host.chan, &p->d_chan);
-        if (e == hipSuccess && lds > 64 * 1024)
-            for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
-                e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                        (int)lds);
+    if (!p->direct && e == hipSuccess) e = upload_tables(p, lds);
+    if (e != hipSuccess) {
+        plan_free_device(p);
+        delete p;
+        return map_hip(e);
     }
+    *out = p;
+    return ROCKET_OK;
+}
+
+extern "C" rocket_status rocket_minirocket_plan_create(const rocket_minirocket_params *m, uint32_t flags,
+                                                       rocket_plan **out) {
+    if (!out) return ROCKET_ERR_INVALID_ARG;
+    *out = nullptr;
+    if (flags & ~ROCKET_PLAN_CLAMPED) return ROCKET_ERR_INVALID_ARG;
+    rocket_status st = rocket::validate_minirocket(m);
+    if (st != ROCKET_OK) return st;
+    rocket_plan *p = new (std::nothrow) rocket_plan();
+    if (!p) return ROCKET_ERR_OOM;
+    st = rocket::build_minirocket_plan(m, &p->host);
+    if (st != ROCKET_OK) {
+        delete p;
+        return st;
+    }
+    hipError_t e = hipGetDevice(&p->device);
+    hipDeviceProp_t prop;
+    if (e == hipSuccess) e = hipGetDeviceProperties(&prop, p->device);
+    if (e != hipSuccess) {
+        delete p;
+        return ROCKET_ERR_HIP;
+    }
+    p->n_cu = prop.multiProcessorCount;
+    p->minirocket = true;
+    p->C = 1;
+    p->f_cols = p->host.n_features;
+    int64_t lds = 0;
+    if (!choose_layout(p, (flags & ROCKET_PLAN_CLAMPED) != 0, prop, &lds)) {
+        // a series too long for one workgroup's LDS even with 512-zero margins
+        delete p;
+        return ROCKET_ERR_LENGTH;
+    }
+    p->lds_bytes = lds;
+    e = upload_tables(p, lds);
     if (e != hipSuccess) {
         plan_free_device(p);
         delete p;
@@ -849,7 +1106,10 @@ extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_fact
     out->lds_bytes = p->lds_bytes;
     out->direct = p->direct ? 1 : 0;
     out->clamped = p->clamp ? 1 : 0;
-    out->features_per_kernel = p->mpv ? 3 : 2;
+    out->features_per_kernel = p->minirocket ? 0 : (p->mpv ? 3 : 2);
+    out->n_features = p->f_cols;
+    out->minirocket = p->minirocket ? 1 : 0;
+    out->reserved = 0;
     out->rows_per_block = p->direct ? 0 : p->rows_per_block;
     return ROCKET_OK;
 }
@@ -889,8 +1149,11 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.X = X;
     a.F = F;
     a.L = p->host.L;
-    a.K = p->host.n_kernels;
-    a.nf = p->mpv ? 3 : 2;
+    // F rows hold nf * K floats: per kernel (PPV, MAX[, MPV]); a MINIROCKET
+    // plan's rows hold its n_features PPVs (nf = 1)
+    a.K = p->minirocket ? (int32_t)p->f_cols : p->host.n_kernels;
+    a.nf = p->minirocket ? 1 : (p->mpv ? 3 : 2);
+    a.thr = p->d_thr;
     a.C = p->C;
     a.chan = p->d_chan;
     a.items = p->d_items;
@@ -920,8 +1183,9 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         const size_t lds = (size_t)p->lds_bytes;
         const bool big = row_bytes * p->C > kBigLds;
         const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
+        const void *fn = p->minirocket ? mr_fn(sel & 3) : fused_fn(sel);
         void *args[] = {&a};
-        if (hipLaunchKernel(fused_fn(sel), dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) !=
+        if (hipLaunchKernel(fn, dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) !=
             hipSuccess)
             return ROCKET_ERR_HIP;
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
@@ -950,7 +1214,7 @@ extern "C" rocket_status rocket_transform_host(const rocket_plan *p, const float
     if (n == 0) return ROCKET_OK;
     if (!X_host || !F_host) return ROCKET_ERR_INVALID_ARG;
     const int64_t L = (int64_t)p->host.L * p->C;  // floats per series (every channel)
-    const int64_t K2 = (int64_t)(p->mpv ? 3 : 2) * p->host.n_kernels;
+    const int64_t K2 = p->f_cols;  // floats per feature row
     int64_t B = batch_rows;
     // default: about 8 batches, so copies have neighbours to overlap with,
     // each within 256 MiB of staging

@@ -42,6 +42,9 @@ EXPORTED = (
     "rocket_plan_tables_build",
     "rocket_plan_tables_free",
     "rocket_status_string",
+    "rocket_minirocket_fit",
+    "rocket_minirocket_free",
+    "rocket_minirocket_plan_create",
 )
 
 
@@ -73,6 +76,17 @@ class CPlanFacts(ctypes.Structure):
         ("mfma_per_row", ctypes.c_int64), ("lds_bytes", ctypes.c_int64),
         ("direct", ctypes.c_int32), ("clamped", ctypes.c_int32),
         ("features_per_kernel", ctypes.c_int32), ("rows_per_block", ctypes.c_int32),
+        ("n_features", ctypes.c_int64), ("minirocket", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    ]
+
+
+class CMiniRocketParams(ctypes.Structure):
+    _fields_ = [
+        ("input_length", ctypes.c_int32), ("n_dilations", ctypes.c_int32),
+        ("n_features", ctypes.c_int32),
+        ("dilations", ctypes.POINTER(ctypes.c_int32)),
+        ("features_per_dilation", ctypes.POINTER(ctypes.c_int32)),
+        ("biases", ctypes.POINTER(ctypes.c_float)),
     ]
 
 
@@ -132,6 +146,13 @@ def library() -> ctypes.CDLL:
     lib.rocket_plan_tables_free.restype = None
     lib.rocket_status_string.argtypes = [ctypes.c_int]
     lib.rocket_status_string.restype = ctypes.c_char_p
+    mp = ctypes.POINTER(CMiniRocketParams)
+    lib.rocket_minirocket_fit.argtypes = [vp, i64, i32, i32, ctypes.c_uint64, mp]
+    lib.rocket_minirocket_fit.restype = ctypes.c_int
+    lib.rocket_minirocket_free.argtypes = [mp]
+    lib.rocket_minirocket_free.restype = None
+    lib.rocket_minirocket_plan_create.argtypes = [mp, ctypes.c_uint32, ctypes.POINTER(vp)]
+    lib.rocket_minirocket_plan_create.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -305,11 +326,13 @@ class Plan:
         _check(library().rocket_plan_info(self._h, ctypes.byref(f)), "rocket_plan_info")
         return dict(n_items=f.n_items, n_buckets=f.n_buckets, mfma_per_row=f.mfma_per_row,
                     lds_bytes=f.lds_bytes, direct=bool(f.direct), clamped=bool(f.clamped),
-                    features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block)
+                    features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block,
+                    n_features=f.n_features, minirocket=bool(f.minirocket))
 
     @property
     def n_features(self) -> int:
-        """Columns of F: features_per_kernel * n_kernels."""
+        """Columns of F: features_per_kernel * n_kernels (MINIROCKET: its
+        feature count)."""
         return self.features_per_kernel * self.n_kernels
 
     def transform_into(self, X, F, stream=None):
@@ -366,6 +389,61 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+
+def minirocket_fit(X_train, num_features: int = 10000, seed: int = 0) -> dict:
+    """rocket_minirocket_fit on a host training set X_train [n, L] (fp32),
+    copied into numpy arrays (library copy freed)."""
+    lib = library()
+    X = np.ascontiguousarray(X_train, dtype=np.float32)
+    if X.ndim != 2:
+        raise ValueError("X_train must be [n, L]")
+    cp = CMiniRocketParams()
+    _check(lib.rocket_minirocket_fit(_ptr(X, ctypes.c_float), X.shape[0], X.shape[1], int(num_features),
+                                     ctypes.c_uint64(seed & (2 ** 64 - 1)), ctypes.byref(cp)),
+           "rocket_minirocket_fit")
+    try:
+        nd, nf = cp.n_dilations, cp.n_features
+        return dict(input_length=cp.input_length,
+                    dilations=np.ctypeslib.as_array(cp.dilations, (nd,)).copy(),
+                    features_per_dilation=np.ctypeslib.as_array(cp.features_per_dilation, (nd,)).copy(),
+                    biases=np.ctypeslib.as_array(cp.biases, (nf,)).copy())
+    finally:
+        lib.rocket_minirocket_free(ctypes.byref(cp))
+
+
+def as_c_minirocket(params: dict):
+    """A rocket_minirocket_params view of numpy MINIROCKET parameters; returns
+    (struct, keepalive)."""
+    dil = np.ascontiguousarray(params["dilations"], dtype=np.int32)
+    feats = np.ascontiguousarray(params["features_per_dilation"], dtype=np.int32)
+    biases = np.ascontiguousarray(params["biases"], dtype=np.float32)
+    c = CMiniRocketParams(int(params["input_length"]), dil.shape[0], biases.shape[0],
+                          _ptr(dil, ctypes.c_int32), _ptr(feats, ctypes.c_int32), _ptr(biases, ctypes.c_float))
+    return c, (dil, feats, biases)
+
+
+class MiniRocketPlan(Plan):
+    """rocket_minirocket_plan_create: MINIROCKET parameters planned for series
+    of their input length; transform_into writes F [n, n_features] (PPV)."""
+
+    def __init__(self, params: dict, clamped: bool = False):
+        lib = library()
+        self._c, self._keep = as_c_minirocket(params)
+        self.L = int(params["input_length"])
+        h = ctypes.c_void_p()
+        _check(lib.rocket_minirocket_plan_create(ctypes.byref(self._c),
+                                                 ROCKET_PLAN_CLAMPED if clamped else ROCKET_PLAN_DEFAULT,
+                                                 ctypes.byref(h)), "rocket_minirocket_plan_create")
+        self._h = h
+        self.n_kernels = 84
+        self.features_per_kernel = 0
+        self.n_channels = 1
+        self._n_features = int(self._c.n_features)
+
+    @property
+    def n_features(self) -> int:
+        return self._n_features
 
 
 def transform(X, kernels: dict, stream=None):

@@ -25,6 +25,8 @@ row in fp64 (population standard deviation) and stored as fp32, row-major.
                   kernels (Sec. 3.3): per series, 3 latent random walks mixed
                   into the 6 channels with random weights plus N(0, 0.3)
                   noise; every channel z-normalised
+  minirocket      the manufacturing series with MINIROCKET (Sec. 5 names it):
+                  10,000 features fitted on the first 1,000 series
 
 Kernel seed 200 + i and data seed 100 + i for workload i = 1 .. 5.
 """
@@ -55,6 +57,10 @@ WORKLOADS = {
     "many_short": Workload("many_short", 1000000, 64, 10000, 205, 105, "trend"),
     "paper_sweep": Workload("paper_sweep", 1000, 10000, 10000, 206, 106, "random_walk"),
     "multivariate": Workload("multivariate", 10000, 500, 10000, 208, 108, "mixed_walks", 6),
+    # MINIROCKET (Sec. 5): the Manufacturing series; n_kernels is the number of
+    # features requested from the fit, kernel_seed the fit's seed; the fit uses
+    # the first 1,000 series
+    "minirocket": Workload("minirocket", 100000, 1000, 10000, 209, 103, "ar1"),
 }
 
 

@@ -149,3 +149,62 @@ def test_plan_tables_errors(lib):
     lib.rocket_plan_tables_free(ctypes.byref(t))
     lib.rocket_plan_tables_free(ctypes.byref(t))
     lib.rocket_plan_tables_free(None)
+
+
+@pytest.mark.parametrize("n,L,nf,seed", [(5, 9, 10000, 0), (7, 17, 10000, 1), (40, 300, 5000, 2),
+                                         (30, 1000, 10000, 3), (3, 64, 10000, 2 ** 64 - 1)])
+def test_minirocket_fit_matches_oracle_bitwise(lib, oracle, n, L, nf, seed):
+    from oracle import minirocket_oracle as mo
+    rng = np.random.default_rng(seed % 1000)
+    X = rng.standard_normal((n, L)).cumsum(axis=1).astype(np.float32)
+    a = rk.minirocket_fit(X, nf, seed)
+    b = mo.fit(X, nf, seed)
+    assert a["input_length"] == L
+    for key in ("dilations", "features_per_dilation", "biases"):
+        assert a[key].dtype == b[key].dtype, key
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+
+
+def test_minirocket_fit_errors_and_free(lib):
+    cp = rb.CMiniRocketParams()
+    X = np.zeros((2, 20), np.float32)
+    xp = X.ctypes.data_as(ctypes.c_void_p)
+    assert lib.rocket_minirocket_fit(None, 2, 20, 100, 0, ctypes.byref(cp)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_minirocket_fit(xp, 0, 20, 100, 0, ctypes.byref(cp)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_minirocket_fit(xp, 2, 8, 100, 0, ctypes.byref(cp)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_minirocket_fit(xp, 2, 20, 83, 0, ctypes.byref(cp)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_minirocket_fit(xp, 2, 20, 100, 0, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_minirocket_fit(xp, 2, 20, 100, 0, ctypes.byref(cp)) == rb.ROCKET_OK
+    assert cp.n_features == 84 and cp.n_dilations == 1 and cp.input_length == 20
+    lib.rocket_minirocket_free(ctypes.byref(cp))
+    assert cp.n_features == 0 and not cp.biases
+    lib.rocket_minirocket_free(ctypes.byref(cp))  # idempotent
+    lib.rocket_minirocket_free(None)              # NULL-safe
+
+
+def test_minirocket_plan_rejects_bad_params_before_the_device(lib):
+    """Validation happens before any device call, so these run without a GPU."""
+    good = dict(input_length=100, dilations=np.array([1, 3], np.int32),
+                features_per_dilation=np.array([1, 2], np.int32), biases=np.zeros(84 * 3, np.float32))
+
+    def status(params, flags=0):
+        c, keep = rb.as_c_minirocket(params)
+        h = ctypes.c_void_p()
+        r = lib.rocket_minirocket_plan_create(ctypes.byref(c), flags, ctypes.byref(h))
+        del keep
+        return r
+
+    bad = [
+        (dict(good, biases=np.zeros(84 * 3 - 1, np.float32)), rb.ROCKET_ERR_INVALID_ARG),  # count mismatch
+        (dict(good, dilations=np.array([3, 1], np.int32)), rb.ROCKET_ERR_INVALID_ARG),     # not ascending
+        (dict(good, dilations=np.array([0, 3], np.int32)), rb.ROCKET_ERR_INVALID_ARG),
+        (dict(good, features_per_dilation=np.array([-1, 4], np.int32)), rb.ROCKET_ERR_INVALID_ARG),
+        (dict(good, input_length=8), rb.ROCKET_ERR_INVALID_ARG),
+        (dict(good, dilations=np.array([1, 13], np.int32)), rb.ROCKET_ERR_LENGTH),         # 100 - 8*13 < 1
+    ]
+    for params, want in bad:
+        assert status(params) == want, (params, want)
+    assert status(good, rb.ROCKET_PLAN_MPV) == rb.ROCKET_ERR_INVALID_ARG
+    assert status(good, rb.ROCKET_PLAN_DIRECT) == rb.ROCKET_ERR_INVALID_ARG
+    h = ctypes.c_void_p()
+    assert lib.rocket_minirocket_plan_create(None, 0, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
