@@ -54,16 +54,16 @@ def valid_taps(kernels, L):
 
 def source_digest():
     h = hashlib.sha256()
-    for name in ("transform.hip", "plan.cpp", "rocket_internal.h"):
+    for name in ("transform.hip", "plan.cpp", "rocket_internal.h", "minirocket.cpp"):
         with open(os.path.join(ROOT, "paper_2601_17091_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(workload, digest):
+def traffic_from_profile(workload, digest, kernel="rocket_fused_kernel"):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it
     was taken on the current kernel sources; else None."""
-    path = os.path.join(ROOT, "profiles", "rocket_fused_kernel_%s_pmc.json" % workload)
+    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.json" % (kernel, workload))
     if not os.path.exists(path):
         return None
     try:
@@ -110,6 +110,8 @@ def main():
 
     if args.sweep:
         return sweep(args)
+    if args.workload == "minirocket":
+        return bench_minirocket(args)
 
     if not os.path.exists(rk.rocket.LIB_PATH):
         from paper_2601_17091_amd import build_lib
@@ -263,6 +265,134 @@ def main():
                      "nominal_fma_per_series": nominal_per_row,
                      "mfma_fma_issued_per_series": 256 * info["mfma_per_row"],
                      "mfma_pipe_frac": mfma_fma_issued_frac(mfma_fma_per_pass, ms_per_step)},
+        "plan": dict(info, create_ms=plan_ms),
+        "device": {"name": props.name, "cu": props.multi_processor_count},
+        "source_digest": digest,
+        "cpu_baseline": cpu,
+        "parity": parity,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def minirocket_valid_taps(params, L):
+    """Algorithmic FMAs of one series under MINIROCKET: the valid taps of
+    every (dilation, kernel) pair, counted once per pair (its biases share
+    the pair's dot products)."""
+    total = 0
+    for i, d in enumerate(params["dilations"]):
+        if int(params["features_per_dilation"][i]) == 0:
+            continue
+        d = int(d)
+        for k in range(84):
+            p = 4 * d if (i + k) % 2 == 0 else 0
+            O = L + 2 * p - 8 * d
+            for j in range(9):
+                lo, hi = max(0, p - j * d), min(O, p - j * d + L)
+                total += max(0, hi - lo)
+    return total
+
+
+def bench_minirocket(args):
+    """MINIROCKET (Sec. 5 names it): the Manufacturing series, 10,000
+    features fitted on the first 1,000 series; one step = one transform pass
+    over every series (F [n, n_features] of PPVs)."""
+    import torch
+
+    import paper_2601_17091_amd as rk
+    from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
+
+    if not os.path.exists(rk.rocket.LIB_PATH):
+        from paper_2601_17091_amd import build_lib
+        build_lib.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = WORKLOADS["minirocket"]
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(dev)
+    log("workload minirocket: n=%d L=%d features requested=%d" % (w.n, w.L, w.n_kernels))
+    t0 = time.perf_counter()
+    X_np = workload_series(w.name)
+    log("series generated in %.1f s" % (time.perf_counter() - t0))
+    t0 = time.perf_counter()
+    params = rk.minirocket_fit(X_np[:1000], w.n_kernels, w.kernel_seed)
+    fit_ms = (time.perf_counter() - t0) * 1e3
+    nf = int(params["biases"].shape[0])
+    log("fit on 1000 series: %d dilations, %d features (%.1f ms)" % (len(params["dilations"]), nf, fit_ms))
+    X = torch.from_numpy(X_np).to(dev)
+    t0 = time.perf_counter()
+    plan = rk.MiniRocketPlan(params)
+    torch.cuda.synchronize()
+    plan_ms = (time.perf_counter() - t0) * 1e3
+    info = plan.info()
+    log("plan: %s (%.1f ms)" % (info, plan_ms))
+    F = torch.empty((w.n, nf), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    if args.copy_mb > 0:
+        src = torch.ones(args.copy_mb << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        log("copy reference: %d MiB read, %d MiB written" % (args.copy_mb, args.copy_mb))
+        del src, dst
+    for i in range(args.warmup):
+        plan.transform_into(X, F, stream)
+        torch.cuda.synchronize()
+        log("warmup %d/%d done" % (i + 1, args.warmup))
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        plan.transform_into(X, F, stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / max(args.steps, 1)
+    log("timed %d passes: %.3f ms per pass" % (args.steps, ms))
+    valid = minirocket_valid_taps(params, w.L)
+    flops = 2.0 * w.n * valid
+    achieved = flops / (ms * 1e-3) / 1e12
+    digest = source_digest()
+    cpu = parity = None
+    if not args.no_cpu_baseline:
+        from oracle import minirocket_oracle, rocket_oracle
+        rocket_oracle.build()
+        threads = rocket_oracle.max_threads()
+        rng_rows = sample_rows(w.n, w.n, 4096)
+        t0 = time.perf_counter()
+        minirocket_oracle.transform(X_np, params, rows=rng_rows[:2], threads=threads)
+        per_row = max((time.perf_counter() - t0) / 2.0, 1e-6)
+        m = int(max(2, min(rng_rows.shape[0], args.cpu_seconds / per_row * threads)))
+        rows = np.unique(np.concatenate([rng_rows[:2], rng_rows[-2:],
+                                         np.random.default_rng(3).choice(rng_rows, m, replace=False)]))
+        log("oracle on %d rows (%d threads)" % (rows.shape[0], threads))
+        t0 = time.perf_counter()
+        ref = minirocket_oracle.transform(X_np, params, rows=rows, threads=threads)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": rows.shape[0] * nf / cpu_s, "unit": "series*features/s", "cores": threads,
+               "kind": "oracle",
+               "sample": "%d of %d minirocket rows (first/last row, seeded random), all %d features, fp64, "
+                         "%.1f s" % (rows.shape[0], w.n, nf, cpu_s)}
+        plan.transform_into(X, F, stream)
+        torch.cuda.synchronize()
+        got = F[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
+        cnt = np.rint(got * ref["O"][None, :])
+        parity = {"rows": int(rows.shape[0]), "max_count_err": int(np.abs(cnt - ref["cnt"]).max()),
+                  "outside_certified": int(((cnt < ref["cnt_lo"]) | (cnt > ref["cnt_hi"])).sum())}
+        log("parity %s" % parity)
+    out = {
+        "metric": "series*features/s (MINIROCKET transform, fp32, 1 MI355X)",
+        "value": w.n * nf / (ms * 1e-3),
+        "unit": "series*features/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "fp32",
+        "data": "synthetic (seeded ar1 series, z-normalised; MINIROCKET fitted on the first 1000)",
+        "config": {"workload": "minirocket", "n_series": w.n, "series_length": w.L, "features": nf,
+                   "dilations": [int(d) for d in params["dilations"]], "fit_seed": w.kernel_seed,
+                   "data_seed": w.data_seed, "fit_ms": fit_ms},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_TFLOPS,
+                     "traffic": traffic_from_profile("minirocket", digest, "rocket_minirocket_kernel"),
+                     "kernel": "rocket_minirocket_kernel", "launches_per_step": 1, "launch_ms": ms,
+                     "algorithmic_flops_per_launch": flops, "valid_fma_per_series": valid,
+                     "mfma_fma_issued_per_series": 256 * info["mfma_per_row"]},
         "plan": dict(info, create_ms=plan_ms),
         "device": {"name": props.name, "cu": props.multi_processor_count},
         "source_digest": digest,
