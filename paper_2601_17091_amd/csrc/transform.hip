@@ -388,7 +388,7 @@ __device__ __forceinline__ float reduce4(const v4f &m) {
 // fold32(m0, m1): lanes 0-31 slot 0, lanes 32-63 slot 1; fold16 of
 // (slot0|slot1) and (slot2|slot3): row 0 slot 0, row 1 slot 2, row 2 slot 1,
 // row 3 slot 3.
-__device__ __forceinline__ int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
+__device__ constexpr int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
 
 template <int G, bool MPV>
 __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
@@ -411,17 +411,17 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&okid)
     for (int g = 0; g < G; ++g) {
         const float m = reduce4<OpMax>(ra.mx[g]);
         const float psum = MPV ? reduce4<OpSum>(ra.ps[g]) : 0.0f;
-        // the count of slot slot_of_row(q) for the lanes of row q
-        // (readfirstlane keeps the four uniform counts independent scalars,
-        // so the selects stay selects)
-        const uint32_t c0 = __builtin_amdgcn_readfirstlane(ra.cnt[g][0]);
-        const uint32_t c1 = __builtin_amdgcn_readfirstlane(ra.cnt[g][1]);
-        const uint32_t c2 = __builtin_amdgcn_readfirstlane(ra.cnt[g][2]);
-        const uint32_t c3 = __builtin_amdgcn_readfirstlane(ra.cnt[g][3]);
-        uint32_t c = c0;
-        c = lane >= 16 ? c2 : c;
-        c = lane >= 32 ? c1 : c;
-        c = lane >= 48 ? c3 : c;
+        // the count of slot slot_of_row(q) into writer lane 16q (scalar to
+        // lane moves: one instruction each, no lane masks)
+        uint32_t c;
+        asm volatile(
+            "v_writelane_b32 %0, %1, 0\n\t"
+            "v_writelane_b32 %0, %2, 16\n\t"
+            "v_writelane_b32 %0, %3, 32\n\t"
+            "v_writelane_b32 %0, %4, 48"
+            : "=&v"(c)
+            : "s"(ra.cnt[g][slot_of_row(0)]), "s"(ra.cnt[g][slot_of_row(1)]), "s"(ra.cnt[g][slot_of_row(2)]),
+              "s"(ra.cnt[g][slot_of_row(3)]));
         const int ok = okid[g];
         if (ok >= 0) {
             // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
