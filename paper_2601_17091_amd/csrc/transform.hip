@@ -22,6 +22,11 @@
 //      the scalar unit; no dot product is written to memory (Sec. 3.2 keeps
 //      only the two counters per pair as well);
 //   6. PPV = count / O and MAX are written to F in the original kernel order.
+//
+// MINIROCKET kernel (the variant Sec. 5 names): the same staging, tiles and
+// MFMA contraction over 4 of its 84 fixed kernels at one (dilation,
+// padding), the chains starting from 0; each pair's dot products are then
+// compared with up to 4 of its biases, and PPV = count / O per (pair, bias).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -133,7 +138,8 @@ struct FusedArgs {
     int64_t n_rows;    // rows in this launch
     int32_t L;
     int32_t K;
-    int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV)
+    int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV); 1 for
+                       // MINIROCKET, whose K is then its feature count
     int32_t C;         // channels per series
     const int32_t *chan;  // item channel lists
     const float *thr;     // MINIROCKET items: per item [nq][4] thresholds
@@ -406,7 +412,7 @@ __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 // 0, 16, 32 and 48.
 template <int G, bool MPV>
 __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&okid)[G], double inv_O,
-                                          int lane, float *Frow) {
+                                          float *Frow) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const float m = reduce4<OpMax>(ra.mx[g]);
@@ -516,7 +522,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         else
             TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(
                 nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra);
-        write_row<G, MPV>(ra, okid, it.inv_O, lane, F0 + r * f_stride);
+        write_row<G, MPV>(ra, okid, it.inv_O, F0 + r * f_stride);
     }
 }
 
