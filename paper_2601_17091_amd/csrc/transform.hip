@@ -40,6 +40,8 @@
 using rocket::ItemDesc;
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
+constexpr uint64_t kNegInfPair = 0xff800000ff800000ull;  // two fp32 -inf
 
 // Read-only tables indexed by wavefront-uniform values are read through the
 // constant address space, which lets the compiler use scalar loads.
@@ -108,17 +110,94 @@ __device__ __forceinline__ void lds_tiles<4>(uint32_t m, float (&xv)[4]) {
         : "s"(m)
         : "memory");
 }
-// 5..8 tiles: the first 4, then the rest from 1,024 bytes further
+// 5..8 tiles: all reads from one M0, then two waits.  lds_tiles waits until
+// at most NT-4 reads are in flight (lgkmcnt(NT-4)); LDS reads complete in
+// order, so tiles 0-3 are ready and their MFMAs can issue while the rest
+// arrive.  lds_tiles_rest then waits for the rest: it takes tiles 4.. as
+// operands and returns them, so no use of them precedes it.
 template <int NT>
-__device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]) {
-    static_assert(NT > 4 && NT <= 8, "1 to 8 tiles per block");
-    float a[4], b[NT - 4];
-    lds_tiles<4>(m, a);
-    lds_tiles<NT - 4>(m + 1024u, b);
-#pragma unroll
-    for (int u = 0; u < 4; ++u) xv[u] = a[u];
-#pragma unroll
-    for (int u = 4; u < NT; ++u) xv[u] = b[u - 4];
+__device__ __forceinline__ void lds_tiles_rest(float (&xv)[NT]);
+
+template <>
+__device__ __forceinline__ void lds_tiles<5>(uint32_t m, float (&xv)[5]) {
+    asm volatile(
+        "s_mov_b32 m0, %5\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\t"
+        "ds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\t"
+        "ds_read_addtid_b32 %3 offset:768\n\t"
+        "ds_read_addtid_b32 %4 offset:1024\n\t"
+        "s_waitcnt lgkmcnt(1)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles_rest<5>(float (&xv)[5]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]) : : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_tiles<6>(uint32_t m, float (&xv)[6]) {
+    asm volatile(
+        "s_mov_b32 m0, %6\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\t"
+        "ds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\t"
+        "ds_read_addtid_b32 %3 offset:768\n\t"
+        "ds_read_addtid_b32 %4 offset:1024\n\t"
+        "ds_read_addtid_b32 %5 offset:1280\n\t"
+        "s_waitcnt lgkmcnt(2)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles_rest<6>(float (&xv)[6]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]), "+v"(xv[5]) : : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_tiles<7>(uint32_t m, float (&xv)[7]) {
+    asm volatile(
+        "s_mov_b32 m0, %7\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\t"
+        "ds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\t"
+        "ds_read_addtid_b32 %3 offset:768\n\t"
+        "ds_read_addtid_b32 %4 offset:1024\n\t"
+        "ds_read_addtid_b32 %5 offset:1280\n\t"
+        "ds_read_addtid_b32 %6 offset:1536\n\t"
+        "s_waitcnt lgkmcnt(3)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5]), "=&v"(xv[6])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles_rest<7>(float (&xv)[7]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]), "+v"(xv[5]), "+v"(xv[6]) : : "memory");
+}
+
+template <>
+__device__ __forceinline__ void lds_tiles<8>(uint32_t m, float (&xv)[8]) {
+    asm volatile(
+        "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\t"
+        "ds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\t"
+        "ds_read_addtid_b32 %3 offset:768\n\t"
+        "ds_read_addtid_b32 %4 offset:1024\n\t"
+        "ds_read_addtid_b32 %5 offset:1280\n\t"
+        "ds_read_addtid_b32 %6 offset:1536\n\t"
+        "ds_read_addtid_b32 %7 offset:1792\n\t"
+        "s_waitcnt lgkmcnt(4)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5]), "=&v"(xv[6]), "=&v"(xv[7])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_tiles_rest<8>(float (&xv)[8]) {
+    asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]), "+v"(xv[5]), "+v"(xv[6]), "+v"(xv[7]) : : "memory");
 }
 
 namespace {
@@ -164,6 +243,7 @@ constexpr int kDppQuadSwap1 = 0xB1;   // quad_perm(1,0,3,2)
 constexpr int kDppQuadSwap2 = 0x4E;   // quad_perm(2,3,0,1)
 constexpr int kDppRowHalfMirror = 0x141;
 constexpr int kDppRowMirror = 0x140;
+constexpr int kDppRowRor8 = 0x128;     // row_ror:8 (lane i of a row reads lane i^8)
 
 // Where a block's series values come from.  m0(j) is the LDS byte address
 // of lane 0's value under tap j in the block's first tile; lane l reads 4*l
@@ -239,14 +319,23 @@ __device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][E
     for (int j = 0; j < ELL; ++j) {
         float xv[NT];
         lds_tiles<NT>(src.m0(j), xv);
+        constexpr int NA = NT > 4 ? 4 : NT;  // tiles ready after lds_tiles
 #pragma unroll
-        for (int u = 0; u < NT; ++u)
+        for (int u = 0; u < NT; ++u) {
+            if (NT > 4 && u == NA) {
+                // tiles 4..: wait for the rest of the reads only now, after
+                // the MFMAs of tiles 0-3 (the barriers keep this order)
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (NT > 4) lds_tiles_rest<NT>(xv);
+            }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 const v4f c = (FIRST && j == 0) ? ((LAST && u == NT - 1) ? blast[g] : binit[g])
                                                 : acc[u][g];
                 acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xv[u], c, 0, 0, 0);
             }
+        }
+        if (NT > 4) __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -396,27 +485,80 @@ __device__ __forceinline__ float reduce4(const v4f &m) {
 // row 3 slot 3.
 __device__ constexpr int slot_of_row(int q) { return ((q & 1) << 1) | (q >> 1); }
 
+// The same for the 8 slots of two groups at once: after the 32- and 16-lane
+// folds of each group, the two 16-lane rows q of the groups fold over lane
+// pairs (i, i+8) into one register (lanes 0-7 of the row keep group 0,
+// lanes 8-15 group 1), and three DPP steps finish each 8-lane half-row.  On
+// return the lanes 16q + 8h .. 16q + 8h + 7 hold slot slot_of_row(q) of
+// group h.  18 vector instructions for 8 slots, against 20 for two reduce4.
+template <typename Op>
+__device__ __forceinline__ float reduce8(const v4f &m0, const v4f &m1, bool hi8) {
+    const float e = fold16<Op>(fold32<Op>(m0[0], m0[1]), fold32<Op>(m0[2], m0[3]));
+    const float h = fold16<Op>(fold32<Op>(m1[0], m1[1]), fold32<Op>(m1[2], m1[3]));
+    const float re = dpp_row_step<Op, kDppRowRor8>(e);
+    const float rh = dpp_row_step<Op, kDppRowRor8>(h);
+    float v = hi8 ? rh : re;
+    v = dpp_row_step<Op, kDppQuadSwap1>(v);
+    v = dpp_row_step<Op, kDppQuadSwap2>(v);
+    return dpp_row_step<Op, kDppRowHalfMirror>(v);
+}
+
+// The writer lane of a kernel slot after the wavefront reduction (-1: the
+// lane writes nothing): lane 16q writes slot slot_of_row(q) of a 4-kernel
+// item; lane 16q + 8h writes slot slot_of_row(q) of group h of an 8-kernel
+// item.  Returns the slot index 4h + v, or -1.
+template <int G>
+__device__ __forceinline__ int writer_slot(int lane) {
+    if (G == 1) return (lane & 15) == 0 ? slot_of_row(lane >> 4) : -1;
+    return (lane & 7) == 0 ? 4 * ((lane >> 3) & 1) + slot_of_row(lane >> 4) : -1;
+}
+
 template <int G, bool MPV>
 __device__ __forceinline__ void init_row(RowAcc<G> &ra) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-        ra.mx[g] = v4f{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        // -inf into the four running maxima with two 64-bit moves
+        v2f lo, hi;
+        asm volatile("v_mov_b64 %0, %2\n\tv_mov_b64 %1, %2" : "=v"(lo), "=v"(hi) : "s"(kNegInfPair));
+        ra.mx[g] = v4f{lo[0], lo[1], hi[0], hi[1]};
         if (MPV) ra.ps[g] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int v = 0; v < 4; ++v) ra.cnt[g][v] = 0;
     }
 }
 
+// One kernel's features from its writer lane: PPV = c / O, MAX, and MPV.
+template <bool MPV>
+__device__ __forceinline__ void write_features(uint32_t c, float m, float psum, int ok, double inv_O,
+                                               float *Frow) {
+    // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the quotient
+    // is never a float midpoint and lies at least 2^-49 (relative) from one,
+    // while c * fl64(1/O) is within 2^-52 of it, so rounding the double
+    // product to float gives the same float as the fp32 division
+    const float ppv = (float)((double)c * inv_O);
+    if (MPV) {
+        // rows of 3 floats: 4-byte aligned only
+        float *f = Frow + 3 * (int64_t)ok;
+        f[0] = ppv;
+        f[1] = m;
+        f[2] = c > 0 ? psum / (float)c : 0.0f;
+    } else {
+        float2 res;
+        res.x = ppv;
+        res.y = m;
+        *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)ok) = res;
+    }
+}
+
 // MAX (and the MPV numerator) over the wavefront (counts are already
-// scalar), then per kernel {PPV, MAX} (or {PPV, MAX, MPV}), written by lanes
-// 0, 16, 32 and 48.
+// scalar), then per kernel {PPV, MAX} (or {PPV, MAX, MPV}), written by the
+// writer lanes (writer_slot); okid is the kernel id the lane writes, or -1.
 template <int G, bool MPV>
-__device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&okid)[G], double inv_O,
-                                          float *Frow) {
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-        const float m = reduce4<OpMax>(ra.mx[g]);
-        const float psum = MPV ? reduce4<OpSum>(ra.ps[g]) : 0.0f;
+__device__ __forceinline__ void write_row(const RowAcc<G> &ra, int okid, double inv_O, float *Frow,
+                                          bool hi8) {
+    if constexpr (G == 1) {
+        const float m = reduce4<OpMax>(ra.mx[0]);
+        const float psum = MPV ? reduce4<OpSum>(ra.ps[0]) : 0.0f;
         // the count of slot slot_of_row(q) into writer lane 16q (scalar to
         // lane moves: one instruction each, no lane masks)
         uint32_t c;
@@ -426,29 +568,28 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, const int (&okid)
             "v_writelane_b32 %0, %3, 32\n\t"
             "v_writelane_b32 %0, %4, 48"
             : "=&v"(c)
-            : "s"(ra.cnt[g][slot_of_row(0)]), "s"(ra.cnt[g][slot_of_row(1)]), "s"(ra.cnt[g][slot_of_row(2)]),
-              "s"(ra.cnt[g][slot_of_row(3)]));
-        const int ok = okid[g];
-        if (ok >= 0) {
-            // (float)c / (float)O, correctly rounded: for c <= O < 2^24 the
-            // quotient is never a float midpoint and lies at least 2^-49
-            // (relative) from one, while c * fl64(1/O) is within 2^-52 of
-            // it, so rounding the double product to float gives the same
-            // float as the fp32 division
-            const float ppv = (float)((double)c * inv_O);
-            if (MPV) {
-                // rows of 3 floats: 4-byte aligned only
-                float *f = Frow + 3 * (int64_t)ok;
-                f[0] = ppv;
-                f[1] = m;
-                f[2] = c > 0 ? psum / (float)c : 0.0f;
-            } else {
-                float2 res;
-                res.x = ppv;
-                res.y = m;
-                *reinterpret_cast<float2 *>(Frow + 2 * (int64_t)ok) = res;
-            }
-        }
+            : "s"(ra.cnt[0][slot_of_row(0)]), "s"(ra.cnt[0][slot_of_row(1)]), "s"(ra.cnt[0][slot_of_row(2)]),
+              "s"(ra.cnt[0][slot_of_row(3)]));
+        if (okid >= 0) write_features<MPV>(c, m, psum, okid, inv_O, Frow);
+    } else {
+        const float m = reduce8<OpMax>(ra.mx[0], ra.mx[1], hi8);
+        const float psum = MPV ? reduce8<OpSum>(ra.ps[0], ra.ps[1], hi8) : 0.0f;
+        // the count of slot slot_of_row(q) of group h into lane 16q + 8h
+        uint32_t c;
+        asm volatile(
+            "v_writelane_b32 %0, %1, 0\n\t"
+            "v_writelane_b32 %0, %2, 8\n\t"
+            "v_writelane_b32 %0, %3, 16\n\t"
+            "v_writelane_b32 %0, %4, 24\n\t"
+            "v_writelane_b32 %0, %5, 32\n\t"
+            "v_writelane_b32 %0, %6, 40\n\t"
+            "v_writelane_b32 %0, %7, 48\n\t"
+            "v_writelane_b32 %0, %8, 56"
+            : "=&v"(c)
+            : "s"(ra.cnt[0][slot_of_row(0)]), "s"(ra.cnt[1][slot_of_row(0)]), "s"(ra.cnt[0][slot_of_row(1)]),
+              "s"(ra.cnt[1][slot_of_row(1)]), "s"(ra.cnt[0][slot_of_row(2)]), "s"(ra.cnt[1][slot_of_row(2)]),
+              "s"(ra.cnt[0][slot_of_row(3)]), "s"(ra.cnt[1][slot_of_row(3)]));
+        if (okid >= 0) write_features<MPV>(c, m, psum, okid, inv_O, Frow);
     }
 }
 
@@ -493,12 +634,11 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         }
     const int nfull = (it.n_tiles - 1) / NT;  // full blocks before the last block
     const int nv = it.n_tiles - nfull * NT;   // tiles in the last block, 1..NT
-    // after the reduction, lane 16q writes slot slot_of_row(q) of each group:
-    // the kernel ids it writes (-1: not a writer, or an empty slot)
-    int okid[G];
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-        okid[g] = (lane & 15) == 0 ? a.kid[it.k_off + 4 * g + slot_of_row(lane >> 4)] : -1;
+    // the kernel id this lane writes after the reduction (-1: not a writer,
+    // or an empty slot)
+    const int wslot = writer_slot<G>(lane);
+    const int okid = wslot >= 0 ? a.kid[it.k_off + wslot] : -1;
+    const bool hi8 = (lane & 8) != 0;
     const int64_t f_stride = (int64_t)a.nf * a.K;
     for (int r = 0; r < nrows; ++r) {
         RowAcc<G> ra;
@@ -522,7 +662,7 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
         else
             TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(
                 nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra);
-        write_row<G, MPV>(ra, okid, it.inv_O, F0 + r * f_stride);
+        write_row<G, MPV>(ra, okid, it.inv_O, F0 + r * f_stride, hi8);
     }
 }
 
