@@ -9,6 +9,7 @@
 #include <new>
 #include <tuple>
 #include <utility>
+#include <vector>
 
 #include "rocket_internal.h"
 
@@ -16,6 +17,83 @@ namespace rocket {
 
 static int64_t output_length(int64_t L, int64_t len, int64_t dil, int64_t pad) {
     return L + 2 * pad - (len - 1) * dil;
+}
+
+static int popcount64(uint64_t m) { return __builtin_popcountll(m); }
+
+// Multivariate kernel lists: cut into groups of 4 kernels whose channel
+// unions stay small.  Every channel in a group's union costs the group one
+// MFMA chain pass (a kernel that does not read the channel has zero weights
+// there), so the issued work is the sum over groups of |union| x taps x
+// tiles.  Greedy: each group starts from the remaining kernel that reads the
+// most channels and adds, one at a time, the kernel that adds the fewest new
+// channels (ties: the one reading more channels, then list order); then
+// pairwise swaps between groups are applied while they shrink the sum of the
+// two unions.  Deterministic; the swap pass is skipped for lists above 1,024
+// kernels (its cost is quadratic in the group count).
+using KernelSlot = std::pair<int32_t, int32_t>;  // (kernel, first frame tap)
+template <typename MaskOf>
+static std::vector<std::vector<KernelSlot>> group_by_channels(std::vector<KernelSlot> ks,
+                                                              const MaskOf &mask_of) {
+    std::vector<std::vector<KernelSlot>> groups;
+    std::vector<char> used(ks.size(), 0);
+    size_t left = ks.size();
+    while (left > 0) {
+        size_t seed = ks.size();
+        for (size_t i = 0; i < ks.size(); ++i)
+            if (!used[i] && (seed == ks.size() ||
+                             popcount64(mask_of(ks[i].first)) > popcount64(mask_of(ks[seed].first))))
+                seed = i;
+        std::vector<KernelSlot> g{ks[seed]};
+        used[seed] = 1;
+        --left;
+        uint64_t u = mask_of(ks[seed].first);
+        while (g.size() < (size_t)kSlotsPerGroup && left > 0) {
+            size_t best = ks.size();
+            int best_add = 0, best_cnt = 0;
+            for (size_t i = 0; i < ks.size(); ++i) {
+                if (used[i]) continue;
+                const uint64_t m = mask_of(ks[i].first);
+                const int add = popcount64(u | m) - popcount64(u), cnt = popcount64(m);
+                if (best == ks.size() || add < best_add || (add == best_add && cnt > best_cnt)) {
+                    best = i;
+                    best_add = add;
+                    best_cnt = cnt;
+                }
+            }
+            g.push_back(ks[best]);
+            used[best] = 1;
+            --left;
+            u |= mask_of(ks[best].first);
+        }
+        groups.push_back(std::move(g));
+    }
+    if (ks.size() > 1024) return groups;
+    auto uni = [&](const std::vector<KernelSlot> &g) {
+        uint64_t u = 0;
+        for (const KernelSlot &e : g) u |= mask_of(e.first);
+        return popcount64(u);
+    };
+    for (int pass = 0; pass < 4; ++pass) {
+        bool improved = false;
+        for (size_t a = 0; a < groups.size(); ++a)
+            for (size_t b = a + 1; b < groups.size(); ++b) {
+                int base = uni(groups[a]) + uni(groups[b]);
+                for (size_t ia = 0; ia < groups[a].size(); ++ia)
+                    for (size_t ib = 0; ib < groups[b].size(); ++ib) {
+                        std::swap(groups[a][ia], groups[b][ib]);
+                        const int c = uni(groups[a]) + uni(groups[b]);
+                        if (c < base) {
+                            base = c;
+                            improved = true;
+                        } else {
+                            std::swap(groups[a][ia], groups[b][ib]);
+                        }
+                    }
+            }
+        if (!improved) break;
+    }
+    return groups;
 }
 
 rocket_status validate_kernels(const rocket_kernels *k, int32_t L) {
@@ -197,13 +275,19 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
         for (Frame &fr : frames) {
             const int32_t d = fr.d, p = fr.p;
             auto &ks = fr.ks;
-            // multivariate: kernels with similar channel sets next to each
-            // other, so that an item's channel union stays small
-            if (C > 1)
-                std::stable_sort(ks.begin(), ks.end(), [&](const std::pair<int32_t, int32_t> &a,
-                                                           const std::pair<int32_t, int32_t> &b) {
-                    return mask_of(a.first) < mask_of(b.first);
-                });
+            // multivariate: items of one 4-kernel group each, grouped so that
+            // the channel unions stay small (an 8-kernel item would run both
+            // of its groups over the union of all 8 channel sets)
+            std::vector<int32_t> item_sizes;
+            if (C > 1) {
+                std::vector<KernelSlot> flat;
+                for (auto &g : group_by_channels(ks, mask_of)) {
+                    item_sizes.push_back((int32_t)g.size());
+                    flat.insert(flat.end(), g.begin(), g.end());
+                }
+                ks = std::move(flat);
+            }
+            size_t next_item = 0;
             const int eidx = fr.eidx;
             const int ell = kEllValues[eidx];
             // every kernel of a frame list has these outputs
@@ -212,8 +296,9 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             size_t pos = 0;
             while (pos < ks.size()) {
                 const size_t rem = ks.size() - pos;
-                const int G = rem > 4 ? 2 : 1;
-                const size_t take = std::min<size_t>(rem, (size_t)(4 * G));
+                const int G = (C > 1 || rem <= 4) ? 1 : 2;
+                const size_t take = C > 1 ? (size_t)item_sizes[next_item++]
+                                          : std::min<size_t>(rem, (size_t)(4 * G));
                 ItemDesc it;
                 std::memset(&it, 0, sizeof(it));
                 it.variant = eidx * 2 + (G - 1);

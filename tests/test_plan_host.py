@@ -289,3 +289,54 @@ def test_multichannel_generator_matches_oracle():
         b = o.generate_kernels_multi(77, 300, 500, C)
         for key in ("length", "dilation", "padding", "bias", "channel_count", "channel_index", "weights"):
             assert np.array_equal(a[key], b[key]), (C, key)
+
+
+def _multichannel_set(chan_sets, C, L, seed, length=9, dilation=1, padding=0):
+    """A hand-built multivariate set: kernel i reads the channels chan_sets[i]."""
+    rng = np.random.default_rng(seed)
+    K = len(chan_sets)
+    count = np.array([len(s) for s in chan_sets], dtype=np.int32)
+    index = np.zeros((K, C), dtype=np.int32)
+    W = np.zeros((K, C, 11), dtype=np.float32)
+    for i, s in enumerate(chan_sets):
+        index[i, :len(s)] = sorted(s)
+        W[i, :len(s), :length] = rng.standard_normal((len(s), length))
+    return dict(length=np.full(K, length, np.int32), dilation=np.full(K, dilation, np.int32),
+                padding=np.full(K, padding, np.int32), bias=rng.uniform(-1, 1, K).astype(np.float32),
+                weights=W, n_channels=C, channel_count=count, channel_index=index, input_length=L)
+
+
+def test_multichannel_groups_share_channels():
+    """Multivariate buckets are cut into 4-kernel items whose channel unions
+    stay small: eight kernels of one bucket reading {0,1}, {2,3}, {0}, {2},
+    {1}, {3}, {0,1}, {2,3} form two items, each over 2 channels (one item of
+    eight would run both of its groups over all 4 channels)."""
+    sets = [{0, 1}, {2, 3}, {0}, {2}, {1}, {3}, {0, 1}, {2, 3}]
+    L = 40
+    ks = _multichannel_set(sets, 4, L, 5)
+    t = check_tables(ks, L)
+    items = t["items"]
+    assert items.shape[0] == 2
+    assert (items[:, 0] % 2 == 0).all()          # 4-kernel items
+    assert sorted(items[:, 8].tolist()) == [2, 2]  # two channels each
+    unions = []
+    for r in items:
+        chans = set(int(c) for c in t["chan"][r[9]:r[9] + r[8]])
+        kids = [int(x) for x in t["slot_kernel"][r[6]:r[6] + 4] if x >= 0]
+        assert set().union(*(sets[k] for k in kids)) == chans
+        unions.append(frozenset(chans))
+    assert set(unions) == {frozenset({0, 1}), frozenset({2, 3})}
+
+
+def test_multichannel_issued_work():
+    """The multivariate benchmark's kernel set (10,000 kernels, 6 channels,
+    L = 500): MFMA work issued over the channel unions stays within 1.5x of
+    the valid (kernel, channel, tap, output) products."""
+    from paper_2601_17091_amd.workloads import WORKLOADS
+    w = WORKLOADS["multivariate"]
+    ks = rk.generate_kernels_multi(w.kernel_seed, w.n_kernels, w.L, w.channels)
+    items = rk.plan_tables(ks, w.L)["items"]
+    assert (items[:, 0] % 2 == 0).all()
+    valid = (ks["channel_count"].astype(np.int64) * ks["length"] *
+             (w.L + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
+    assert items[:, 7].sum() * 256 < 1.5 * valid
