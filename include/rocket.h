@@ -268,11 +268,13 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  * rocket_plan_tables_free (NULL-safe, idempotent).
  *   items        n_items x item_words (16) int32, one row per work item:
  *                [variant, dilation, padding, outputs O, tiles, w_off,
- *                 k_off, cost, n_ch, ch_off, 0, 0, 0, 0, inv_O (words
- *                 14-15: 1/O as an IEEE double, little-endian)];
+ *                 k_off, cost, n_ch, ch_off, 0, 0, mask_lo, mask_hi,
+ *                 inv_O (words 14-15: 1/O as an IEEE double,
+ *                 little-endian)];
  *                n_ch channels, listed in chan[ch_off .. ch_off + n_ch),
  *                are the union of the channels the item's kernels read
- *                (1 and channel 0 for univariate sets);
+ *                (1 and channel 0 for univariate sets); mask_lo |
+ *                mask_hi << 32 holds the same channels as a bit mask;
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
  *                7/9/11 taps, G kernel groups of 4 slots;
  *                the O outputs are computed in tiles = ceil(O / 64) tiles

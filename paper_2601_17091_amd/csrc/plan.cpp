@@ -312,6 +312,8 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 for (size_t s = 0; s < take; ++s) umask |= mask_of(ks[pos + s].first);
                 it.n_ch = 0;
                 it.ch_off = (int32_t)P.chan.size();
+                it.ch_mask[0] = (uint32_t)umask;
+                it.ch_mask[1] = (uint32_t)(umask >> 32);
                 for (int32_t c = 0; c < C; ++c)
                     if ((umask >> c) & 1u) {
                         P.chan.push_back(c);

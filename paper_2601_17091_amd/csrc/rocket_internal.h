@@ -37,6 +37,9 @@ constexpr int kMaxTilesPerBlock = 8;
 // fall outside the series reads zeros from a margin.
 constexpr int kClampMargin = kTile * kMaxTilesPerBlock;
 
+// The fused kernel runs multichannel items over a 64-bit channel mask.
+static_assert(ROCKET_MAX_CHANNELS <= 64, "channel masks are 64 bits");
+
 // Every output of an item is computed by exactly one lane of one tile; lanes
 // of the last tile past O start from -inf and change no feature.
 constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
@@ -56,7 +59,7 @@ struct alignas(16) ItemDesc {
     int32_t ch_off;    // first entry of the item's channel list
     int32_t t_off;     // MINIROCKET: first threshold, [nq][4] floats
     int32_t nq;        // MINIROCKET: thresholds (features) per slot in this item
-    int32_t reserved[2];
+    uint32_t ch_mask[2];  // multichannel: the item's channels as a bit mask (lo, hi words)
     double inv_O;      // 1 / O rounded to double (exact PPV, see transform.hip)
 };
 static_assert(sizeof(ItemDesc) == 64, "ItemDesc must stay 64 bytes");

@@ -220,7 +220,6 @@ struct FusedArgs {
     int32_t nf;        // features per kernel in F: 2 (PPV, MAX) or 3 (+ MPV); 1 for
                        // MINIROCKET, whose K is then its feature count
     int32_t C;         // channels per series
-    const int32_t *chan;  // item channel lists
     const float *thr;     // MINIROCKET items: per item [nq][4] thresholds
     const ItemDesc *items;
     const float *wpk;
@@ -296,14 +295,24 @@ struct RowAcc {
 
 // Multichannel items (Sec. 3.3): where the item's weights and channel rows
 // are.  w is the lane's first packed weight (slot lane & 3); the weights of
-// channel list entry ci, group g, tap j are at w[((ci*G + g)*ELL + j)*4].
-// The row of channel c sits c*cstride floats after the series' first row.
+// the item's ci-th channel, group g, tap j are at w[((ci*G + g)*ELL + j)*4].
+// The channels are the set bits of mask, in ascending order; the row of
+// channel c sits c*cstride floats after the series' first row.
 struct McCtx {
     const float *w;
-    ConstPtr<int32_t> chan;  // the item's channel list
+    uint64_t mask;
     int n_ch;
     int cstride;
 };
+
+// One channel's A-operand weights of a multichannel item (wp: its first).
+template <int ELL, int G>
+__device__ __forceinline__ void load_channel_weights(const float *wp, float (&wc)[G][ELL]) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int j = 0; j < ELL; ++j) wc[g][j] = wp[(g * ELL + j) * 4];
+}
 
 // The contraction of one block of NT tiles over the taps of one channel:
 // tap j of every tile and kernel group is issued before tap j+1, so the
@@ -377,7 +386,9 @@ __device__ __forceinline__ void block_reduce(const v4f (&acc)[NT][G], RowAcc<G> 
 
 // One block of NT tiles.  Univariate items keep their weights in registers
 // (wa); multichannel items (MC) run the MFMA chains over every channel of
-// their list, reading each channel's weights in turn.  The scheduling
+// their mask, reading each channel's weights in turn: the next channel's
+// weights are loaded while the current channel's MFMAs run, and the channel
+// numbers come from the mask (s_ff1) without a memory access.  The scheduling
 // barriers keep the block's MFMAs in one run and its reduction in another:
 // on gfx950 fp32 MFMA and VALU instructions of a SIMD do not execute at the
 // same time, and a VALU instruction placed between two MFMAs of a wavefront
@@ -390,18 +401,28 @@ __device__ __forceinline__ void tile_block(const Src &src, const float (&wa)[G][
     if constexpr (!MC) {
         tile_mfma<ELL, G, NT, LAST, true>(src, wa, binit, blast, acc);
     } else {
-        float wc[G][ELL];
+        float wc[G][ELL], wn[G][ELL];
+        uint64_t m = mc.mask;
+        int c = (int)__builtin_ctzll(m);
+        m &= m - 1;
+        load_channel_weights<ELL, G>(mc.w, wc);
         for (int ci = 0; ci < mc.n_ch; ++ci) {
-            const float *wp = mc.w + ci * (G * ELL * 4);
-#pragma unroll
-            for (int g = 0; g < G; ++g)
-#pragma unroll
-                for (int j = 0; j < ELL; ++j) wc[g][j] = wp[(g * ELL + j) * 4];
-            const Src s = src.channel(mc.chan[ci] * mc.cstride);
+            int cn = 0;
+            if (ci + 1 < mc.n_ch) {
+                load_channel_weights<ELL, G>(mc.w + (ci + 1) * (G * ELL * 4), wn);
+                cn = (int)__builtin_ctzll(m);
+                m &= m - 1;
+            }
+            const Src s = src.channel(c * mc.cstride);
             if (ci == 0)
                 tile_mfma<ELL, G, NT, LAST, true>(s, wc, binit, blast, acc);
             else
                 tile_mfma<ELL, G, NT, LAST, false>(s, wc, binit, blast, acc);
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int j = 0; j < ELL; ++j) wc[g][j] = wn[g][j];
+            c = cn;
         }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -611,8 +632,9 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
             for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
     }
     McCtx mc{};
-    if constexpr (MC) mc = McCtx{a.wpk + it.w_off + (lane & 3), as_const(a.chan) + it.ch_off, it.n_ch,
-                                 a.row_stride};
+    if constexpr (MC)
+        mc = McCtx{a.wpk + it.w_off + (lane & 3), ((uint64_t)it.ch_mask[1] << 32) | it.ch_mask[0], it.n_ch,
+                   a.row_stride};
     const int row_pitch = a.C * a.row_stride;  // floats per staged series (LDS offsets fit 32 bits)
     // C operand of the first tap: the bias of block row v (kernel slot v),
     // and in the last tile of a series -inf on the lanes past the last
@@ -680,6 +702,8 @@ __device__ __forceinline__ ItemDesc load_item(ConstPtr<ItemDesc> p) {
     it.ch_off = p->ch_off;
     it.t_off = p->t_off;
     it.nq = p->nq;
+    it.ch_mask[0] = p->ch_mask[0];
+    it.ch_mask[1] = p->ch_mask[1];
     it.inv_O = p->inv_O;
     return it;
 }
@@ -761,13 +785,22 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
     float *F0 = a.F + w.grow * (int64_t)a.nf * a.K;
     const float *rows0 = smem + a.halo_lo;
     const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
-    switch (w.variant) {
-        case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 1: run_items<7, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+    if constexpr (MC) {
+        // multichannel plans hold 4-kernel items only (variants 0, 2, 4)
+        switch (w.variant) {
+            case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            default: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        }
+    } else {
+        switch (w.variant) {
+            case 0: run_items<7, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 1: run_items<7, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        }
     }
 }
 
@@ -1064,7 +1097,6 @@ struct rocket_plan {
     int32_t *d_kid = nullptr;
     int32_t *d_order = nullptr;
     int32_t *d_split_begin = nullptr;
-    int32_t *d_chan = nullptr;
     float *d_thr = nullptr;
     // the kernel set as given, for the direct kernel
     int32_t max_len = 0;
@@ -1079,7 +1111,7 @@ struct rocket_plan {
 
 static void plan_free_device(rocket_plan *p) {
     void *ptrs[] = {p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
-                    p->d_split_begin, p->d_chan, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
+                    p->d_split_begin, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
     for (void *q : ptrs)
         if (q) (void)hipFree(q);
@@ -1131,7 +1163,6 @@ static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
     if (e == hipSuccess) e = upload(p->host.kid, &p->d_kid);
     if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
     if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
-    if (e == hipSuccess) e = upload(p->host.chan, &p->d_chan);
     if (e == hipSuccess) e = upload(p->host.thr, &p->d_thr);
     if (e == hipSuccess && lds > 64 * 1024) {
         for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
@@ -1301,7 +1332,6 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.nf = p->minirocket ? 1 : (p->mpv ? 3 : 2);
     a.thr = p->d_thr;
     a.C = p->C;
-    a.chan = p->d_chan;
     a.items = p->d_items;
     a.wpk = p->d_wpk;
     a.bias = p->d_bias;

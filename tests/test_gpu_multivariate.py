@@ -122,3 +122,15 @@ def test_multichannel_host_to_host(env):
     Fh = torch.empty((11, 2 * 800), dtype=torch.float32, pin_memory=True)
     p.transform_host(Xh, Fh, batch_rows=4)
     assert torch.equal(Fh, want)
+
+
+def test_most_channels(env, oracle):
+    """The largest channel count the ABI takes (32): the item channel masks
+    reach their top channel."""
+    torch, rk = env
+    C, L = 32, 48
+    ks = rk.generate_kernels_multi(96, 400, L, C)
+    assert ks["channel_index"].max() == C - 1
+    X = _series(96, 3, C, L)
+    _log("C=%d" % C)
+    assert_parity(run(env, X, ks, "fused"), oracle.transform(X, ks), "mc-C32")

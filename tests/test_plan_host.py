@@ -324,6 +324,9 @@ def test_multichannel_groups_share_channels():
         chans = set(int(c) for c in t["chan"][r[9]:r[9] + r[8]])
         kids = [int(x) for x in t["slot_kernel"][r[6]:r[6] + 4] if x >= 0]
         assert set().union(*(sets[k] for k in kids)) == chans
+        # the channel mask the fused kernel iterates holds the same channels
+        mask = int(r[12]) | (int(r[13]) << 32)
+        assert mask == sum(1 << c for c in chans)
         unions.append(frozenset(chans))
     assert set(unions) == {frozenset({0, 1}), frozenset({2, 3})}
 
