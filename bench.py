@@ -237,6 +237,12 @@ def main():
             parity["mpv_max_excess_over_rule"] = float(max(0.0, excess[same].max()))
         log("parity %s" % parity)
 
+    # the layout the timed calls ran: series-lane for short univariate series
+    # in calls of at least 4,096 series (then a permutation kernel writes F)
+    series_path = bool(info.get("series_lane")) and batch >= 4096
+    path = "direct" if info["direct"] else ("series-lane-mfma" if series_path else "fused-mfma")
+    kernel_name = ("rocket_direct_kernel" if info["direct"] else
+                   ("rocket_series_kernel + rocket_slot_permute_kernel" if series_path else "rocket_fused_kernel"))
     out = {
         "metric": "series*kernels/s (ROCKET transform, fp32, 1 MI355X)",
         "value": pairs_per_s,
@@ -253,12 +259,12 @@ def main():
         "config": {"workload": w.name, "n_series": w.n, "series_length": w.L, "channels": w.channels,
                    "n_kernels": w.n_kernels, "features": K2, "f_batch_rows": batch,
                    "kernel_seed": w.kernel_seed, "data_seed": w.data_seed,
-                   "path": "direct" if info["direct"] else "fused-mfma"},
+                   "path": path},
         "pct_fp32_peak": 100.0 * achieved / PEAK_FP32_TFLOPS,
         "pct_fp32_fma_nopack_peak": 100.0 * achieved / PEAK_FP32_FMA_NOPACK,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS, "traffic": traffic,
-                     "kernel": "rocket_direct_kernel" if info["direct"] else "rocket_fused_kernel",
+                     "kernel": kernel_name,
                      "launches_per_step": launches, "launch_ms": per_launch_ms,
                      "algorithmic_flops_per_launch": flops_per_pass / launches,
                      "valid_fma_per_series": valid_per_row,

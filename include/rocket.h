@@ -155,6 +155,8 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
 #define ROCKET_PLAN_DIRECT 1u  /* use the plain one-wavefront-per-pair kernel */
 #define ROCKET_PLAN_CLAMPED 2u /* fused kernel with the long-series row layout */
 #define ROCKET_PLAN_MPV 4u     /* a third feature per kernel: mean of positive values */
+#define ROCKET_PLAN_TILED 8u   /* fused kernel with position tiles, also for short series */
+#define ROCKET_PLAN_SERIES 16u /* series-lane layout for every call (short univariate series) */
 
 /*
  * rocket_plan_create with flags.  ROCKET_PLAN_DIRECT selects the plain
@@ -165,8 +167,21 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
  * forces the layout the default plan picks for long series: rows staged with
  * 512 zeros on each side, and the series offset of each block of tiles
  * clamped into those margins on the scalar unit (same results).
- * ROCKET_PLAN_DIRECT together with ROCKET_PLAN_CLAMPED is
- * ROCKET_ERR_INVALID_ARG.
+ * Short univariate series (L <= 128): calls with at least 4,096 series run
+ * by default in the series-lane layout.  The 64 lanes of a wavefront take 64
+ * series, staged position-major in LDS, so every MFMA computes one output
+ * position for 4 kernels x 64 series and each lane reduces its own series;
+ * the features go through a plan-owned buffer in slot order (allocated on
+ * first use, at most 1 GiB, freed with the plan) and a permutation kernel
+ * writes F.  Same results as the position-tiled layout, which serves calls
+ * with fewer series.  Transforms of one plan on different streams take turns
+ * on that buffer (each waits for the previous one on the device).
+ * ROCKET_PLAN_TILED keeps every call in the position-tiled layout;
+ * ROCKET_PLAN_SERIES runs every call in the series-lane layout
+ * (ROCKET_ERR_INVALID_ARG for multivariate sets or L > 128).
+ * ROCKET_PLAN_DIRECT together with ROCKET_PLAN_CLAMPED or ROCKET_PLAN_TILED,
+ * and ROCKET_PLAN_SERIES together with any of ROCKET_PLAN_DIRECT,
+ * ROCKET_PLAN_CLAMPED and ROCKET_PLAN_TILED, are ROCKET_ERR_INVALID_ARG.
  * ROCKET_PLAN_MPV adds a third feature per kernel, the mean of the positive
  * values (MPV; the CUROCKET paper, Sec. 5, names it as a feature that does
  * not depend on time positions and so fuses into the same pass):
@@ -229,7 +244,9 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  * Plan facts for benchmarks and tests (host only).
  *   n_items      number of work items (groups of kernels sharing one bucket)
  *   n_buckets    number of distinct (length, dilation, padding) buckets
- *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks)
+ *   mfma_per_row MFMA instructions one series costs (4x4x1 fp32 blocks;
+ *                in the series-lane layout one MFMA serves 64 series, and
+ *                this is the rounded share of one series)
  *   lds_bytes    LDS one workgroup uses (0 for the direct kernel)
  *   direct       1 if the plan runs the direct kernel, else 0
  *   clamped      1 if the fused kernel stages rows with 512 zeros on each
@@ -242,6 +259,10 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *   rows_per_block       series staged per workgroup (0 for the direct kernel)
  *   n_features   columns of F
  *   minirocket   1 for a MINIROCKET plan, else 0
+ *   series_lane  1 if the plan runs the series-lane layout (for calls of at
+ *                least 4,096 series, or every call with ROCKET_PLAN_SERIES);
+ *                lds_bytes, rows_per_block and mfma_per_row then describe
+ *                that layout
  */
 typedef struct {
     int64_t n_items;
@@ -254,7 +275,7 @@ typedef struct {
     int32_t rows_per_block;
     int64_t n_features;
     int32_t minirocket;
-    int32_t reserved;
+    int32_t series_lane;
 } rocket_plan_facts;
 
 /* Fill *out with the plan's facts.  Errors: ROCKET_ERR_INVALID_ARG if p or

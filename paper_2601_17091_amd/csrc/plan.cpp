@@ -352,6 +352,7 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                 }
                 P.items.push_back(it);
                 P.mfma_per_row += n_tiles * ell * G * it.n_ch;
+                P.series_mfma_64 += O * ell * G;
                 pos += take;
             }
         }

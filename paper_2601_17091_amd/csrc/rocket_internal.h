@@ -92,6 +92,7 @@ struct HostPlan {
     int32_t n_channels = 1;  // channels per series
     int64_t n_buckets = 0;
     int64_t mfma_per_row = 0;
+    int64_t series_mfma_64 = 0;  // MFMAs for 64 series in the series-lane layout (O x taps x G)
     std::vector<ItemDesc> items;
     std::vector<float> wpk;       // packed A-operand weights
     std::vector<float> bias;      // per slot

@@ -33,6 +33,7 @@
 #include <climits>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "rocket_internal.h"
@@ -235,6 +236,8 @@ struct FusedArgs {
     int32_t row_stride;
     int32_t tail_pad;        // zero floats staged after the last row
     int32_t rows_per_block;  // series staged together in one workgroup's LDS
+    float *S;                // series-lane layout: features in slot order (see below)
+    int64_t s_rows;          // rows one slot column of S holds
 };
 
 // DPP controls (GFX9 encoding)
@@ -735,13 +738,9 @@ struct GroupWork {
 // Workgroup = (variant, row group, split).  Workgroup b runs on XCD b % 8.
 // Every XCD takes its own share of the row groups and walks them variant by
 // variant, so all XCDs get the same mix of work while the CUs of an XCD run
-// one code variant at a time.  Stages the group's series (every channel)
-// with their zero margins into smem, coalesced (channel c of row r at
-// (r*C + c)*row_stride), and the tail pad after them.  Returns false when the
-// workgroup has nothing to do (uniformly for the whole workgroup).
-template <int BLOCK>
-__device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int *next_item,
-                                            GroupWork &w) {
+// one code variant at a time.  Returns false when the workgroup has nothing
+// to do (uniformly for the whole workgroup).
+__device__ __forceinline__ bool group_work(const FusedArgs &a, GroupWork &w) {
     const int64_t b = blockIdx.x;
     const int xcd = (int)(b % kXcds);
     const int64_t local = b / kXcds;
@@ -757,6 +756,16 @@ __device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int
     if (w.cnt_items == 0 || first >= a.n_rows) return false;
     w.nrows = (int)min((int64_t)a.rows_per_block, a.n_rows - first);
     w.grow = a.row0 + first;
+    return true;
+}
+
+// Stages the group's series (every channel) with their zero margins into
+// smem, coalesced (channel c of row r at (r*C + c)*row_stride), and the tail
+// pad after them.
+template <int BLOCK>
+__device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int *next_item,
+                                            GroupWork &w) {
+    if (!group_work(a, w)) return false;
     for (int rc = 0; rc < w.nrows * a.C; ++rc) {
         const float *x = a.X + ((w.grow * a.C) + rc) * (int64_t)a.L;
         float *dst = smem + rc * a.row_stride;
@@ -800,6 +809,265 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
             case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
             case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
             default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Series-lane layout (short univariate series).  The 64 lanes of a
+// wavefront take 64 series, and LDS holds the workgroup's 64 series
+// position-major: the values of all 64 series at one position are 64
+// consecutive floats, so a tap's read is again one ds_read_addtid_b32 per
+// position.  One MFMA then computes one output position for 4 kernels x 64
+// series, and a block runs NT consecutive positions.  Every lane keeps the
+// count, the max (and the MPV sum) of its own series, so no cross-lane
+// reduction is needed: for short series the per-series reductions and
+// writes of the position-tiled layout cost more than the dot products.
+// ---------------------------------------------------------------------------
+
+constexpr int kSeriesLanes = rocket::kWave;              // series per workgroup
+constexpr int kSeriesMargin = rocket::kMaxTilesPerBlock;  // zero positions on each side
+constexpr int kSeriesMaxL = 128;                           // longest series it takes
+constexpr int64_t kSeriesMinRows = 4096;  // fewer series per call: too few workgroups, use tiles
+
+// Stages the group's series: position m of series r at
+// smem[(m + kSeriesMargin) * 64 + r], with zeros in the margins and in the
+// lanes past the group's last series.  Consecutive threads write
+// consecutive LDS words (no bank conflicts); their global reads are a
+// series apart and hit the same cache lines across the loop.
+template <int BLOCK>
+__device__ __forceinline__ bool stage_series(const FusedArgs &a, float *smem, int *next_item,
+                                             GroupWork &w) {
+    if (!group_work(a, w)) return false;
+    const int total = (a.L + 2 * kSeriesMargin) * kSeriesLanes;
+    const float *x = a.X + w.grow * (int64_t)a.L;
+    for (int e = threadIdx.x; e < total; e += BLOCK) {
+        const int r = e & (kSeriesLanes - 1);
+        const int m = e / kSeriesLanes - kSeriesMargin;
+        smem[e] = (r < w.nrows && m >= 0 && m < a.L) ? x[(int64_t)r * a.L + m] : 0.0f;
+    }
+    if (threadIdx.x == 0) *next_item = 0;
+    __syncthreads();
+    return true;
+}
+
+// Series-lane reads.  pos0 is the LDS byte address of position 0 (its 64
+// series); the position of the block's first output under tap j is clamped
+// into [-kSeriesMargin, L] on the scalar unit, as for ClampedTiles: a block
+// whose positions all lie outside the series reads zeros from a margin, a
+// block that overlaps it is not moved.
+struct SeriesTiles {
+    uint32_t pos0;
+    int b0;  // position under tap 0 of the block's first output
+    int d;
+    int L;
+    __device__ __forceinline__ uint32_t m0(int j) const {
+        const int b = min(max(b0 + j * d, -kSeriesMargin), L);
+        return pos0 + 256u * (uint32_t)b;
+    }
+};
+
+// Per-lane (per-series) accumulators of one work item.
+template <int G>
+struct SeriesAcc {
+    v4f mx[G];
+    uint32_t cnt[G][4];
+    v4f ps[G];
+};
+
+// [y > 0] as 0 or 1.  For a float that is not a NaN the bits read as a
+// signed integer are positive exactly when y > 0 (+0 reads 0; -0 and the
+// negative values read negative), so med3(bits, 0, 1) is the indicator.
+__device__ __forceinline__ uint32_t positive01(float y) {
+    uint32_t r;
+    asm("v_med3_i32 %0, %1, 0, 1" : "=v"(r) : "v"(y));
+    return r;
+}
+
+// Fold NT positions of finished dot products into the lanes' accumulators:
+// the counts add the indicators two at a time, MAX folds pairs with v_max3.
+template <int G, int NT, bool MPV>
+__device__ __forceinline__ void series_reduce(const v4f (&acc)[NT][G], SeriesAcc<G> &sa) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            uint32_t c = sa.cnt[g][v];
+#pragma unroll
+            for (int u = 0; u < NT; u += 2) {
+                if (u + 1 < NT)
+                    c += positive01(acc[u][g][v]) + positive01(acc[u + 1][g][v]);
+                else
+                    c += positive01(acc[u][g][v]);
+            }
+            sa.cnt[g][v] = c;
+        }
+    if (MPV) {
+#pragma unroll
+        for (int u = 0; u < NT; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) sa.ps[g][v] += fmaxf(acc[u][g][v], 0.0f);
+    }
+#pragma unroll
+    for (int u = 0; u + 1 < NT; u += 2)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                sa.mx[g][v] = fmaxf(fmaxf(sa.mx[g][v], acc[u][g][v]), acc[u + 1][g][v]);
+    if (NT % 2 == 1) {
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) sa.mx[g][v] = fmaxf(sa.mx[g][v], acc[NT - 1][g][v]);
+    }
+}
+
+// NT consecutive output positions of one item for the 64 series.
+template <int ELL, int G, int NT, bool MPV>
+__device__ __forceinline__ void series_block(const SeriesTiles &src, const float (&wa)[G][ELL],
+                                             const v4f (&binit)[G], SeriesAcc<G> &sa) {
+    v4f acc[NT][G];
+    tile_mfma<ELL, G, NT, false, true>(src, wa, binit, binit, acc);
+    __builtin_amdgcn_sched_barrier(0);
+    series_reduce<G, NT, MPV>(acc, sa);
+}
+
+// The last positions of an item, nv (1..N) of them: a code copy per count.
+template <int ELL, int G, int N, bool MPV>
+struct SeriesTail {
+    __device__ __forceinline__ static void run(int nv, const SeriesTiles &src, const float (&wa)[G][ELL],
+                                               const v4f (&binit)[G], SeriesAcc<G> &sa) {
+        if (nv == N)
+            series_block<ELL, G, N, MPV>(src, wa, binit, sa);
+        else
+            SeriesTail<ELL, G, N - 1, MPV>::run(nv, src, wa, binit, sa);
+    }
+};
+template <int ELL, int G, bool MPV>
+struct SeriesTail<ELL, G, 0, MPV> {
+    __device__ __forceinline__ static void run(int, const SeriesTiles &, const float (&)[G][ELL],
+                                               const v4f (&)[G], SeriesAcc<G> &) {}
+};
+
+// One work item over the group's 64 series: all O positions in blocks of
+// NT, then each lane writes the features of its series for the item's
+// kernels.
+template <int ELL, int G, bool MPV>
+__device__ __forceinline__ void run_series_item(const ItemDesc &it, uint32_t pos0, int nrows,
+                                                const FusedArgs &a, int64_t srow0, int lane) {
+    constexpr int NT = rocket::kTilesPerBlock[G - 1];
+    float wa[G][ELL];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int j = 0; j < ELL; ++j) wa[g][j] = a.wpk[it.w_off + (g * ELL + j) * 4 + (lane & 3)];
+    // C operand of the first tap: the bias of block row v (kernel slot v),
+    // the same on every lane (series)
+    v4f binit[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float b = as_const(a.bias)[it.k_off + 4 * g + v];
+            float bv;
+            asm volatile("v_mov_b32 %0, %1" : "=v"(bv) : "s"(b));
+            binit[g][v] = bv;
+        }
+    SeriesAcc<G> sa;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        v2f lo, hi;
+        asm volatile("v_mov_b64 %0, %2\n\tv_mov_b64 %1, %2" : "=v"(lo), "=v"(hi) : "s"(kNegInfPair));
+        sa.mx[g] = v4f{lo[0], lo[1], hi[0], hi[1]};
+        if (MPV) sa.ps[g] = v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sa.cnt[g][v] = 0;
+    }
+    const int nfull = it.O / NT;          // full blocks
+    const int nv = it.O - nfull * NT;     // positions in the last block, 0..NT-1
+    for (int blk = 0; blk < nfull; ++blk)
+        series_block<ELL, G, NT, MPV>(SeriesTiles{pos0, blk * NT - it.p, it.d, a.L}, wa, binit, sa);
+    if (nv > 0)
+        SeriesTail<ELL, G, NT - 1, MPV>::run(nv, SeriesTiles{pos0, nfull * NT - it.p, it.d, a.L}, wa,
+                                             binit, sa);
+    // features into the slot-ordered buffer: slot s of series r (of this
+    // launch) at S[(s * s_rows + r) * nf], so the 64 lanes of a slot write
+    // 64 * nf consecutive floats
+    if (lane < nrows) {
+        float *Srow = a.S + (srow0 + lane) * (int64_t)a.nf;
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int slot = it.k_off + 4 * g + v;
+                if (as_const(a.kid)[slot] >= 0)
+                    write_features<MPV>(sa.cnt[g][v], sa.mx[g][v], sa.ps[g][v], 0, it.inv_O,
+                                        Srow + slot * a.s_rows * (int64_t)a.nf);
+            }
+    }
+}
+
+template <int ELL, int G, bool MPV>
+__device__ __forceinline__ void run_series_items(int *next_item, int beg, int cnt_items, uint32_t pos0,
+                                                 int nrows, const FusedArgs &a, int64_t srow0, int lane) {
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
+        run_series_item<ELL, G, MPV>(it, pos0, nrows, a, srow0, lane);
+    }
+}
+
+// Workgroup = (variant, group of 64 series, split), mapped as for the fused
+// kernel; each wavefront takes items from the workgroup's counter.
+template <bool MPV>
+__global__ __launch_bounds__(kBlock) void rocket_series_kernel(FusedArgs a) {
+    extern __shared__ float smem[];
+    __shared__ int next_item;
+    GroupWork w;
+    if (!stage_series<kBlock>(a, smem, &next_item, w)) return;
+    const int lane = threadIdx.x & (rocket::kWave - 1);
+    const int64_t F0 = w.grow - a.row0;  // first series of the group in S
+    uint32_t pos0 = lds_addr(smem + kSeriesMargin * kSeriesLanes);
+    asm volatile("" : "+s"(pos0));  // computed once (not again in every block)
+    const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
+    switch (w.variant) {
+        case 0: run_series_items<7, 1, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+        case 1: run_series_items<7, 2, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+        case 2: run_series_items<9, 1, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+        case 3: run_series_items<9, 2, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+        case 4: run_series_items<11, 1, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+        default: run_series_items<11, 2, MPV>(&next_item, beg, cnt, pos0, nr, a, F0, lane); break;
+    }
+}
+
+// F rows in the original kernel order from the slot-ordered buffer: a
+// workgroup of 4 wavefronts takes 64 kernels x 64 series; lane l moves
+// kernel k0 + l, so each series' 64 kernels are written as 64 * nf
+// consecutive floats, and each lane reads its slot column downward (the
+// column's cache lines serve the following series).
+template <int NF>
+__global__ __launch_bounds__(kBlock) void rocket_slot_permute_kernel(const float *S, int64_t s_rows,
+                                                                     const int32_t *slot_of, int32_t K,
+                                                                     int64_t n_rows, float *F) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t k = (int64_t)blockIdx.x * 64 + lane;
+    const int64_t r0 = (int64_t)blockIdx.y * 64;
+    if (k >= K) return;
+    const float *src = S + (int64_t)slot_of[k] * s_rows * NF;
+    for (int64_t r = r0 + wave; r < min(r0 + 64, n_rows); r += 4) {
+        const float *a = src + r * NF;
+        float *b = F + r * (int64_t)K * NF + k * NF;
+        if constexpr (NF == 2) {
+            *reinterpret_cast<float2 *>(b) = *reinterpret_cast<const float2 *>(a);
+        } else {
+#pragma unroll
+            for (int f = 0; f < NF; ++f) b[f] = a[f];
         }
     }
 }
@@ -1076,12 +1344,27 @@ static const void *mr_fn(int sel) {
     return fns[sel];
 }
 
+static const void *series_fn(bool mpv) {
+    return mpv ? (const void *)rocket_series_kernel<true> : (const void *)rocket_series_kernel<false>;
+}
+
 struct rocket_plan {
     rocket::HostPlan host;
     int device = 0;
     int n_cu = 0;
     bool direct = false;
     bool clamp = false;      // rows staged with kClampMargin zeros on each side, tap offsets clamped
+    bool series = false;     // series-lane layout available (short univariate series)
+    int64_t series_min_rows = 0;  // calls with at least this many series use it
+    int64_t series_lds = 0;       // its LDS per workgroup
+    int32_t *d_slot_of = nullptr;  // series-lane layout: the slot of each kernel
+    // series-lane layout: the slot-ordered feature buffer, allocated on first
+    // use and grown as needed; transforms on different streams take turns on
+    // it (each waits for the previous user's event)
+    mutable std::mutex scratch_mu;
+    mutable float *d_scratch = nullptr;
+    mutable size_t scratch_bytes = 0;
+    mutable hipEvent_t scratch_done = nullptr;
     bool mpv = false;        // third feature per kernel: mean of positive values
     bool minirocket = false; // MINIROCKET plan: F [n, n_features], PPV only
     int64_t f_cols = 0;      // columns of F
@@ -1110,7 +1393,8 @@ struct rocket_plan {
 };
 
 static void plan_free_device(rocket_plan *p) {
-    void *ptrs[] = {p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
+    if (p->scratch_done) (void)hipEventDestroy(p->scratch_done);
+    void *ptrs[] = {p->d_scratch, p->d_slot_of, p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
                     p->d_split_begin, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
     for (void *q : ptrs)
@@ -1177,8 +1461,11 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
                                                rocket_plan **out) {
     if (!out) return ROCKET_ERR_INVALID_ARG;
     *out = nullptr;
-    if ((flags & ~(ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED | ROCKET_PLAN_MPV)) ||
-        ((flags & ROCKET_PLAN_DIRECT) && (flags & ROCKET_PLAN_CLAMPED)))
+    if ((flags & ~(ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED | ROCKET_PLAN_MPV | ROCKET_PLAN_TILED |
+                   ROCKET_PLAN_SERIES)) ||
+        ((flags & ROCKET_PLAN_DIRECT) && (flags & (ROCKET_PLAN_CLAMPED | ROCKET_PLAN_TILED))) ||
+        ((flags & ROCKET_PLAN_SERIES) &&
+         (flags & (ROCKET_PLAN_DIRECT | ROCKET_PLAN_CLAMPED | ROCKET_PLAN_TILED))))
         return ROCKET_ERR_INVALID_ARG;
     rocket_status st = rocket::validate_kernels(k, L);
     if (st != ROCKET_OK) return st;
@@ -1202,8 +1489,35 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     p->f_cols = (int64_t)(p->mpv ? 3 : 2) * k->n_kernels;
     int64_t lds = 0;
     p->direct = (flags & ROCKET_PLAN_DIRECT) != 0;
+    // short univariate series: the series-lane layout for calls with many
+    // series (ROCKET_PLAN_SERIES: for every call), unless a position-tiled
+    // layout is asked for; the position-tiled layout serves the rest
+    const bool want_series = (flags & ROCKET_PLAN_SERIES) != 0;
+    if (!p->direct && !(flags & (ROCKET_PLAN_CLAMPED | ROCKET_PLAN_TILED)) && p->C == 1 && L <= kSeriesMaxL) {
+        p->series_lds = (int64_t)(L + 2 * kSeriesMargin) * kSeriesLanes * (int64_t)sizeof(float);
+        if (p->series_lds <= (int64_t)prop.sharedMemPerBlock) {
+            p->series = true;
+            p->series_min_rows = want_series ? 0 : kSeriesMinRows;
+        }
+    }
+    if (want_series && !p->series) {
+        delete p;
+        return ROCKET_ERR_INVALID_ARG;
+    }
     if (!p->direct && !choose_layout(p, (flags & ROCKET_PLAN_CLAMPED) != 0, prop, &lds)) p->direct = true;
     p->lds_bytes = p->direct ? 0 : lds;
+    if (p->series) {
+        std::vector<int32_t> slot_of((size_t)k->n_kernels, -1);
+        for (size_t q = 0; q < p->host.kid.size(); ++q)
+            if (p->host.kid[q] >= 0) slot_of[(size_t)p->host.kid[q]] = (int32_t)q;
+        if (std::find(slot_of.begin(), slot_of.end(), -1) != slot_of.end()) {  // every kernel has a slot
+            plan_free_device(p);
+            delete p;
+            return ROCKET_ERR_INTERNAL;
+        }
+        e = upload(slot_of, &p->d_slot_of);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->scratch_done, hipEventDisableTiming);
+    }
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
     if (e == hipSuccess) e = upload_raw(k->length, (size_t)K, &p->d_len);
@@ -1279,15 +1593,18 @@ extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_fact
     if (!p || !out) return ROCKET_ERR_INVALID_ARG;
     out->n_items = (int64_t)p->host.items.size();
     out->n_buckets = p->host.n_buckets;
-    out->mfma_per_row = p->host.mfma_per_row;
-    out->lds_bytes = p->lds_bytes;
+    // series-lane plans: one MFMA serves 64 series, so a series costs
+    // (positions x taps x groups) / 64 of them
+    out->mfma_per_row = p->series ? (p->host.series_mfma_64 + kSeriesLanes / 2) / kSeriesLanes
+                                  : p->host.mfma_per_row;
+    out->lds_bytes = p->series ? p->series_lds : p->lds_bytes;
     out->direct = p->direct ? 1 : 0;
     out->clamped = p->clamp ? 1 : 0;
     out->features_per_kernel = p->minirocket ? 0 : (p->mpv ? 3 : 2);
     out->n_features = p->f_cols;
     out->minirocket = p->minirocket ? 1 : 0;
-    out->reserved = 0;
-    out->rows_per_block = p->direct ? 0 : p->rows_per_block;
+    out->series_lane = p->series ? 1 : 0;
+    out->rows_per_block = p->direct ? 0 : (p->series ? kSeriesLanes : p->rows_per_block);
     return ROCKET_OK;
 }
 
@@ -1311,13 +1628,16 @@ static rocket_status launch_direct(const rocket_plan *p, const float *X, int64_t
     return ROCKET_OK;
 }
 
-static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t n, float *F,
-                                  hipStream_t s) {
+// The workgroup kernels (fused, MINIROCKET, series-lane) over n rows: F
+// receives the features, or, for the series-lane kernel, S (s_rows rows per
+// slot column).
+static rocket_status launch_groups(const rocket_plan *p, bool series, const float *X, int64_t n, float *F,
+                                   float *S, int64_t s_rows, hipStream_t s) {
     // enough workgroups to fill the chip several times over: split the work
     // items of a series across workgroups when there are few series
     const int64_t target = 8 * (int64_t)std::max(p->n_cu, 1);
     const int64_t row_bytes = (int64_t)p->row_stride * (int64_t)sizeof(float);  // one channel
-    const int R = p->rows_per_block;
+    const int R = series ? kSeriesLanes : p->rows_per_block;
     const int64_t groups = (n + R - 1) / R;
     int li = 0;
     while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target) ++li;
@@ -1348,6 +1668,8 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
     a.row_stride = p->row_stride;
     a.tail_pad = p->tail_pad;
     a.rows_per_block = R;
+    a.S = S;
+    a.s_rows = s_rows;
     const int64_t max_rows =
         ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1)) / kXcds - 1) * kXcds * R;
     for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
@@ -1356,10 +1678,10 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         const int64_t groups_now = (a.n_rows + R - 1) / R;
         a.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
         const unsigned nb = (unsigned)(kXcds * a.groups_per_xcd * nsplit * a.n_variants);
-        const size_t lds = (size_t)p->lds_bytes;
-        const bool big = row_bytes * p->C > kBigLds;
+        const size_t lds = (size_t)(series ? p->series_lds : p->lds_bytes);
+        const bool big = !series && row_bytes * p->C > kBigLds;
         const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
-        const void *fn = p->minirocket ? mr_fn(sel & 3) : fused_fn(sel);
+        const void *fn = series ? series_fn(p->mpv) : (p->minirocket ? mr_fn(sel & 3) : fused_fn(sel));
         void *args[] = {&a};
         if (hipLaunchKernel(fn, dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) !=
             hipSuccess)
@@ -1367,6 +1689,60 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
     }
     return ROCKET_OK;
+}
+
+// Series-lane layout: the rows go in chunks; for each chunk the series
+// kernel writes the features in slot order into the plan's scratch buffer
+// (each slot's features of 64 consecutive series are contiguous), and the
+// permutation kernel writes the chunk's F rows in the original kernel order,
+// 64 kernels (64 * nf floats) at a time.  The scatter of single features
+// over F rows would otherwise cost more than the dot products of short
+// series.  The scratch holds at most 1 GiB (chunks of up to 8,192 rows).
+static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                   hipStream_t s) {
+    const int64_t K = p->host.n_kernels;
+    const int64_t n_slots = (int64_t)p->host.kid.size();
+    const int nf = p->mpv ? 3 : 2;
+    const int64_t slot_row_bytes = n_slots * nf * (int64_t)sizeof(float);
+    int64_t chunk = ((int64_t)1 << 30) / std::max<int64_t>(slot_row_bytes, 1);
+    chunk = std::max<int64_t>(kSeriesLanes, std::min<int64_t>(8192, chunk / kSeriesLanes * kSeriesLanes));
+    chunk = std::min(chunk, (n + kSeriesLanes - 1) / kSeriesLanes * kSeriesLanes);
+    const size_t need = (size_t)(chunk * slot_row_bytes);
+    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    if (p->scratch_bytes < need) {
+        // hipFree waits for the work that still uses the old buffer
+        if (p->d_scratch && hipFree(p->d_scratch) != hipSuccess) return ROCKET_ERR_HIP;
+        p->d_scratch = nullptr;
+        p->scratch_bytes = 0;
+        if (hipMalloc(&p->d_scratch, need) != hipSuccess) return ROCKET_ERR_OOM;
+        p->scratch_bytes = need;
+    }
+    // the previous transform of this plan (on any stream) is done with it
+    if (hipStreamWaitEvent(s, p->scratch_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
+    for (int64_t r0 = 0; r0 < n; r0 += chunk) {
+        const int64_t m = std::min(chunk, n - r0);
+        const rocket_status st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, p->d_scratch, chunk, s);
+        if (st != ROCKET_OK) return st;
+        const dim3 grid((unsigned)((K + 63) / 64), (unsigned)((m + 63) / 64));
+        const void *pf = nf == 3 ? (const void *)rocket_slot_permute_kernel<3>
+                                 : (const void *)rocket_slot_permute_kernel<2>;
+        const float *S = p->d_scratch;
+        const int32_t *slot_of = p->d_slot_of;
+        int32_t K32 = (int32_t)K;
+        int64_t s_rows = chunk;
+        float *Fc = F + r0 * K * nf;
+        void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&m, &Fc};
+        if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, s) != hipSuccess) return ROCKET_ERR_HIP;
+        if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+    }
+    if (hipEventRecord(p->scratch_done, s) != hipSuccess) return ROCKET_ERR_HIP;
+    return ROCKET_OK;
+}
+
+static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                  hipStream_t s) {
+    return (p->series && n >= p->series_min_rows) ? launch_series(p, X, n, F, s)
+                                                  : launch_groups(p, false, X, n, F, nullptr, 0, s);
 }
 
 extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,

@@ -25,6 +25,8 @@ ROCKET_PLAN_DEFAULT = 0
 ROCKET_PLAN_DIRECT = 1
 ROCKET_PLAN_CLAMPED = 2
 ROCKET_PLAN_MPV = 4
+ROCKET_PLAN_TILED = 8
+ROCKET_PLAN_SERIES = 16
 MAX_KERNEL_LENGTH = 11
 
 # every symbol include/rocket.h declares
@@ -76,7 +78,7 @@ class CPlanFacts(ctypes.Structure):
         ("mfma_per_row", ctypes.c_int64), ("lds_bytes", ctypes.c_int64),
         ("direct", ctypes.c_int32), ("clamped", ctypes.c_int32),
         ("features_per_kernel", ctypes.c_int32), ("rows_per_block", ctypes.c_int32),
-        ("n_features", ctypes.c_int64), ("minirocket", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("n_features", ctypes.c_int64), ("minirocket", ctypes.c_int32), ("series_lane", ctypes.c_int32),
     ]
 
 
@@ -307,14 +309,15 @@ class Plan:
     """rocket_plan: a kernel set planned for series of length L on the current device."""
 
     def __init__(self, kernels: dict, L: int, direct: bool = False, clamped: bool = False,
-                 mpv: bool = False):
+                 mpv: bool = False, tiled: bool = False, series: bool = False):
         lib = library()
         self._c, self._keep = as_c_kernels(kernels)
         self.n_kernels = int(self._c.n_kernels)
         self.L = int(L)
         h = ctypes.c_void_p()
         flags = ((ROCKET_PLAN_DIRECT if direct else ROCKET_PLAN_DEFAULT)
-                 | (ROCKET_PLAN_CLAMPED if clamped else 0) | (ROCKET_PLAN_MPV if mpv else 0))
+                 | (ROCKET_PLAN_CLAMPED if clamped else 0) | (ROCKET_PLAN_MPV if mpv else 0)
+                 | (ROCKET_PLAN_TILED if tiled else 0) | (ROCKET_PLAN_SERIES if series else 0))
         _check(lib.rocket_plan_create_ex(ctypes.byref(self._c), self.L, flags, ctypes.byref(h)),
                "rocket_plan_create")
         self._h = h
@@ -327,7 +330,8 @@ class Plan:
         return dict(n_items=f.n_items, n_buckets=f.n_buckets, mfma_per_row=f.mfma_per_row,
                     lds_bytes=f.lds_bytes, direct=bool(f.direct), clamped=bool(f.clamped),
                     features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block,
-                    n_features=f.n_features, minirocket=bool(f.minirocket))
+                    n_features=f.n_features, minirocket=bool(f.minirocket),
+                    series_lane=bool(f.series_lane))
 
     @property
     def n_features(self) -> int:

@@ -231,9 +231,12 @@ def assert_mpv_parity(F3, ref, what=""):
     fp32 range and, where the GPU counted the same positives as the oracle,
     within MPV_REL_TOL * MPV + beta of it.  beta (the oracle's bound on any
     one dot product's fp32 error) covers the error the averaged values carry;
-    the relative part covers the kernel's own summation: each lane adds at
-    most ceil(O/64) values in sequence and a 64-lane tree adds 6 more
-    roundings, (O/64 + 6) * 2^-24 < 1e-4 for every O below 2^24 / 100."""
+    the relative part covers the kernel's own summation: in the
+    position-tiled layout each lane adds at most ceil(O/64) values in
+    sequence and a 64-lane tree adds 6 more roundings, (O/64 + 6) * 2^-24 <
+    1e-4 for every O below 2^24 / 100; in the series-lane layout (L <= 128)
+    a lane adds the O <= 128 values of its series in sequence, 128 * 2^-24 <
+    1e-4."""
     F2, mpv = split_mpv(F3)
     r = assert_parity(F2, ref, what)
     mpv = np.asarray(mpv, dtype=np.float64)

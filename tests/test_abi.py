@@ -108,9 +108,11 @@ def test_plan_validation_null_and_flags(lib):
     k = _kernels()
     c, keep = rb.as_c_kernels(k)
     assert lib.rocket_plan_create(ctypes.byref(c), 100, None) == rb.ROCKET_ERR_INVALID_ARG
-    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, 8, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
-    both = rb.ROCKET_PLAN_DIRECT | rb.ROCKET_PLAN_CLAMPED
-    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, both, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, 32, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+    for a, b in ((rb.ROCKET_PLAN_DIRECT, rb.ROCKET_PLAN_CLAMPED), (rb.ROCKET_PLAN_DIRECT, rb.ROCKET_PLAN_TILED),
+                 (rb.ROCKET_PLAN_SERIES, rb.ROCKET_PLAN_DIRECT), (rb.ROCKET_PLAN_SERIES, rb.ROCKET_PLAN_CLAMPED),
+                 (rb.ROCKET_PLAN_SERIES, rb.ROCKET_PLAN_TILED)):
+        assert lib.rocket_plan_create_ex(ctypes.byref(c), 100, a | b, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
     bad = rb.CKernels(2, 0, 11, c.length, c.dilation, c.padding, c.bias, None)
     assert lib.rocket_plan_create(ctypes.byref(bad), 100, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
     bad = rb.CKernels(2, 0, 12, c.length, c.dilation, c.padding, c.bias, c.weights)
