@@ -270,6 +270,7 @@ def main():
                      "valid_fma_per_series": valid_per_row,
                      "nominal_fma_per_series": nominal_per_row,
                      "mfma_fma_issued_per_series": 256 * info["mfma_per_row"],
+                     "valu_fma_issued_per_series": 64 * info.get("valu_fma_per_row", 0),
                      "mfma_pipe_frac": mfma_fma_issued_frac(mfma_fma_per_pass, ms_per_step)},
         "plan": dict(info, create_ms=plan_ms),
         "device": {"name": props.name, "cu": props.multi_processor_count},

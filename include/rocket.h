@@ -263,6 +263,10 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *                least 4,096 series, or every call with ROCKET_PLAN_SERIES);
  *                lds_bytes, rows_per_block and mfma_per_row then describe
  *                that layout
+ *   valu_fma_per_row  fp32 FMA instructions (64 lanes each) one series costs
+ *                in VALU items: the one or two kernels left over in a bucket
+ *                of a univariate plan for series longer than 128 samples,
+ *                run without MFMA
  */
 typedef struct {
     int64_t n_items;
@@ -276,6 +280,7 @@ typedef struct {
     int64_t n_features;
     int32_t minirocket;
     int32_t series_lane;
+    int64_t valu_fma_per_row;
 } rocket_plan_facts;
 
 /* Fill *out with the plan's facts.  Errors: ROCKET_ERR_INVALID_ARG if p or
@@ -297,18 +302,22 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                (1 and channel 0 for univariate sets); mask_lo |
  *                mask_hi << 32 holds the same channels as a bit mask;
  *                variant = 2 * ell_index + (G - 1), ell_index 0/1/2 for
- *                7/9/11 taps, G kernel groups of 4 slots;
+ *                7/9/11 taps, G kernel groups of 4 slots (MFMA items), or
+ *                6 + 2 * ell_index + (nk - 1) for VALU items of nk = 1 or 2
+ *                kernels in slots 0..nk-1 (G = 1 packing; univariate plans
+ *                for series longer than 128 samples);
  *                the O outputs are computed in tiles = ceil(O / 64) tiles
  *                of 64 consecutive positions (lane l of tile k computes
  *                output 64k + l; lanes past O compute nothing that counts);
- *                cost = MFMA instructions per series (tiles x taps x G x n_ch)
+ *                cost = MFMA instructions per series (tiles x taps x G x n_ch;
+ *                VALU items: (tiles x taps x nk + 1) / 2)
  *   wpk          packed weights, per item [n_ch][G][taps][4 slots]
  *   slot_bias, slot_kernel  per item 4G slots (kernel -1 = empty slot)
  *   order, split_begin, layout_off  item orders for the split counts in
  *                split_counts[n_layouts]: the items of variant v in split s
  *                of layout i (ns = split_counts[i] splits) are
  *                order[split_begin[layout_off[i] + v*ns + s] ..
- *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..5
+ *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..11
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
  *                of the padded layout (every tap of every real output lands
  *                inside the row)

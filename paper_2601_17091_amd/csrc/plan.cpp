@@ -293,15 +293,21 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             // every kernel of a frame list has these outputs
             const int64_t O = output_length(L, k->length[ks[0].first], d, k->padding[ks[0].first]);
             const int64_t n_tiles = ceil_div(O, kTile);
+            // univariate sets of long series: the one or two kernels left
+            // after the 4- and 8-kernel items run as a VALU item (a 5-kernel
+            // rest as 4 + 1): one kernel costs a quarter of a 4-slot MFMA
+            // group's FMA work, two about half
+            const bool valu_ok = C == 1 && L > kSeriesMaxL;
             size_t pos = 0;
             while (pos < ks.size()) {
                 const size_t rem = ks.size() - pos;
-                const int G = (C > 1 || rem <= 4) ? 1 : 2;
+                const int nk_valu = (valu_ok && rem <= 2) ? (int)rem : 0;
+                const int G = (C > 1 || rem <= 4 || (valu_ok && rem == 5)) ? 1 : 2;
                 const size_t take = C > 1 ? (size_t)item_sizes[next_item++]
                                           : std::min<size_t>(rem, (size_t)(4 * G));
                 ItemDesc it;
                 std::memset(&it, 0, sizeof(it));
-                it.variant = eidx * 2 + (G - 1);
+                it.variant = nk_valu ? kValuVariant0 + eidx * 2 + (nk_valu - 1) : eidx * 2 + (G - 1);
                 it.d = d;
                 it.p = p;
                 it.O = (int32_t)O;
@@ -320,8 +326,11 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                         ++it.n_ch;
                     }
                 // MFMA instructions per series: ell taps per tile and group,
-                // for every channel of the item (capped: it only orders work)
-                it.cost = (int32_t)std::min<int64_t>(n_tiles * ell * G * it.n_ch, INT32_MAX);
+                // for every channel of the item (capped: it only orders work);
+                // a VALU item's nk FMAs per tap and tile count as half an
+                // MFMA each (4.5 against 8.7 cycles)
+                it.cost = nk_valu ? (int32_t)std::min<int64_t>((n_tiles * ell * nk_valu + 1) / 2, INT32_MAX)
+                                  : (int32_t)std::min<int64_t>(n_tiles * ell * G * it.n_ch, INT32_MAX);
                 it.inv_O = 1.0 / (double)O;
                 // A-operand weights: [channel][g][j][slot i]; zeros for empty
                 // slots, for channels a slot's kernel does not read and for
@@ -351,8 +360,12 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
                     }
                 }
                 P.items.push_back(it);
-                P.mfma_per_row += n_tiles * ell * G * it.n_ch;
-                P.series_mfma_64 += O * ell * G;
+                if (!nk_valu) {
+                    P.mfma_per_row += n_tiles * ell * G * it.n_ch;
+                    P.series_mfma_64 += O * ell * G;
+                } else {
+                    P.valu_fma_per_row += n_tiles * ell * nk_valu;
+                }
                 pos += take;
             }
         }

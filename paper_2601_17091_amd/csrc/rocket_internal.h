@@ -69,7 +69,18 @@ constexpr int kItemWords = (int)(sizeof(ItemDesc) / sizeof(int32_t));
 // the items are grouped by variant, so that every workgroup runs one code
 // variant: the items of variant v in split s are
 // order[split_begin[v*nsplit + s] .. split_begin[v*nsplit + s + 1]).
-constexpr int kNumVariants = 2 * kNumEll;
+// Variants 0..5 are MFMA items, 2 * ell_index + (G - 1).  Variants 6..11 are
+// VALU items: the one or two leftover kernels of a bucket (nk of them), run
+// with plain fp32 FMA instead of a 4-slot MFMA group that would be mostly
+// empty, 6 + 2 * ell_index + (nk - 1); their weights keep the 4-slot packing
+// of a one-group item.
+constexpr int kNumMfmaVariants = 2 * kNumEll;
+constexpr int kNumVariants = 4 * kNumEll;
+constexpr int kValuVariant0 = kNumMfmaVariants;
+
+// Series of at most this length can run in the series-lane layout, which
+// takes MFMA items only; VALU items are made for longer series.
+constexpr int kSeriesMaxL = 128;
 constexpr int kNumSplitLayouts = 6;  // 1, 2, 4, 8, 16, 32 splits
 constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 
@@ -93,6 +104,7 @@ struct HostPlan {
     int64_t n_buckets = 0;
     int64_t mfma_per_row = 0;
     int64_t series_mfma_64 = 0;  // MFMAs for 64 series in the series-lane layout (O x taps x G)
+    int64_t valu_fma_per_row = 0;  // VALU items: fp32 FMA instructions (64 lanes) per series
     std::vector<ItemDesc> items;
     std::vector<float> wpk;       // packed A-operand weights
     std::vector<float> bias;      // per slot

@@ -727,6 +727,157 @@ __device__ __forceinline__ void run_items(int *next_item, int beg, int cnt_items
 }
 
 // What one workgroup does: a row group, one variant, one split of its items.
+// ---------------------------------------------------------------------------
+// VALU items: the one or two kernels left over in a bucket of a long-series
+// plan.  A 4-slot MFMA group would run them with 3 or 2 empty slots, and
+// each empty slot still costs its share of the MFMA and of the reduction; on
+// the VALU each kernel costs one fp32 FMA per tap and tile (4.5 cycles
+// against 8.7 for the 4-slot MFMA) and one result register to reduce.  The
+// tiles, blocks (8 tiles), series reads and the -inf start of lanes past O
+// are those of a one-group MFMA item; the weights and biases are scalars.
+// ---------------------------------------------------------------------------
+
+template <int NK>
+struct ValuAcc {
+    float mx[NK];
+    uint32_t cnt[NK];
+    float ps[NK];
+};
+
+template <int ELL, int NK, int NT, bool LAST, bool MPV, typename Src>
+__device__ __forceinline__ void valu_block(const Src &src, const float (&w)[NK][ELL], const float (&binit)[NK],
+                                           const float (&blast)[NK], ValuAcc<NK> &va) {
+    float acc[NT][NK];
+#pragma unroll
+    for (int j = 0; j < ELL; ++j) {
+        float xv[NT];
+        lds_tiles<NT>(src.m0(j), xv);
+        if constexpr (NT > 4) lds_tiles_rest<NT>(xv);
+#pragma unroll
+        for (int u = 0; u < NT; ++u)
+#pragma unroll
+            for (int c = 0; c < NK; ++c) {
+                const float a0 = (j == 0) ? ((LAST && u == NT - 1) ? blast[c] : binit[c]) : acc[u][c];
+                acc[u][c] = fmaf(w[c][j], xv[u], a0);
+            }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+        for (int c = 0; c < NK; ++c) va.cnt[c] += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][c] > 0.0f));
+    if (MPV) {
+#pragma unroll
+        for (int u = 0; u < NT; ++u)
+#pragma unroll
+            for (int c = 0; c < NK; ++c) va.ps[c] += fmaxf(acc[u][c], 0.0f);
+    }
+#pragma unroll
+    for (int u = 0; u + 1 < NT; u += 2)
+#pragma unroll
+        for (int c = 0; c < NK; ++c) va.mx[c] = fmaxf(fmaxf(va.mx[c], acc[u][c]), acc[u + 1][c]);
+    if (NT % 2 == 1) {
+#pragma unroll
+        for (int c = 0; c < NK; ++c) va.mx[c] = fmaxf(va.mx[c], acc[NT - 1][c]);
+    }
+}
+
+template <int ELL, int NK, int N, bool MPV, typename Src>
+struct ValuTail {
+    __device__ __forceinline__ static void run(int nv, const Src &src, const float (&w)[NK][ELL],
+                                               const float (&binit)[NK], const float (&blast)[NK],
+                                               ValuAcc<NK> &va) {
+        if (nv == N)
+            valu_block<ELL, NK, N, true, MPV>(src, w, binit, blast, va);
+        else
+            ValuTail<ELL, NK, N - 1, MPV, Src>::run(nv, src, w, binit, blast, va);
+    }
+};
+template <int ELL, int NK, bool MPV, typename Src>
+struct ValuTail<ELL, NK, 0, MPV, Src> {
+    __device__ __forceinline__ static void run(int, const Src &, const float (&)[NK][ELL], const float (&)[NK],
+                                               const float (&)[NK], ValuAcc<NK> &) {}
+};
+
+// Combine over the whole wavefront (every lane gets the result).
+template <typename Op>
+__device__ __forceinline__ float wave_all(float v) {
+    return row_reduce<Op>(fold16<Op>(fold32<Op>(v, v), fold32<Op>(v, v)));
+}
+
+template <int ELL, int NK, bool CLAMP, bool MPV>
+__device__ __forceinline__ void run_valu_item(const ItemDesc &it, const float *rows0, int nrows, const FusedArgs &a,
+                                              float *F0, int lane) {
+    constexpr int NT = rocket::kTilesPerBlock[0];
+    // weights and biases are the same on every lane: scalar registers
+    float w[NK][ELL], binit[NK], blast[NK];
+    const int rem = it.O - (it.n_tiles - 1) * kTile;
+#pragma unroll
+    for (int c = 0; c < NK; ++c) {
+#pragma unroll
+        for (int j = 0; j < ELL; ++j) w[c][j] = as_const(a.wpk)[it.w_off + j * 4 + c];
+        const float b = as_const(a.bias)[it.k_off + c];
+        float bv;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(bv) : "s"(b));
+        binit[c] = bv;
+        blast[c] = lane < rem ? bv : -INFINITY;
+    }
+    int kid[NK];
+#pragma unroll
+    for (int c = 0; c < NK; ++c) kid[c] = as_const(a.kid)[it.k_off + c];
+    const int row_pitch = a.C * a.row_stride;
+    const int nfull = (it.n_tiles - 1) / NT;
+    const int nv = it.n_tiles - nfull * NT;
+    const int64_t f_stride = (int64_t)a.nf * a.K;
+    for (int r = 0; r < nrows; ++r) {
+        ValuAcc<NK> va;
+#pragma unroll
+        for (int c = 0; c < NK; ++c) {
+            va.mx[c] = -INFINITY;
+            va.cnt[c] = 0;
+            va.ps[c] = 0.0f;
+        }
+        const uint32_t row = lds_addr(rows0 + r * row_pitch);
+        for (int blk = 0; blk < nfull; ++blk) {
+            const int b0 = blk * (NT * kTile) - it.p;
+            if constexpr (CLAMP)
+                valu_block<ELL, NK, NT, false, MPV>(ClampedTiles{row, b0, it.d, a.L}, w, binit, blast, va);
+            else
+                valu_block<ELL, NK, NT, false, MPV>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, w, binit, blast, va);
+        }
+        const int b0 = nfull * (NT * kTile) - it.p;
+        if constexpr (CLAMP)
+            ValuTail<ELL, NK, NT, MPV, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, w, binit, blast, va);
+        else
+            ValuTail<ELL, NK, NT, MPV, PaddedTiles>::run(nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, w, binit,
+                                                         blast, va);
+        float m[NK], psum[NK];
+#pragma unroll
+        for (int c = 0; c < NK; ++c) {
+            m[c] = wave_all<OpMax>(va.mx[c]);
+            psum[c] = MPV ? wave_all<OpSum>(va.ps[c]) : 0.0f;
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int c = 0; c < NK; ++c)
+                write_features<MPV>(va.cnt[c], m[c], psum[c], kid[c], it.inv_O, F0 + r * f_stride);
+        }
+    }
+}
+
+template <int ELL, int NK, bool CLAMP, bool MPV>
+__device__ __forceinline__ void run_valu_items(int *next_item, int beg, int cnt_items, const float *rows0, int nrows,
+                                               const FusedArgs &a, float *F0, int lane) {
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
+        run_valu_item<ELL, NK, CLAMP, MPV>(it, rows0, nrows, a, F0, lane);
+    }
+}
+
 struct GroupWork {
     int variant;
     int beg;        // first entry of the items' order
@@ -808,7 +959,14 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
             case 2: run_items<9, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
             case 3: run_items<9, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
             case 4: run_items<11, 1, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-            default: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 5: run_items<11, 2, CLAMP, MPV, MC>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            // VALU items (univariate long-series plans)
+            case 6: run_valu_items<7, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 7: run_valu_items<7, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 8: run_valu_items<9, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 9: run_valu_items<9, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            case 10: run_valu_items<11, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+            default: run_valu_items<11, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
         }
     }
 }
@@ -827,7 +985,7 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
 
 constexpr int kSeriesLanes = rocket::kWave;              // series per workgroup
 constexpr int kSeriesMargin = rocket::kMaxTilesPerBlock;  // zero positions on each side
-constexpr int kSeriesMaxL = 128;                           // longest series it takes
+using rocket::kSeriesMaxL;                                 // longest series it takes
 constexpr int64_t kSeriesMinRows = 4096;  // fewer series per call: too few workgroups, use tiles
 
 // Stages the group's series: position m of series r at
@@ -1604,6 +1762,7 @@ extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_fact
     out->n_features = p->f_cols;
     out->minirocket = p->minirocket ? 1 : 0;
     out->series_lane = p->series ? 1 : 0;
+    out->valu_fma_per_row = p->host.valu_fma_per_row;
     out->rows_per_block = p->direct ? 0 : (p->series ? kSeriesLanes : p->rows_per_block);
     return ROCKET_OK;
 }

@@ -26,6 +26,16 @@ ELLS = (7, 9, 11)
 TILE = 64
 TILES_PER_BLOCK = {1: 8, 2: 4}
 CLAMP_MARGIN = 512
+N_VARIANTS = 12      # 0..5 MFMA items, 6..11 VALU items
+SERIES_MAX_L = 128   # VALU items only for longer series
+
+
+def variant_info(v):
+    """(taps, MFMA groups G, VALU kernels nk) of an item variant: MFMA items
+    2*ell_index + (G-1); VALU items 6 + 2*ell_index + (nk-1), packed as G = 1."""
+    if v < 6:
+        return ELLS[v // 2], v % 2 + 1, 0
+    return ELLS[(v - 6) // 2], 1, (v - 6) % 2 + 1
 
 
 def item_fields(row):
@@ -48,7 +58,7 @@ def kernel_row(kernels, k, c):
 
 def tile_reads(f, ell, L, clamped):
     """Series index every lane reads, [tile, lane, tap], in the given layout."""
-    G = f["variant"] % 2 + 1
+    G = variant_info(f["variant"])[1]
     NT = TILES_PER_BLOCK[G]
     nt, d, p = f["n_tiles"], f["d"], f["p"]
     k = np.arange(nt)
@@ -80,8 +90,8 @@ def walk(tables, kernels, L, X=None, clamped=False):
         rows[:, :, halo_lo:halo_lo + L] = Xc
     for row in tables["items"]:
         f = item_fields(row)
-        d, p, O, ell = f["d"], f["p"], f["O"], ELLS[f["variant"] // 2]
-        G = f["variant"] % 2 + 1
+        d, p, O = f["d"], f["p"], f["O"]
+        ell, G, nk = variant_info(f["variant"])
         nslot = 4 * G
         kid = tables["slot_kernel"][f["k_off"]:f["k_off"] + nslot]
         bias = tables["slot_bias"][f["k_off"]:f["k_off"] + nslot]
@@ -114,7 +124,12 @@ def walk(tables, kernels, L, X=None, clamped=False):
                 assert np.all(Wslot[:, s_] == 0)
         assert used.all()     # the channel list is exactly the union
         assert f["n_tiles"] == -(-O // TILE)
-        assert f["cost"] == f["n_tiles"] * ell * G * nch
+        if nk:
+            # VALU items: the first nk slots, univariate long series
+            assert nch == 1 and L > SERIES_MAX_L and np.all(kid[:nk] >= 0) and np.all(kid[nk:] < 0)
+            assert f["cost"] == (f["n_tiles"] * ell * nk + 1) // 2
+        else:
+            assert f["cost"] == f["n_tiles"] * ell * G * nch
         assert f["inv_O"] == 1.0 / O
         # outputs: lane l of tile k computes 64k + l; the real ones are < O
         t = (np.arange(f["n_tiles"])[:, None] * TILE + np.arange(TILE)[None, :])   # [tile, lane]
@@ -156,9 +171,9 @@ def check_tables(kernels, L, X=None, oracle=None):
     n_items = t["items"].shape[0]
     for li in range(len(t["layout_off"])):
         ns = t["split_counts"][li]
-        beg = t["split_begin"][t["layout_off"][li]:t["layout_off"][li] + 6 * ns + 1]
+        beg = t["split_begin"][t["layout_off"][li]:t["layout_off"][li] + N_VARIANTS * ns + 1]
         ids = []
-        for v in range(6):
+        for v in range(N_VARIANTS):
             for s_ in range(ns):
                 part = t["order"][beg[v * ns + s_]:beg[v * ns + s_ + 1]]
                 assert np.all(t["items"][part, 0] == v)
@@ -219,17 +234,21 @@ def test_item_cost_and_groups():
     ks = rk.generate_kernels(203, 10000, 1000)
     t = rk.plan_tables(ks, 1000)
     items = t["items"]
-    G = items[:, 0] % 2 + 1
-    ell = np.array(ELLS)[items[:, 0] // 2]
+    info = np.array([variant_info(int(v)) for v in items[:, 0]])
+    ell, G, nk = info[:, 0], info[:, 1], info[:, 2]
     O, n_tiles = items[:, 3], items[:, 4]
     np.testing.assert_array_equal(n_tiles, (O + TILE - 1) // TILE)
-    np.testing.assert_array_equal(items[:, 7], n_tiles * ell * G * items[:, 8])
-    # a bucket is split into groups of 8 with at most one smaller group
-    assert (G == 2).sum() > (G == 1).sum()
-    # MFMA work issued (256 FMA per instruction: 4 slots x 64 lanes) stays
-    # within 12% of the nominal taps x outputs
+    mf = nk == 0
+    np.testing.assert_array_equal(items[mf, 7], (n_tiles * ell * G * items[:, 8])[mf])
+    np.testing.assert_array_equal(items[~mf, 7], ((n_tiles * ell * nk + 1) // 2)[~mf])
+    # a bucket is split into groups of 8 with at most one smaller group,
+    # whose one or two last kernels run as a VALU item
+    assert (G[mf] == 2).sum() > (G[mf] == 1).sum() and (~mf).sum() > 0
+    # FMA work issued (an MFMA: 4 slots x 64 lanes; a VALU FMA: 64 lanes)
+    # stays within 12% of the nominal taps x outputs
     nominal = (ks["length"] * (1000 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
-    assert items[:, 7].sum() * 256 < 1.12 * nominal
+    issued = (n_tiles * ell * G * 256)[mf].sum() + (n_tiles * ell * nk * 64)[~mf].sum()
+    assert issued < 1.12 * nominal
 
 
 def test_centred_kernels_fill_longer_frames():
