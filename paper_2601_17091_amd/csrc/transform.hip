@@ -1799,7 +1799,19 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     const int R = series ? kSeriesLanes : p->rows_per_block;
     const int64_t groups = (n + R - 1) / R;
     int li = 0;
-    while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target) ++li;
+    // ... but keep a few items per wavefront of a workgroup in each split (on
+    // average over the variants present): 2 for 4-wavefront workgroups, 4
+    // for the 16-wavefront ones of long rows (with fewer, wavefronts wait
+    // idle at the end of a workgroup while others finish)
+    const bool big_group = !series && row_bytes * p->C > kBigLds;
+    const int min_items = big_group ? 4 * (kBigBlock / 64) : 2 * (kBlock / 64);
+    int64_t n_present = 0;
+    for (int v = 0; v < rocket::kNumVariants; ++v)
+        if (p->host.split_begin[v + 1] > p->host.split_begin[v]) ++n_present;
+    const int64_t per_variant = (int64_t)p->host.items.size() / std::max<int64_t>(n_present, 1);
+    while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target &&
+           per_variant / rocket::kSplitCounts[li + 1] >= min_items)
+        ++li;
     const int nsplit = rocket::kSplitCounts[li];
     FusedArgs a;
     a.X = X;
@@ -1838,7 +1850,7 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
         a.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
         const unsigned nb = (unsigned)(kXcds * a.groups_per_xcd * nsplit * a.n_variants);
         const size_t lds = (size_t)(series ? p->series_lds : p->lds_bytes);
-        const bool big = !series && row_bytes * p->C > kBigLds;
+        const bool big = big_group;
         const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
         const void *fn = series ? series_fn(p->mpv) : (p->minirocket ? mr_fn(sel & 3) : fused_fn(sel));
         void *args[] = {&a};
