@@ -136,8 +136,10 @@ void rocket_free_kernels(rocket_kernels *k);
  * Opaque execution plan for one kernel set and one series length L, on the
  * HIP device that is current when it is created.  Creating a plan validates
  * the set, groups the kernels by (length, dilation, padding), builds the
- * device work tables and uploads them (synchronously).  A plan is immutable
- * afterwards: transforms on different streams may share it.
+ * device work tables and uploads them (synchronously).  A plan's tables are
+ * immutable afterwards: transforms on different streams may share it.  The
+ * one mutable part is the series-lane layout's feature buffer (short
+ * series, see rocket_plan_create_ex), which transforms take in turn.
  */
 typedef struct rocket_plan rocket_plan;
 
@@ -206,8 +208,14 @@ void rocket_plan_destroy(rocket_plan *p);
  * Asynchronous on hip_stream (a hipStream_t; NULL = null stream).
  * n == 0 is a no-op.  Rows are independent; any row range of X may be
  * passed (row batching is the caller's loop over pointer offsets).
+ * A call that runs the series-lane layout (short series, n >= 4,096 or
+ * ROCKET_PLAN_SERIES) allocates the plan's feature buffer on first use, or
+ * grows it (hipMalloc, at most 1 GiB; growing first waits for the device),
+ * and makes the stream wait on the device for the previous call that used
+ * the buffer.
  * Errors: ROCKET_ERR_INVALID_ARG (p, X_dev or F_dev NULL with n > 0, n < 0);
- *         ROCKET_ERR_HIP (launch failure).
+ *         ROCKET_ERR_OOM (the feature buffer); ROCKET_ERR_HIP (launch
+ *         failure).
  */
 rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
                                     float *F_dev, void *hip_stream);
