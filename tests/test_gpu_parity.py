@@ -189,3 +189,36 @@ def test_random_small_cases(torch_gpu, rk, oracle, seed, mode):
     X = rng.standard_normal((n, L)).astype(np.float32)
     F, _ = run(rk, torch_gpu, X, ks, mode)
     assert_parity(F, oracle.transform(X, ks), "random")
+
+
+@pytest.mark.parametrize("mode", ["fused", "clamped"])
+@pytest.mark.parametrize("mpv", [False, True])
+def test_valu_items(torch_gpu, rk, oracle, mode, mpv):
+    """Buckets of 1, 2, 5, 9 and 10 kernels at L = 200 (above the short-series
+    limit): the one or two kernels left over in a bucket, and the fifth of a
+    five, run as VALU items beside 4- and 8-kernel MFMA items; lengths 3, 7,
+    9 and 11, padded and not, last tiles ragged."""
+    from _util import assert_mpv_parity
+    rng = np.random.default_rng(31)
+    L = 200
+    lengths, dil, pad, bias, weights = [], [], [], [], []
+    for size, (ln, d, padded) in zip((1, 2, 5, 10, 9, 1, 2, 2),
+                                     ((9, 3, 0), (7, 5, 1), (11, 2, 0), (9, 1, 1), (3, 17, 0), (11, 19, 1), (7, 33, 0),
+                                      (11, 7, 0))):
+        for _ in range(size):
+            lengths.append(ln)
+            dil.append(d)
+            pad.append((ln - 1) * d // 2 if padded else 0)
+            bias.append(float(rng.uniform(-1, 1)))
+            weights.append(rng.standard_normal(ln))
+    ks = kernel_set(lengths, dil, pad, bias, weights)
+    t = rk.plan_tables(ks, L)
+    assert set(range(6, 12)) <= set(t["items"][:, 0].tolist())  # every VALU variant
+    X = rng.standard_normal((11, L)).astype(np.float32)
+    _log("VALU items mode=%s mpv=%s" % (mode, mpv))
+    Xd = torch_gpu.from_numpy(X).cuda()
+    plan = rk.Plan(ks, L, clamped=mode == "clamped", mpv=mpv)
+    F = plan.transform(Xd)
+    torch_gpu.cuda.synchronize()
+    ref = oracle.transform(X, ks)
+    (assert_mpv_parity if mpv else assert_parity)(F.cpu().numpy(), ref, "valu items")
