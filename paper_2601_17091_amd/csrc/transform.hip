@@ -1799,18 +1799,22 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     const int R = series ? kSeriesLanes : p->rows_per_block;
     const int64_t groups = (n + R - 1) / R;
     int li = 0;
-    // ... but keep a few items per wavefront of a workgroup in each split (on
-    // average over the variants present): 2 for 4-wavefront workgroups, 4
-    // for the 16-wavefront ones of long rows (with fewer, wavefronts wait
-    // idle at the end of a workgroup while others finish)
+    // ... but once there are 2 workgroups per CU, keep a few items per
+    // wavefront of a workgroup in each split (on average over the variants
+    // present): 2 for 4-wavefront workgroups, 4 for the 16-wavefront ones of
+    // long rows (with fewer, wavefronts wait idle at the end of a workgroup
+    // while others finish)
     const bool big_group = !series && row_bytes * p->C > kBigLds;
     const int min_items = big_group ? 4 * (kBigBlock / 64) : 2 * (kBlock / 64);
     int64_t n_present = 0;
     for (int v = 0; v < rocket::kNumVariants; ++v)
         if (p->host.split_begin[v + 1] > p->host.split_begin[v]) ++n_present;
-    const int64_t per_variant = (int64_t)p->host.items.size() / std::max<int64_t>(n_present, 1);
+    n_present = std::max<int64_t>(n_present, 1);
+    const int64_t per_variant = (int64_t)p->host.items.size() / n_present;
+    const int64_t few_groups = 2 * (int64_t)std::max(p->n_cu, 1);
     while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target &&
-           per_variant / rocket::kSplitCounts[li + 1] >= min_items)
+           (per_variant / rocket::kSplitCounts[li + 1] >= min_items ||
+            groups * n_present * rocket::kSplitCounts[li] < few_groups))
         ++li;
     const int nsplit = rocket::kSplitCounts[li];
     FusedArgs a;
