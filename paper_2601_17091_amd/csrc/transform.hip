@@ -1516,13 +1516,19 @@ struct rocket_plan {
     int64_t series_min_rows = 0;  // calls with at least this many series use it
     int64_t series_lds = 0;       // its LDS per workgroup
     int32_t *d_slot_of = nullptr;  // series-lane layout: the slot of each kernel
-    // series-lane layout: the slot-ordered feature buffer, allocated on first
-    // use and grown as needed; transforms on different streams take turns on
-    // it (each waits for the previous user's event)
+    // series-lane layout: the slot-ordered feature buffer (two halves),
+    // allocated on first use and grown as needed; transforms on different
+    // streams take turns on it (each waits for the previous user's event).
+    // The permutation of one chunk runs on the plan's own stream while the
+    // next chunk's series kernel runs on the caller's.
     mutable std::mutex scratch_mu;
     mutable float *d_scratch = nullptr;
     mutable size_t scratch_bytes = 0;
     mutable hipEvent_t scratch_done = nullptr;
+    hipStream_t aux = nullptr;
+    hipEvent_t half_full[2] = {nullptr, nullptr};
+    hipEvent_t half_free[2] = {nullptr, nullptr};
+    hipEvent_t aux_done = nullptr;
     bool mpv = false;        // third feature per kernel: mean of positive values
     bool minirocket = false; // MINIROCKET plan: F [n, n_features], PPV only
     int64_t f_cols = 0;      // columns of F
@@ -1552,6 +1558,9 @@ struct rocket_plan {
 
 static void plan_free_device(rocket_plan *p) {
     if (p->scratch_done) (void)hipEventDestroy(p->scratch_done);
+    for (hipEvent_t ev : {p->half_full[0], p->half_full[1], p->half_free[0], p->half_free[1], p->aux_done})
+        if (ev) (void)hipEventDestroy(ev);
+    if (p->aux) (void)hipStreamDestroy(p->aux);
     void *ptrs[] = {p->d_scratch, p->d_slot_of, p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
                     p->d_split_begin, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
@@ -1674,7 +1683,10 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
             return ROCKET_ERR_INTERNAL;
         }
         e = upload(slot_of, &p->d_slot_of);
-        if (e == hipSuccess) e = hipEventCreateWithFlags(&p->scratch_done, hipEventDisableTiming);
+        for (hipEvent_t *ev : {&p->scratch_done, &p->half_full[0], &p->half_full[1], &p->half_free[0],
+                               &p->half_free[1], &p->aux_done})
+            if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking);
     }
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
@@ -1867,22 +1879,28 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
 }
 
 // Series-lane layout: the rows go in chunks; for each chunk the series
-// kernel writes the features in slot order into the plan's scratch buffer
-// (each slot's features of 64 consecutive series are contiguous), and the
-// permutation kernel writes the chunk's F rows in the original kernel order,
-// 64 kernels (64 * nf floats) at a time.  The scatter of single features
-// over F rows would otherwise cost more than the dot products of short
-// series.  The scratch holds at most 1 GiB (chunks of up to 8,192 rows).
+// kernel writes the features in slot order into one half of the plan's
+// buffer (each slot's features of 64 consecutive series are contiguous), and
+// the permutation kernel writes the chunk's F rows in the original kernel
+// order, 64 kernels (64 * nf floats) at a time.  The scatter of single
+// features over F rows would otherwise cost more than the dot products of
+// short series.  The permutation (memory-bound) runs on the plan's own
+// stream, beside the next chunk's series kernel (compute-bound) on the
+// caller's; chunk i uses half i % 2, which it takes once the permutation of
+// chunk i - 2 is done with it.  The call ends on the caller's stream after
+// the last permutation.  The buffer holds at most 1 GiB (halves of up to
+// 8,192 rows).
 static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t n, float *F,
                                    hipStream_t s) {
     const int64_t K = p->host.n_kernels;
     const int64_t n_slots = (int64_t)p->host.kid.size();
     const int nf = p->mpv ? 3 : 2;
     const int64_t slot_row_bytes = n_slots * nf * (int64_t)sizeof(float);
-    int64_t chunk = ((int64_t)1 << 30) / std::max<int64_t>(slot_row_bytes, 1);
+    int64_t chunk = ((int64_t)1 << 29) / std::max<int64_t>(slot_row_bytes, 1);
     chunk = std::max<int64_t>(kSeriesLanes, std::min<int64_t>(8192, chunk / kSeriesLanes * kSeriesLanes));
     chunk = std::min(chunk, (n + kSeriesLanes - 1) / kSeriesLanes * kSeriesLanes);
-    const size_t need = (size_t)(chunk * slot_row_bytes);
+    const int64_t half = chunk * n_slots * nf;  // floats
+    const size_t need = (size_t)(2 * half) * sizeof(float);
     std::lock_guard<std::mutex> lock(p->scratch_mu);
     if (p->scratch_bytes < need) {
         // hipFree waits for the work that still uses the old buffer
@@ -1894,22 +1912,31 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
     }
     // the previous transform of this plan (on any stream) is done with it
     if (hipStreamWaitEvent(s, p->scratch_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
-    for (int64_t r0 = 0; r0 < n; r0 += chunk) {
+    const void *pf = nf == 3 ? (const void *)rocket_slot_permute_kernel<3>
+                             : (const void *)rocket_slot_permute_kernel<2>;
+    int i = 0;
+    for (int64_t r0 = 0; r0 < n; r0 += chunk, ++i) {
+        const int h = i & 1;
         const int64_t m = std::min(chunk, n - r0);
-        const rocket_status st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, p->d_scratch, chunk, s);
+        float *Sh = p->d_scratch + h * half;
+        if (i >= 2 && hipStreamWaitEvent(s, p->half_free[h], 0) != hipSuccess) return ROCKET_ERR_HIP;
+        const rocket_status st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, Sh, chunk, s);
         if (st != ROCKET_OK) return st;
+        if (hipEventRecord(p->half_full[h], s) != hipSuccess) return ROCKET_ERR_HIP;
+        if (hipStreamWaitEvent(p->aux, p->half_full[h], 0) != hipSuccess) return ROCKET_ERR_HIP;
         const dim3 grid((unsigned)((K + 63) / 64), (unsigned)((m + 63) / 64));
-        const void *pf = nf == 3 ? (const void *)rocket_slot_permute_kernel<3>
-                                 : (const void *)rocket_slot_permute_kernel<2>;
-        const float *S = p->d_scratch;
+        const float *S = Sh;
         const int32_t *slot_of = p->d_slot_of;
         int32_t K32 = (int32_t)K;
         int64_t s_rows = chunk;
         float *Fc = F + r0 * K * nf;
         void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&m, &Fc};
-        if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, s) != hipSuccess) return ROCKET_ERR_HIP;
+        if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, p->aux) != hipSuccess) return ROCKET_ERR_HIP;
         if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+        if (hipEventRecord(p->half_free[h], p->aux) != hipSuccess) return ROCKET_ERR_HIP;
     }
+    if (hipEventRecord(p->aux_done, p->aux) != hipSuccess) return ROCKET_ERR_HIP;
+    if (hipStreamWaitEvent(s, p->aux_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
     if (hipEventRecord(p->scratch_done, s) != hipSuccess) return ROCKET_ERR_HIP;
     return ROCKET_OK;
 }
