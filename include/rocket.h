@@ -175,7 +175,9 @@ rocket_status rocket_plan_create(const rocket_kernels *k, int32_t L, rocket_plan
  * position for 4 kernels x 64 series and each lane reduces its own series;
  * the features go through a plan-owned buffer in slot order (allocated on
  * first use, at most 1 GiB, freed with the plan) and a permutation kernel
- * writes F.  Same results as the position-tiled layout, which serves calls
+ * writes F; it runs on a stream the plan owns (non-blocking, default
+ * priority) beside the next chunk of rows, and the call still completes on
+ * hip_stream.  Same results as the position-tiled layout, which serves calls
  * with fewer series.  Transforms of one plan on different streams take turns
  * on that buffer (each waits for the previous one on the device).
  * ROCKET_PLAN_TILED keeps every call in the position-tiled layout;
