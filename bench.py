@@ -98,8 +98,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs the transform on a single "
-              "MI355X (rows shard across GPUs with no exchange; see the design notes). "
+        print("bench.py measures one GPU only: the transform runs on a single MI355X "
+              "(rows would shard across GPUs with no exchange). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
