@@ -1204,28 +1204,52 @@ __global__ __launch_bounds__(kBlock) void rocket_series_kernel(FusedArgs a) {
     }
 }
 
-// F rows in the original kernel order from the slot-ordered buffer: a
-// workgroup of 4 wavefronts takes 64 kernels x 64 series; lane l moves
-// kernel k0 + l, so each series' 64 kernels are written as 64 * nf
-// consecutive floats, and each lane reads its slot column downward (the
-// column's cache lines serve the following series).
+// F rows in the original kernel order from the slot-ordered buffer: a tile
+// is 64 kernels x 64 series, and the workgroups (4 wavefronts) stride over
+// the tiles; wavefront w takes the tile's series 16w .. 16w + 15.  Lane l
+// moves kernel k0 + l: it reads the 16 series' features from its slot column
+// as whole 16-byte vectors (16 * NF consecutive floats, 128 or 192 bytes),
+// then writes them series by series, so each series' 64 kernels go out as
+// 64 * NF consecutive floats.  Columns hold s_rows series, a multiple of 64,
+// so the reads of a partial last tile stay inside the column; only the
+// writes check the series count.  No LDS: the kernel runs beside the series
+// kernel, which fills the LDS.
 template <int NF>
 __global__ __launch_bounds__(kBlock) void rocket_slot_permute_kernel(const float *S, int64_t s_rows,
                                                                      const int32_t *slot_of, int32_t K,
                                                                      int64_t n_rows, float *F) {
+    constexpr int kRows = 16;
+    constexpr int kVec = kRows * NF / 4;  // float4 per lane
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t k = (int64_t)blockIdx.x * 64 + lane;
-    const int64_t r0 = (int64_t)blockIdx.y * 64;
-    if (k >= K) return;
-    const float *src = S + (int64_t)slot_of[k] * s_rows * NF;
-    for (int64_t r = r0 + wave; r < min(r0 + 64, n_rows); r += 4) {
-        const float *a = src + r * NF;
-        float *b = F + r * (int64_t)K * NF + k * NF;
-        if constexpr (NF == 2) {
-            *reinterpret_cast<float2 *>(b) = *reinterpret_cast<const float2 *>(a);
-        } else {
+    const int64_t k_tiles = ((int64_t)K + 63) / 64;
+    const int64_t n_tiles = k_tiles * ((n_rows + 63) / 64);
+    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+        const int64_t k = (t % k_tiles) * 64 + lane;
+        const int64_t r0 = (t / k_tiles) * 64 + wave * kRows;
+        if (k >= K || r0 >= n_rows) continue;
+        const float4 *src = reinterpret_cast<const float4 *>(S + ((int64_t)slot_of[k] * s_rows + r0) * NF);
+        float v[kVec * 4];
 #pragma unroll
-            for (int f = 0; f < NF; ++f) b[f] = a[f];
+        for (int i = 0; i < kVec; ++i) {
+            const float4 q = src[i];
+            v[4 * i] = q.x;
+            v[4 * i + 1] = q.y;
+            v[4 * i + 2] = q.z;
+            v[4 * i + 3] = q.w;
+        }
+        const int nr = (int)min<int64_t>(kRows, n_rows - r0);
+        float *b = F + r0 * (int64_t)K * NF + k * NF;
+#pragma unroll
+        for (int rr = 0; rr < kRows; ++rr) {
+            if (rr < nr) {
+                if constexpr (NF == 2) {
+                    *reinterpret_cast<float2 *>(b) = make_float2(v[2 * rr], v[2 * rr + 1]);
+                } else {
+#pragma unroll
+                    for (int f = 0; f < NF; ++f) b[f] = v[NF * rr + f];
+                }
+            }
+            b += (int64_t)K * NF;
         }
     }
 }
@@ -1924,7 +1948,11 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
         if (st != ROCKET_OK) return st;
         if (hipEventRecord(p->half_full[h], s) != hipSuccess) return ROCKET_ERR_HIP;
         if (hipStreamWaitEvent(p->aux, p->half_full[h], 0) != hipSuccess) return ROCKET_ERR_HIP;
-        const dim3 grid((unsigned)((K + 63) / 64), (unsigned)((m + 63) / 64));
+        const int64_t tiles = ((K + 63) / 64) * ((m + 63) / 64);
+        // one workgroup per CU, striding over the tiles: the permutation then
+        // moves its bytes at a modest rate over the whole of the next chunk's
+        // series kernel (a full grid moves them in a burst that stalls it)
+        const dim3 grid((unsigned)std::min<int64_t>(tiles, std::max(p->n_cu, 1)));
         const float *S = Sh;
         const int32_t *slot_of = p->d_slot_of;
         int32_t K32 = (int32_t)K;

@@ -153,6 +153,30 @@ def test_series_lane_chunks(env):
     assert np.array_equal(Fs, Ft)
 
 
+@pytest.mark.parametrize("mpv", [False, True])
+def test_series_lane_chunks_many_tiles(env, oracle, mpv):
+    """Two chunks whose permutations hold more 64 x 64 tiles (700 kernels,
+    not a multiple of 64, x 8,192 series) than the permutation has
+    workgroups, so each workgroup strides over several tiles: PPV and MAX
+    equal the position-tiled layout's on every row, MPV meets the oracle's
+    parity rule on rows around the chunk boundary and the ends."""
+    torch, rk = env
+    L, K = 20, 700
+    ks = rk.generate_kernels(16, K, L)
+    X = _series(8192 + 300, L, 16)
+    _log("chunks many tiles n=%d K=%d mpv=%s" % (X.shape[0], K, mpv))
+    Fs, info = _run(env, ks, X, mpv=mpv, series=True)
+    assert info["series_lane"]
+    Ft, _ = _run(env, ks, X, mpv=mpv, tiled=True)
+    nf = 3 if mpv else 2
+    a = Fs.reshape(len(X), K, nf)
+    b = Ft.reshape(len(X), K, nf)
+    assert np.array_equal(a[:, :, :2], b[:, :, :2])
+    if mpv:
+        rows = np.r_[0:64, 8128:8256, len(X) - 64:len(X)]
+        assert_mpv_parity(Fs[rows], oracle.transform(X[rows], ks), "series mpv chunks")
+
+
 def test_series_lane_two_streams(env):
     """Transforms of one plan on two streams at once take turns on the
     plan's slot-ordered buffer: each result equals its one-stream result."""
