@@ -1938,16 +1938,25 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
     if (hipStreamWaitEvent(s, p->scratch_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
     const void *pf = nf == 3 ? (const void *)rocket_slot_permute_kernel<3>
                              : (const void *)rocket_slot_permute_kernel<2>;
+    // a failure part-way still ends with the tail below, so that the next
+    // transform of this plan waits for whatever this one enqueued
+    rocket_status st = ROCKET_OK;
     int i = 0;
     for (int64_t r0 = 0; r0 < n; r0 += chunk, ++i) {
         const int h = i & 1;
         const int64_t m = std::min(chunk, n - r0);
         float *Sh = p->d_scratch + h * half;
-        if (i >= 2 && hipStreamWaitEvent(s, p->half_free[h], 0) != hipSuccess) return ROCKET_ERR_HIP;
-        const rocket_status st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, Sh, chunk, s);
-        if (st != ROCKET_OK) return st;
-        if (hipEventRecord(p->half_full[h], s) != hipSuccess) return ROCKET_ERR_HIP;
-        if (hipStreamWaitEvent(p->aux, p->half_full[h], 0) != hipSuccess) return ROCKET_ERR_HIP;
+        if (i >= 2 && hipStreamWaitEvent(s, p->half_free[h], 0) != hipSuccess) {
+            st = ROCKET_ERR_HIP;
+            break;
+        }
+        st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, Sh, chunk, s);
+        if (st != ROCKET_OK) break;
+        if (hipEventRecord(p->half_full[h], s) != hipSuccess ||
+            hipStreamWaitEvent(p->aux, p->half_full[h], 0) != hipSuccess) {
+            st = ROCKET_ERR_HIP;
+            break;
+        }
         const int64_t tiles = ((K + 63) / 64) * ((m + 63) / 64);
         // one workgroup per CU, striding over the tiles: the permutation then
         // moves its bytes at a modest rate over the whole of the next chunk's
@@ -1959,14 +1968,17 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
         int64_t s_rows = chunk;
         float *Fc = F + r0 * K * nf;
         void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&m, &Fc};
-        if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, p->aux) != hipSuccess) return ROCKET_ERR_HIP;
-        if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
-        if (hipEventRecord(p->half_free[h], p->aux) != hipSuccess) return ROCKET_ERR_HIP;
+        if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, p->aux) != hipSuccess ||
+            hipGetLastError() != hipSuccess || hipEventRecord(p->half_free[h], p->aux) != hipSuccess) {
+            st = ROCKET_ERR_HIP;
+            break;
+        }
     }
-    if (hipEventRecord(p->aux_done, p->aux) != hipSuccess) return ROCKET_ERR_HIP;
-    if (hipStreamWaitEvent(s, p->aux_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
-    if (hipEventRecord(p->scratch_done, s) != hipSuccess) return ROCKET_ERR_HIP;
-    return ROCKET_OK;
+    const bool tail_ok = hipEventRecord(p->aux_done, p->aux) == hipSuccess &&
+                         hipStreamWaitEvent(s, p->aux_done, 0) == hipSuccess &&
+                         hipEventRecord(p->scratch_done, s) == hipSuccess;
+    if (st != ROCKET_OK) return st;
+    return tail_ok ? ROCKET_OK : ROCKET_ERR_HIP;
 }
 
 static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t n, float *F,
