@@ -429,7 +429,12 @@ __device__ __forceinline__ void tile_block(const Src &src, const float (&wa)[G][
         }
     }
     __builtin_amdgcn_sched_barrier(0);
+    // raised wave priority while the reduction runs: a wavefront that has
+    // finished its MFMAs gets its vector work issued first (measured: 0.4 %
+    // faster Manufacturing passes, 0.7 % faster long series; same results)
+    __builtin_amdgcn_s_setprio(1);
     block_reduce<G, NT, MPV>(acc, ra);
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // The last block of a row: its tile count nv (1..N) selects a code copy.
