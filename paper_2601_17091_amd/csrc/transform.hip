@@ -1305,7 +1305,11 @@ __device__ __forceinline__ void mr_block(const Src &src, const float (&wa)[1][ro
     v4f acc[NT][1];
     tile_mfma<rocket::kMrTaps, 1, NT, LAST, true>(src, wa, z, zlast, acc);
     __builtin_amdgcn_sched_barrier(0);
+    // raised wave priority over the compares, as in the fused kernel's
+    // block reduction (measured: 1.5 % faster MINIROCKET passes)
+    __builtin_amdgcn_s_setprio(1);
     mr_reduce<NT, NQ>(acc, thr, part, cnt);
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // The last block of a series: its tile count nv (1..N) selects a code copy.
