@@ -9,7 +9,7 @@ import sys
 import numpy as np
 import pytest
 
-from _util import assert_parity, kernel_set, load_golden, random_kernels
+from _util import assert_mpv_parity, assert_parity, kernel_set, load_golden, random_kernels
 
 pytestmark = pytest.mark.gpu
 
@@ -90,24 +90,25 @@ def test_full_workload_every_row(torch_gpu, rk, oracle, name, mode):
     _log("  %s" % r)
 
 
-def _sampled(torch, rk, oracle, name, extra, batch_rows=None):
+def _sampled(torch, rk, oracle, name, extra, batch_rows=None, mpv=False):
     from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
     w = WORKLOADS[name]
     _log("workload %s: %dx%d, K=%d, sampled rows" % (name, w.n, w.L, w.n_kernels))
     ks = rk.generate_kernels(w.kernel_seed, w.n_kernels, w.L)
     X_np = workload_series(name)
     X = torch.from_numpy(X_np).cuda()
-    plan = rk.Plan(ks, w.L)
+    plan = rk.Plan(ks, w.L, mpv=mpv)
     assert not plan.info()["direct"]
+    nf = 3 if mpv else 2
     rows = sample_rows(w.n, batch_rows or w.n, extra)
-    got = np.zeros((rows.shape[0], 2 * w.n_kernels), np.float32)
+    got = np.zeros((rows.shape[0], nf * w.n_kernels), np.float32)
     if batch_rows is None:
         F = plan.transform(X)
         torch.cuda.synchronize()
         got[:] = F[torch.from_numpy(rows).cuda()].cpu().numpy()
         del F
     else:
-        Fb = torch.empty((batch_rows, 2 * w.n_kernels), dtype=torch.float32, device=X.device)
+        Fb = torch.empty((batch_rows, nf * w.n_kernels), dtype=torch.float32, device=X.device)
 
         def grab(r0, Fv):
             sel = rows[(rows >= r0) & (rows < r0 + Fv.shape[0])]
@@ -118,7 +119,7 @@ def _sampled(torch, rk, oracle, name, extra, batch_rows=None):
         torch.cuda.synchronize()
         del Fb
     ref = oracle.transform(X_np, ks, rows=rows)
-    r = assert_parity(got, ref, name)
+    r = assert_mpv_parity(got, ref, name) if mpv else assert_parity(got, ref, name)
     _log("  rows=%d %s" % (rows.shape[0], r))
 
 
@@ -132,6 +133,12 @@ def test_long_sampled(torch_gpu, rk, oracle):
 
 def test_many_short_batched(torch_gpu, rk, oracle):
     _sampled(torch_gpu, rk, oracle, "many_short", extra=200, batch_rows=100000)
+
+
+def test_many_short_mpv_batched(torch_gpu, rk, oracle):
+    """Many-short with MPV: the series-lane layout's three features through
+    the slot-ordered buffer, every 10^5-row batch of the full workload."""
+    _sampled(torch_gpu, rk, oracle, "many_short", extra=200, batch_rows=100000, mpv=True)
 
 
 def test_paper_sweep_sampled(torch_gpu, rk, oracle):
