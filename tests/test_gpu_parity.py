@@ -127,6 +127,12 @@ def test_manufacturing_sampled(torch_gpu, rk, oracle):
     _sampled(torch_gpu, rk, oracle, "manufacturing", extra=60)
 
 
+def test_manufacturing_mpv_sampled(torch_gpu, rk, oracle):
+    """Manufacturing with MPV (one launch over all 10^5 series, F of
+    3 x 10,000 features per series): sampled rows against the oracle."""
+    _sampled(torch_gpu, rk, oracle, "manufacturing", extra=60, mpv=True)
+
+
 def test_long_sampled(torch_gpu, rk, oracle):
     _sampled(torch_gpu, rk, oracle, "long", extra=14)
 
