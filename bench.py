@@ -32,6 +32,97 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
+class ClockSampler:
+    """The GPU's shader (GFX) clock, sampled from the AMD SMI library in a
+    background thread while the timed passes run (the device is found by its
+    PCI address).  stop() returns the median, min and max of the samples in
+    MHz and how many were taken, or None where the SMI library is not
+    usable."""
+
+    def __init__(self, device_index=0, interval_s=0.02):
+        import threading
+        self.interval_s = interval_s
+        self.samples = []
+        self._stop = threading.Event()
+        self._thread = None
+        self._smi = None
+        self._handle = None
+        self.error = None
+        try:
+            import amdsmi
+            import torch
+            pr = torch.cuda.get_device_properties(device_index)
+            bdf = "%04x:%02x:%02x.0" % (pr.pci_domain_id, pr.pci_bus_id, pr.pci_device_id)
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._handle = amdsmi.amdsmi_get_processor_handle_from_bdf(bdf)
+            self._read()  # one read up front: fail here, not in the thread
+        except Exception as e:  # no SMI access: the line says so
+            self.error = "%s: %s" % (type(e).__name__, e)
+            self._handle = None
+
+    def _read(self):
+        info = self._smi.amdsmi_get_clock_info(self._handle, self._smi.AmdSmiClkType.GFX)
+        clk = info.get("clk")
+        return float(clk) if isinstance(clk, (int, float)) and clk > 0 else None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                v = self._read()
+                if v is not None:
+                    self.samples.append(v)
+            except Exception as e:
+                self.error = "%s: %s" % (type(e).__name__, e)
+                return
+            self._stop.wait(self.interval_s)
+
+    def start(self):
+        if self._handle is not None:
+            import threading
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def stop(self):
+        if self._thread is not None:
+            self._stop.set()
+            self._thread.join()
+        if self._smi is not None:
+            try:
+                self._smi.amdsmi_shut_down()
+            except Exception:
+                pass
+        if not self.samples:
+            return {"mhz": None, "source": "amdsmi (unavailable: %s)" % self.error}
+        a = np.array(self.samples)
+        return {"mhz": float(np.median(a)), "min": float(a.min()), "max": float(a.max()),
+                "samples": int(a.size), "source": "amdsmi GFX clock, sampled every %d ms during the timed passes"
+                                                  % int(self.interval_s * 1e3)}
+
+
+def timed_passes(torch, stream, one_pass, steps):
+    """Time `steps` calls of one_pass on `stream`: a HIP event between
+    consecutive passes (all on the launch stream), synchronised before and
+    after.  Returns (total ms, per-pass ms list, clock record)."""
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    clock = ClockSampler().start()
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for i in range(steps):
+        one_pass()
+        evs[i + 1].record(stream)
+    torch.cuda.synchronize()
+    clk = clock.stop()
+    per = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
+    return evs[0].elapsed_time(evs[-1]), per, clk
+
+
+def pass_stats(per):
+    a = np.array(per, dtype=np.float64)
+    return {"median": float(np.median(a)), "min": float(a.min()), "max": float(a.max()), "n": int(a.size)}
+
+
 def valid_taps(kernels, L):
     """Products whose series index lands inside [0, L) (padding zeros excluded),
     summed over kernels (and, for multivariate sets, over the channels each
@@ -163,16 +254,10 @@ def main():
         torch.cuda.synchronize()
         log("warmup %d/%d done" % (i + 1, args.warmup))
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        one_pass()
-    end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
+    total_ms, per_pass, clock = timed_passes(torch, stream, one_pass, args.steps)
     ms_per_step = total_ms / args.steps
-    log("timed %d passes: %.3f ms per pass" % (args.steps, ms_per_step))
+    log("timed %d passes: %.3f ms per pass (median %.3f), shader clock %s" % (
+        args.steps, ms_per_step, float(np.median(per_pass)), clock))
 
     valid_per_row, nominal_per_row = valid_taps(ks, w.L)
     flops_per_pass = 2.0 * w.n * valid_per_row
@@ -207,6 +292,8 @@ def main():
                "sample": "%d of %d %s rows (first/last row, first/last of each batch, seeded "
                          "random), all %d kernels, fp64, %.1f s" % (rows.shape[0], w.n, w.name,
                                                                      w.n_kernels, cpu_s)}
+        cpu["single_thread"] = single_thread_rate(rocket_oracle.transform, X_np, ks, rows, per_row, threads,
+                                                  w.n_kernels, args.cpu_seconds / 5)
         # GPU features of the same rows
         got = np.zeros((rows.shape[0], K2), np.float32)
         for r0 in range(0, w.n, batch):
@@ -271,7 +358,11 @@ def main():
                      "nominal_fma_per_series": nominal_per_row,
                      "mfma_fma_issued_per_series": 256 * info["mfma_per_row"],
                      "valu_fma_issued_per_series": 64 * info.get("valu_fma_per_row", 0),
-                     "mfma_pipe_frac": mfma_fma_issued_frac(mfma_fma_per_pass, ms_per_step)},
+                     "mfma_pipe_frac": mfma_fma_issued_frac(mfma_fma_per_pass, ms_per_step),
+                     "hbm_gbps": (traffic / (per_launch_ms * 1e-3) / 1e9) if traffic else None},
+        "pass_ms": pass_stats(per_pass),
+        "sclk_mhz": clock["mhz"],
+        "sclk": clock,
         "plan": dict(info, create_ms=plan_ms),
         "device": {"name": props.name, "cu": props.multi_processor_count},
         "source_digest": digest,
@@ -279,6 +370,16 @@ def main():
         "parity": parity,
     }
     print(json.dumps(out), flush=True)
+
+
+def single_thread_rate(fn, X_np, params, rows, per_row_all_threads, threads, per_row_units, seconds):
+    """The oracle on one thread over the first rows of the sample, sized to
+    about `seconds`: units (series x kernels or features) per second."""
+    m = int(max(1, min(rows.shape[0], seconds / max(per_row_all_threads * threads, 1e-6))))
+    t0 = time.perf_counter()
+    fn(X_np, params, rows=rows[:m], threads=1)
+    dt = time.perf_counter() - t0
+    return {"value": m * per_row_units / dt, "rows": m, "seconds": dt}
 
 
 def minirocket_valid_taps(params, L):
@@ -344,19 +445,15 @@ def bench_minirocket(args):
         plan.transform_into(X, F, stream)
         torch.cuda.synchronize()
         log("warmup %d/%d done" % (i + 1, args.warmup))
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
-        plan.transform_into(X, F, stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / max(args.steps, 1)
-    log("timed %d passes: %.3f ms per pass" % (args.steps, ms))
+    total_ms, per_pass, clock = timed_passes(torch, stream, lambda: plan.transform_into(X, F, stream),
+                                             max(args.steps, 1))
+    ms = total_ms / max(args.steps, 1)
+    log("timed %d passes: %.3f ms per pass, shader clock %s" % (args.steps, ms, clock))
     valid = minirocket_valid_taps(params, w.L)
     flops = 2.0 * w.n * valid
     achieved = flops / (ms * 1e-3) / 1e12
     digest = source_digest()
+    mr_traffic = traffic_from_profile("minirocket", digest, "rocket_minirocket_kernel")
     cpu = parity = None
     if not args.no_cpu_baseline:
         from oracle import minirocket_oracle, rocket_oracle
@@ -377,6 +474,8 @@ def bench_minirocket(args):
                "kind": "oracle",
                "sample": "%d of %d minirocket rows (first/last row, seeded random), all %d features, fp64, "
                          "%.1f s" % (rows.shape[0], w.n, nf, cpu_s)}
+        cpu["single_thread"] = single_thread_rate(minirocket_oracle.transform, X_np, params, rows, per_row,
+                                                  threads, nf, args.cpu_seconds / 5)
         plan.transform_into(X, F, stream)
         torch.cuda.synchronize()
         got = F[torch.from_numpy(rows).to(dev)].cpu().numpy().astype(np.float64)
@@ -396,10 +495,14 @@ def bench_minirocket(args):
                    "data_seed": w.data_seed, "fit_ms": fit_ms},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_FP32_TFLOPS,
-                     "traffic": traffic_from_profile("minirocket", digest, "rocket_minirocket_kernel"),
+                     "traffic": mr_traffic,
+                     "hbm_gbps": (mr_traffic / (ms * 1e-3) / 1e9) if mr_traffic else None,
                      "kernel": "rocket_minirocket_kernel", "launches_per_step": 1, "launch_ms": ms,
                      "algorithmic_flops_per_launch": flops, "valid_fma_per_series": valid,
                      "mfma_fma_issued_per_series": 256 * info["mfma_per_row"]},
+        "pass_ms": pass_stats(per_pass),
+        "sclk_mhz": clock["mhz"],
+        "sclk": clock,
         "plan": dict(info, create_ms=plan_ms),
         "device": {"name": props.name, "cu": props.multi_processor_count},
         "source_digest": digest,

@@ -22,6 +22,12 @@
  *     host memory instead).
  *     The library never frees them.  F is fully overwritten.
  *   - Kernel sets (rocket_kernels) live in HOST memory.
+ *   - Series values (X, and the training set of rocket_minirocket_fit) and
+ *     kernel weights and biases must be finite: no NaN, no infinity.  The
+ *     device code compares and takes maxima under that assumption, so the
+ *     features of a series that holds a NaN or an infinity are unspecified
+ *     (they may differ between row layouts and call sizes).  Nothing checks
+ *     the values.
  *   - Every argument is validated on the host before any device work; an
  *     invalid call returns an error and touches nothing.
  *   - No C++ exception crosses this boundary.
@@ -210,6 +216,7 @@ void rocket_plan_destroy(rocket_plan *p);
  * Asynchronous on hip_stream (a hipStream_t; NULL = null stream).
  * n == 0 is a no-op.  Rows are independent; any row range of X may be
  * passed (row batching is the caller's loop over pointer offsets).
+ * X must be finite (see the rules at the top of this file).
  * A call that runs the series-lane layout (short series, n >= 4,096 or
  * ROCKET_PLAN_SERIES) allocates the plan's feature buffer on first use, or
  * grows it (hipMalloc, at most 1 GiB; growing first waits for the device),
@@ -233,7 +240,8 @@ rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const r
 
 /*
  * Transform series held in HOST memory: X_host [n, L] -> F_host [n, f K]
- * (same layout and feature order as rocket_transform_plan).  Rows go
+ * (same layout and feature order as rocket_transform_plan; X_host must be
+ * finite).  Rows go
  * through the device in batches of batch_rows (0: about n/8 rows, at most
  * 256 MiB of staging per buffer).  Each
  * batch's copy in, transform and copy out run on three HIP streams (the
@@ -412,6 +420,7 @@ typedef struct {
  *     positions q_m = frac(m * golden ratio) (m = 1, 2, ... over the whole
  *     feature list, rounded to fp32), by linear interpolation between order
  *     statistics, rounded to fp32.
+ * X_train must be finite (see the rules at the top of this file).
  * Host only; never touches a GPU.
  * out: library-owned arrays; release with rocket_minirocket_free.  On error
  *      *out is zeroed.

@@ -42,8 +42,10 @@ def compile_flags() -> list[str]:
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
         # host arithmetic (the generator) exactly as written
         "-ffp-contract=off",
-        # inputs are finite: plain v_max_f32 without NaN canonicalisation
-        "-fno-honor-nans",
+        # device code only: inputs are finite, so fmaxf is a plain v_max_f32
+        # without NaN canonicalisation; host code (generator, planner,
+        # MINIROCKET fit) keeps IEEE NaN semantics
+        "-Xarch_device", "-fno-honor-nans",
         # MFMA results straight into VGPRs (no accumulator-register copies)
         "-mllvm", "-amdgpu-mfma-vgpr-form",
     ]

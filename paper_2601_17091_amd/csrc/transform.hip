@@ -1639,8 +1639,12 @@ static bool choose_layout(rocket_plan *p, bool clamped, const hipDeviceProp_t &p
     return false;
 }
 
-// Upload the work tables and allow the kernels the workgroup's LDS.
-static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
+// Upload the work tables and allow the kernels the workgroup's LDS.  The
+// dynamic-LDS limit is a process-wide attribute of each kernel function, so
+// it is set to the device's whole per-workgroup LDS (never to this plan's
+// own need): a later plan with a smaller footprint must not lower it below
+// what an earlier plan launches with.
+static hipError_t upload_tables(rocket_plan *p, int64_t lds, int64_t lds_limit) {
     hipError_t e = upload(p->host.items, &p->d_items);
     if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
     if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
@@ -1650,9 +1654,9 @@ static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
     if (e == hipSuccess) e = upload(p->host.thr, &p->d_thr);
     if (e == hipSuccess && lds > 64 * 1024) {
         for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
-            e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit);
         for (int sel = 0; sel < kMrInstances && e == hipSuccess; ++sel)
-            e = hipFuncSetAttribute(mr_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            e = hipFuncSetAttribute(mr_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit);
     }
     return e;
 }
@@ -1730,7 +1734,7 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * p->C * k->max_len, &p->d_w);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_count, (size_t)K, &p->d_cc);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_index, (size_t)K * p->C, &p->d_ci);
-    if (!p->direct && e == hipSuccess) e = upload_tables(p, lds);
+    if (!p->direct && e == hipSuccess) e = upload_tables(p, lds, (int64_t)prop.sharedMemPerBlock);
     if (e != hipSuccess) {
         plan_free_device(p);
         delete p;
@@ -1772,7 +1776,7 @@ extern "C" rocket_status rocket_minirocket_plan_create(const rocket_minirocket_p
         return ROCKET_ERR_LENGTH;
     }
     p->lds_bytes = lds;
-    e = upload_tables(p, lds);
+    e = upload_tables(p, lds, (int64_t)prop.sharedMemPerBlock);
     if (e != hipSuccess) {
         plan_free_device(p);
         delete p;

@@ -113,6 +113,56 @@ class CPlanTables(ctypes.Structure):
 _lib = None
 
 
+def _signatures() -> dict:
+    """argtypes and restype of every entry point include/rocket.h declares."""
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    kp = ctypes.POINTER(CKernels)
+    mp = ctypes.POINTER(CMiniRocketParams)
+    st = ctypes.c_int
+    return {
+        "rocket_generate_kernels": ([ctypes.c_uint64, i32, i32, kp], st),
+        "rocket_generate_kernels_multi": ([ctypes.c_uint64, i32, i32, i32, kp], st),
+        "rocket_free_kernels": ([kp], None),
+        "rocket_plan_create": ([kp, i32, ctypes.POINTER(vp)], st),
+        "rocket_plan_create_ex": ([kp, i32, ctypes.c_uint32, ctypes.POINTER(vp)], st),
+        "rocket_plan_destroy": ([vp], None),
+        "rocket_transform_plan": ([vp, vp, i64, vp, vp], st),
+        "rocket_transform": ([vp, i64, i32, kp, vp, vp], st),
+        "rocket_transform_host": ([vp, vp, i64, vp, i64, vp], st),
+        "rocket_plan_info": ([vp, ctypes.POINTER(CPlanFacts)], st),
+        "rocket_plan_tables_build": ([kp, i32, ctypes.POINTER(CPlanTables)], st),
+        "rocket_plan_tables_free": ([ctypes.POINTER(CPlanTables)], None),
+        "rocket_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "rocket_minirocket_fit": ([vp, i64, i32, i32, ctypes.c_uint64, mp], st),
+        "rocket_minirocket_free": ([mp], None),
+        "rocket_minirocket_plan_create": ([mp, ctypes.c_uint32, ctypes.POINTER(vp)], st),
+    }
+
+
+# the entry points that run on the host only (generator, planner tables,
+# MINIROCKET fit, status strings): plain C++ with no HIP code
+HOST_SYMBOLS = (
+    "rocket_generate_kernels",
+    "rocket_generate_kernels_multi",
+    "rocket_free_kernels",
+    "rocket_plan_tables_build",
+    "rocket_plan_tables_free",
+    "rocket_status_string",
+    "rocket_minirocket_fit",
+    "rocket_minirocket_free",
+)
+
+
+def bind(lib: ctypes.CDLL, names=EXPORTED) -> ctypes.CDLL:
+    """Set the ctypes signatures of `names` on a loaded library (a missing
+    symbol raises AttributeError)."""
+    sig = _signatures()
+    for name in names:
+        fn = getattr(lib, name)
+        fn.argtypes, fn.restype = sig[name]
+    return lib
+
+
 def library() -> ctypes.CDLL:
     """Load librocket.so (built by ``build_lib.build``); raise if it is absent."""
     global _lib
@@ -120,44 +170,8 @@ def library() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError("librocket.so is not built (run paper_2601_17091_amd.build_lib.build())")
-    lib = ctypes.CDLL(LIB_PATH)
-    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-    kp = ctypes.POINTER(CKernels)
-    lib.rocket_generate_kernels.argtypes = [ctypes.c_uint64, i32, i32, kp]
-    lib.rocket_generate_kernels.restype = ctypes.c_int
-    lib.rocket_generate_kernels_multi.argtypes = [ctypes.c_uint64, i32, i32, i32, kp]
-    lib.rocket_generate_kernels_multi.restype = ctypes.c_int
-    lib.rocket_free_kernels.argtypes = [kp]
-    lib.rocket_free_kernels.restype = None
-    lib.rocket_plan_create.argtypes = [kp, i32, ctypes.POINTER(vp)]
-    lib.rocket_plan_create.restype = ctypes.c_int
-    lib.rocket_plan_create_ex.argtypes = [kp, i32, ctypes.c_uint32, ctypes.POINTER(vp)]
-    lib.rocket_plan_create_ex.restype = ctypes.c_int
-    lib.rocket_plan_destroy.argtypes = [vp]
-    lib.rocket_plan_destroy.restype = None
-    lib.rocket_transform_plan.argtypes = [vp, vp, i64, vp, vp]
-    lib.rocket_transform_plan.restype = ctypes.c_int
-    lib.rocket_transform.argtypes = [vp, i64, i32, kp, vp, vp]
-    lib.rocket_transform.restype = ctypes.c_int
-    lib.rocket_transform_host.argtypes = [vp, vp, i64, vp, i64, vp]
-    lib.rocket_transform_host.restype = ctypes.c_int
-    lib.rocket_plan_info.argtypes = [vp, ctypes.POINTER(CPlanFacts)]
-    lib.rocket_plan_info.restype = ctypes.c_int
-    lib.rocket_plan_tables_build.argtypes = [kp, i32, ctypes.POINTER(CPlanTables)]
-    lib.rocket_plan_tables_build.restype = ctypes.c_int
-    lib.rocket_plan_tables_free.argtypes = [ctypes.POINTER(CPlanTables)]
-    lib.rocket_plan_tables_free.restype = None
-    lib.rocket_status_string.argtypes = [ctypes.c_int]
-    lib.rocket_status_string.restype = ctypes.c_char_p
-    mp = ctypes.POINTER(CMiniRocketParams)
-    lib.rocket_minirocket_fit.argtypes = [vp, i64, i32, i32, ctypes.c_uint64, mp]
-    lib.rocket_minirocket_fit.restype = ctypes.c_int
-    lib.rocket_minirocket_free.argtypes = [mp]
-    lib.rocket_minirocket_free.restype = None
-    lib.rocket_minirocket_plan_create.argtypes = [mp, ctypes.c_uint32, ctypes.POINTER(vp)]
-    lib.rocket_minirocket_plan_create.restype = ctypes.c_int
-    _lib = lib
-    return lib
+    _lib = bind(ctypes.CDLL(LIB_PATH))
+    return _lib
 
 
 def status_string(status: int) -> str:

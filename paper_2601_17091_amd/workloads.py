@@ -166,9 +166,11 @@ def workload_series(name: str, n: int | None = None) -> np.ndarray:
     return make_series(w.kind, w.n if n is None else n, w.L, w.data_seed)
 
 
-def sample_rows(n: int, batch: int, extra: int, seed: int = 7) -> np.ndarray:
+def sample_rows(n: int, batch: int, extra: int = 0, seed: int = 7, total: int | None = None) -> np.ndarray:
     """Row sample used for parity and the CPU baseline: the first and last row,
-    the first and last row of every batch, and ``extra`` seeded random rows."""
+    the first and last row of every batch, and ``extra`` seeded random rows
+    (or, with ``total``, as many seeded random rows as bring the sample to
+    ``total`` distinct rows, at most n)."""
     rows = {0, n - 1}
     for s in range(0, n, batch):
         rows.add(s)
@@ -176,4 +178,8 @@ def sample_rows(n: int, batch: int, extra: int, seed: int = 7) -> np.ndarray:
     rng = np.random.default_rng(seed)
     if extra > 0:
         rows.update(int(r) for r in rng.integers(0, n, size=extra))
+    if total is not None:
+        total = min(int(total), n)
+        while len(rows) < total:
+            rows.update(int(r) for r in rng.integers(0, n, size=total - len(rows)))
     return np.array(sorted(rows), dtype=np.int64)

@@ -210,3 +210,24 @@ def test_minirocket_plan_rejects_bad_params_before_the_device(lib):
     assert status(good, rb.ROCKET_PLAN_DIRECT) == rb.ROCKET_ERR_INVALID_ARG
     h = ctypes.c_void_p()
     assert lib.rocket_minirocket_plan_create(None, 0, ctypes.byref(h)) == rb.ROCKET_ERR_INVALID_ARG
+
+
+def _overcommit_mode():
+    try:
+        return int(open("/proc/sys/vm/overcommit_memory").read().strip())
+    except (OSError, ValueError):
+        return None
+
+
+def test_generator_reports_oom(lib):
+    """An absurd kernel set (2^31 - 1 multivariate kernels of 32 channels:
+    2.75 TiB of weights) cannot be allocated: the generator returns
+    ROCKET_ERR_OOM and leaves the output zeroed.  Nothing is touched before
+    the allocation fails, so no memory is used."""
+    if _overcommit_mode() == 1:
+        pytest.skip("the kernel always overcommits memory here: an absurd request would not fail")
+    k = rb.CKernels()
+    rc = lib.rocket_generate_kernels_multi(ctypes.c_uint64(1), 2 ** 31 - 1, 1000, 32, ctypes.byref(k))
+    assert rc == rb.ROCKET_ERR_OOM
+    assert k.n_kernels == 0 and not k.weights and not k.length
+    lib.rocket_free_kernels(ctypes.byref(k))

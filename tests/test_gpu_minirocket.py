@@ -133,6 +133,6 @@ def test_minirocket_workload_sampled(torch_gpu, rk, mo):
     params = _fit(rk, mo, X_np[:1000], w.n_kernels, w.kernel_seed)
     _log("workload fit: %d dilations, %d features" % (len(params["dilations"]), params["biases"].shape[0]))
     F, _ = _run(rk, torch_gpu, params, X_np, False)
-    rows = sample_rows(X_np.shape[0], X_np.shape[0], 48)
+    rows = sample_rows(X_np.shape[0], X_np.shape[0], total=256)
     ref = mo.transform(X_np, params, rows=rows)
     _check(F[rows], ref, "workload sample")

@@ -105,7 +105,7 @@ def test_multivariate_workload_sampled(env, oracle):
     X = torch.from_numpy(X_np).cuda()
     F = plan.transform(X)
     torch.cuda.synchronize()
-    rows = sample_rows(w.n, w.n, 40)
+    rows = sample_rows(w.n, w.n, total=256)
     got = F[torch.from_numpy(rows).cuda()].cpu().numpy()
     r = assert_parity(got, oracle.transform(X_np, ks, rows=rows), "multivariate")
     _log("  rows=%d %s" % (rows.shape[0], r))

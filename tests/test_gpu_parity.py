@@ -90,7 +90,7 @@ def test_full_workload_every_row(torch_gpu, rk, oracle, name, mode):
     _log("  %s" % r)
 
 
-def _sampled(torch, rk, oracle, name, extra, batch_rows=None, mpv=False):
+def _sampled(torch, rk, oracle, name, total, batch_rows=None, mpv=False):
     from paper_2601_17091_amd.workloads import WORKLOADS, sample_rows, workload_series
     w = WORKLOADS[name]
     _log("workload %s: %dx%d, K=%d, sampled rows" % (name, w.n, w.L, w.n_kernels))
@@ -100,7 +100,8 @@ def _sampled(torch, rk, oracle, name, extra, batch_rows=None, mpv=False):
     plan = rk.Plan(ks, w.L, mpv=mpv)
     assert not plan.info()["direct"]
     nf = 3 if mpv else 2
-    rows = sample_rows(w.n, batch_rows or w.n, extra)
+    rows = sample_rows(w.n, batch_rows or w.n, total=total)
+    assert rows.shape[0] == total
     got = np.zeros((rows.shape[0], nf * w.n_kernels), np.float32)
     if batch_rows is None:
         F = plan.transform(X)
@@ -123,34 +124,42 @@ def _sampled(torch, rk, oracle, name, extra, batch_rows=None, mpv=False):
     _log("  rows=%d %s" % (rows.shape[0], r))
 
 
+# sampled rows per workload: the first and last row, the first and last of
+# every F batch, and seeded random rows up to these counts
+ROWS_MANUFACTURING = 1024
+ROWS_LONG = 64
+ROWS_MANY_SHORT = 16384
+ROWS_PAPER_SWEEP = 64
+
+
 def test_manufacturing_sampled(torch_gpu, rk, oracle):
-    _sampled(torch_gpu, rk, oracle, "manufacturing", extra=60)
+    _sampled(torch_gpu, rk, oracle, "manufacturing", total=ROWS_MANUFACTURING)
 
 
 def test_manufacturing_mpv_sampled(torch_gpu, rk, oracle):
     """Manufacturing with MPV (one launch over all 10^5 series, F of
     3 x 10,000 features per series): sampled rows against the oracle."""
-    _sampled(torch_gpu, rk, oracle, "manufacturing", extra=60, mpv=True)
+    _sampled(torch_gpu, rk, oracle, "manufacturing", total=ROWS_MANUFACTURING, mpv=True)
 
 
 def test_long_sampled(torch_gpu, rk, oracle):
-    _sampled(torch_gpu, rk, oracle, "long", extra=14)
+    _sampled(torch_gpu, rk, oracle, "long", total=ROWS_LONG)
 
 
 def test_many_short_batched(torch_gpu, rk, oracle):
-    _sampled(torch_gpu, rk, oracle, "many_short", extra=200, batch_rows=100000)
+    _sampled(torch_gpu, rk, oracle, "many_short", total=ROWS_MANY_SHORT, batch_rows=100000)
 
 
 def test_many_short_mpv_batched(torch_gpu, rk, oracle):
     """Many-short with MPV: the series-lane layout's three features through
     the slot-ordered buffer, every 10^5-row batch of the full workload."""
-    _sampled(torch_gpu, rk, oracle, "many_short", extra=200, batch_rows=100000, mpv=True)
+    _sampled(torch_gpu, rk, oracle, "many_short", total=ROWS_MANY_SHORT, batch_rows=100000, mpv=True)
 
 
 def test_paper_sweep_sampled(torch_gpu, rk, oracle):
     """The default point of the paper's timing sweep (Sec. 4): 1,000 series
     of length 10,000 with 10,000 kernels."""
-    _sampled(torch_gpu, rk, oracle, "paper_sweep", extra=10)
+    _sampled(torch_gpu, rk, oracle, "paper_sweep", total=ROWS_PAPER_SWEEP)
 
 
 @pytest.mark.parametrize("mode", ["fused", "clamped"])

@@ -104,3 +104,27 @@ def test_clamped_layout_matches_padded(env):
     b = rk.Plan(ks, X.shape[1], clamped=True).transform(X)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+def test_large_lds_plan_survives_smaller_plan(env, oracle):
+    """The dynamic-LDS limit is an attribute of the kernel functions shared
+    by every plan of the process: creating a plan with a smaller footprint
+    above 64 KB (series of 17,000 samples) must not lower it below what an
+    earlier plan (20,000 samples, about 160 KB per workgroup) launches with."""
+    torch, rk, _, _ = env
+    from _util import assert_parity
+    from paper_2601_17091_amd.workloads import make_series
+    big_L, small_L = 20000, 17000
+    ks_big = rk.generate_kernels(208, 300, big_L)
+    ks_small = rk.generate_kernels(209, 300, small_L)
+    big = rk.Plan(ks_big, big_L)
+    small = rk.Plan(ks_small, small_L)
+    assert big.info()["lds_bytes"] > small.info()["lds_bytes"] > 64 * 1024
+    X_np = make_series("random_walk", 2, big_L, 108)
+    F = big.transform(torch.from_numpy(X_np).cuda())
+    torch.cuda.synchronize()
+    assert_parity(F.cpu().numpy(), oracle.transform(X_np, ks_big), "big plan after small")
+    Xs = make_series("random_walk", 2, small_L, 109)
+    Fs = small.transform(torch.from_numpy(Xs).cuda())
+    torch.cuda.synchronize()
+    assert_parity(Fs.cpu().numpy(), oracle.transform(Xs, ks_small), "small plan")
