@@ -375,7 +375,9 @@ def main():
 def single_thread_rate(fn, X_np, params, rows, per_row_all_threads, threads, per_row_units, seconds):
     """The oracle on one thread over the first rows of the sample, sized to
     about `seconds`: units (series x kernels or features) per second."""
-    m = int(max(1, min(rows.shape[0], seconds / max(per_row_all_threads * threads, 1e-6))))
+    # per_row_all_threads was timed on two rows, which keep at most two
+    # threads busy: about one thread's time per row
+    m = int(max(1, min(rows.shape[0], seconds / max(per_row_all_threads, 1e-6))))
     t0 = time.perf_counter()
     fn(X_np, params, rows=rows[:m], threads=1)
     dt = time.perf_counter() - t0

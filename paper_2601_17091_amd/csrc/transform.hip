@@ -1639,12 +1639,32 @@ static bool choose_layout(rocket_plan *p, bool clamped, const hipDeviceProp_t &p
     return false;
 }
 
-// Upload the work tables and allow the kernels the workgroup's LDS.  The
-// dynamic-LDS limit is a process-wide attribute of each kernel function, so
-// it is set to the device's whole per-workgroup LDS (never to this plan's
-// own need): a later plan with a smaller footprint must not lower it below
-// what an earlier plan launches with.
-static hipError_t upload_tables(rocket_plan *p, int64_t lds, int64_t lds_limit) {
+// Dynamic-LDS limits already granted to the workgroup kernels, per device.
+// The limit is a process-wide attribute of each kernel function, shared by
+// every plan, so it is only ever raised: a later plan with a smaller
+// footprint above 64 KB must not lower it below what an earlier plan
+// launches with.
+constexpr int kMaxDevices = 64;
+static std::mutex g_lds_attr_mu;
+static int g_lds_attr[kMaxDevices][kFusedInstances + kMrInstances];
+
+static hipError_t allow_lds(int device, int64_t lds) {
+    if (lds <= 64 * 1024) return hipSuccess;
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_lds_attr_mu);
+    hipError_t e = hipSuccess;
+    for (int sel = 0; sel < kFusedInstances + kMrInstances && e == hipSuccess; ++sel) {
+        int &granted = g_lds_attr[device][sel];
+        if (granted >= lds) continue;
+        const void *fn = sel < kFusedInstances ? fused_fn(sel) : mr_fn(sel - kFusedInstances);
+        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e == hipSuccess) granted = (int)lds;
+    }
+    return e;
+}
+
+// Upload the work tables and allow the kernels the workgroup's LDS.
+static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
     hipError_t e = upload(p->host.items, &p->d_items);
     if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
     if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
@@ -1652,12 +1672,7 @@ static hipError_t upload_tables(rocket_plan *p, int64_t lds, int64_t lds_limit) 
     if (e == hipSuccess) e = upload(p->host.order, &p->d_order);
     if (e == hipSuccess) e = upload(p->host.split_begin, &p->d_split_begin);
     if (e == hipSuccess) e = upload(p->host.thr, &p->d_thr);
-    if (e == hipSuccess && lds > 64 * 1024) {
-        for (int sel = 0; sel < kFusedInstances && e == hipSuccess; ++sel)
-            e = hipFuncSetAttribute(fused_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit);
-        for (int sel = 0; sel < kMrInstances && e == hipSuccess; ++sel)
-            e = hipFuncSetAttribute(mr_fn(sel), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit);
-    }
+    if (e == hipSuccess) e = allow_lds(p->device, lds);
     return e;
 }
 
@@ -1734,7 +1749,7 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
     if (e == hipSuccess) e = upload_raw(k->weights, (size_t)K * p->C * k->max_len, &p->d_w);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_count, (size_t)K, &p->d_cc);
     if (e == hipSuccess && p->C > 1) e = upload_raw(k->channel_index, (size_t)K * p->C, &p->d_ci);
-    if (!p->direct && e == hipSuccess) e = upload_tables(p, lds, (int64_t)prop.sharedMemPerBlock);
+    if (!p->direct && e == hipSuccess) e = upload_tables(p, lds);
     if (e != hipSuccess) {
         plan_free_device(p);
         delete p;
@@ -1776,7 +1791,7 @@ extern "C" rocket_status rocket_minirocket_plan_create(const rocket_minirocket_p
         return ROCKET_ERR_LENGTH;
     }
     p->lds_bytes = lds;
-    e = upload_tables(p, lds, (int64_t)prop.sharedMemPerBlock);
+    e = upload_tables(p, lds);
     if (e != hipSuccess) {
         plan_free_device(p);
         delete p;
