@@ -49,7 +49,9 @@ typedef enum {
     ROCKET_ERR_LENGTH = -2,      /* a kernel has O_k < 1 (or O_k >= 2^24) for this L */
     ROCKET_ERR_OOM = -3,         /* host or device allocation failed */
     ROCKET_ERR_HIP = -4,         /* a HIP runtime call or kernel launch failed */
-    ROCKET_ERR_INTERNAL = -5     /* should not happen; a bug */
+    ROCKET_ERR_INTERNAL = -5,    /* should not happen; a bug */
+    ROCKET_ERR_SCRATCH = -6      /* the request needs more than the library's static scratch
+                                    (rocket_transform_plan_noalloc) */
 } rocket_status;
 
 #define ROCKET_MAX_KERNEL_LENGTH 11 /* longest kernel; weights row stride */
@@ -228,6 +230,33 @@ void rocket_plan_destroy(rocket_plan *p);
  */
 rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
                                     float *F_dev, void *hip_stream);
+
+/*
+ * rocket_transform_plan without any device allocation, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, layout, results
+ * and errors as rocket_transform_plan, and the same kernels; it calls no
+ * hipMalloc, hipFree or other allocating routine.  The one layout that needs
+ * device memory beyond X and F, the series-lane layout of short series
+ * (the slot-ordered feature buffer), uses instead a static device array of
+ * ROCKET_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on every GPU
+ * it runs on until the process ends; the series go through it in chunks of
+ * at most 32 MiB of features (rows rounded down to a multiple of 64, at most
+ * 8,192).  Every call on a GPU shares that GPU's array: calls that overlap in
+ * time on one GPU (other streams, other plans) race on it, so the caller
+ * orders them, e.g. on one stream (each call ends, on hip_stream, after its
+ * last use of the array).  Nothing in the array needs clearing between calls.
+ * The plan's device must be the current device.  The array's address on a
+ * device is looked up on the first call there.
+ * Errors: those of rocket_transform_plan, plus ROCKET_ERR_INVALID_ARG when
+ *         the current device is not the plan's, ROCKET_ERR_SCRATCH when the
+ *         features of 64 short series (2 or 3 floats per kernel slot) exceed
+ *         half of the array (more than about 65,000 kernels), before any
+ *         device work; F is then untouched.
+ */
+#define ROCKET_NOALLOC_SCRATCH_BYTES (64u << 20)
+rocket_status rocket_transform_plan_noalloc(const rocket_plan *p, const float *X_dev, int64_t n,
+                                            float *F_dev, void *hip_stream);
 
 /*
  * One-shot transform: plan create + transform + plan destroy.  Returns after

@@ -223,6 +223,7 @@ extern "C" const char *rocket_status_string(rocket_status s) {
         case ROCKET_ERR_OOM: return "out of memory";
         case ROCKET_ERR_HIP: return "HIP runtime error";
         case ROCKET_ERR_INTERNAL: return "internal error";
+        case ROCKET_ERR_SCRATCH: return "request exceeds the library's static scratch";
     }
     return "unknown status";
 }

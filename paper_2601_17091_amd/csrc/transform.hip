@@ -1931,7 +1931,7 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
 }
 
 // Series-lane layout: the rows go in chunks; for each chunk the series
-// kernel writes the features in slot order into one half of the plan's
+// kernel writes the features in slot order into one half of a feature
 // buffer (each slot's features of 64 consecutive series are contiguous), and
 // the permutation kernel writes the chunk's F rows in the original kernel
 // order, 64 kernels (64 * nf floats) at a time.  The scatter of single
@@ -1940,30 +1940,31 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
 // stream, beside the next chunk's series kernel (compute-bound) on the
 // caller's; chunk i uses half i % 2, which it takes once the permutation of
 // chunk i - 2 is done with it.  The call ends on the caller's stream after
-// the last permutation.  The buffer holds at most 1 GiB (halves of up to
-// 8,192 rows).
-static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t n, float *F,
-                                   hipStream_t s) {
+// the last permutation.
+
+// Floats of one series' slot-ordered features.
+static int64_t series_slot_row_floats(const rocket_plan *p) {
+    return (int64_t)p->host.kid.size() * (p->mpv ? 3 : 2);
+}
+
+// Rows per chunk for halves of at most half_bytes (a multiple of 64, at
+// most 8,192 and no more than the call needs); 0 when not even 64 series fit.
+static int64_t series_chunk_rows(const rocket_plan *p, int64_t n, size_t half_bytes) {
+    const int64_t row_bytes = std::max<int64_t>(series_slot_row_floats(p), 1) * (int64_t)sizeof(float);
+    int64_t chunk = (int64_t)(half_bytes / (size_t)row_bytes) / kSeriesLanes * kSeriesLanes;
+    if (chunk < kSeriesLanes) return 0;
+    chunk = std::min<int64_t>(8192, chunk);
+    return std::min(chunk, (n + kSeriesLanes - 1) / kSeriesLanes * kSeriesLanes);
+}
+
+// The chunk loop over a two-half buffer of `chunk` rows per half.  The
+// caller holds p->scratch_mu (the plan's stream and events are shared by
+// every transform of the plan).
+static rocket_status enqueue_series(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                    hipStream_t s, float *buf, int64_t chunk) {
     const int64_t K = p->host.n_kernels;
-    const int64_t n_slots = (int64_t)p->host.kid.size();
     const int nf = p->mpv ? 3 : 2;
-    const int64_t slot_row_bytes = n_slots * nf * (int64_t)sizeof(float);
-    int64_t chunk = ((int64_t)1 << 29) / std::max<int64_t>(slot_row_bytes, 1);
-    chunk = std::max<int64_t>(kSeriesLanes, std::min<int64_t>(8192, chunk / kSeriesLanes * kSeriesLanes));
-    chunk = std::min(chunk, (n + kSeriesLanes - 1) / kSeriesLanes * kSeriesLanes);
-    const int64_t half = chunk * n_slots * nf;  // floats
-    const size_t need = (size_t)(2 * half) * sizeof(float);
-    std::lock_guard<std::mutex> lock(p->scratch_mu);
-    if (p->scratch_bytes < need) {
-        // hipFree waits for the work that still uses the old buffer
-        if (p->d_scratch && hipFree(p->d_scratch) != hipSuccess) return ROCKET_ERR_HIP;
-        p->d_scratch = nullptr;
-        p->scratch_bytes = 0;
-        if (hipMalloc(&p->d_scratch, need) != hipSuccess) return ROCKET_ERR_OOM;
-        p->scratch_bytes = need;
-    }
-    // the previous transform of this plan (on any stream) is done with it
-    if (hipStreamWaitEvent(s, p->scratch_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
+    const int64_t half = chunk * series_slot_row_floats(p);  // floats
     const void *pf = nf == 3 ? (const void *)rocket_slot_permute_kernel<3>
                              : (const void *)rocket_slot_permute_kernel<2>;
     // a failure part-way still ends with the tail below, so that the next
@@ -1973,7 +1974,7 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
     for (int64_t r0 = 0; r0 < n; r0 += chunk, ++i) {
         const int h = i & 1;
         const int64_t m = std::min(chunk, n - r0);
-        float *Sh = p->d_scratch + h * half;
+        float *Sh = buf + h * half;
         if (i >= 2 && hipStreamWaitEvent(s, p->half_free[h], 0) != hipSuccess) {
             st = ROCKET_ERR_HIP;
             break;
@@ -1995,7 +1996,8 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
         int32_t K32 = (int32_t)K;
         int64_t s_rows = chunk;
         float *Fc = F + r0 * K * nf;
-        void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&m, &Fc};
+        int64_t mm = m;
+        void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&mm, &Fc};
         if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, p->aux) != hipSuccess ||
             hipGetLastError() != hipSuccess || hipEventRecord(p->half_free[h], p->aux) != hipSuccess) {
             st = ROCKET_ERR_HIP;
@@ -2003,10 +2005,72 @@ static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t
         }
     }
     const bool tail_ok = hipEventRecord(p->aux_done, p->aux) == hipSuccess &&
-                         hipStreamWaitEvent(s, p->aux_done, 0) == hipSuccess &&
-                         hipEventRecord(p->scratch_done, s) == hipSuccess;
+                         hipStreamWaitEvent(s, p->aux_done, 0) == hipSuccess;
     if (st != ROCKET_OK) return st;
     return tail_ok ? ROCKET_OK : ROCKET_ERR_HIP;
+}
+
+// The plan's own feature buffer: at most 1 GiB (halves of up to 8,192 rows),
+// allocated on first use and grown as needed; transforms on different
+// streams take turns on it (each waits for the previous user's event).
+static rocket_status launch_series(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                   hipStream_t s) {
+    const int64_t chunk = std::max<int64_t>(kSeriesLanes, series_chunk_rows(p, n, (size_t)1 << 29));
+    const size_t need = (size_t)(2 * chunk * series_slot_row_floats(p)) * sizeof(float);
+    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    if (p->scratch_bytes < need) {
+        // hipFree waits for the work that still uses the old buffer
+        if (p->d_scratch && hipFree(p->d_scratch) != hipSuccess) return ROCKET_ERR_HIP;
+        p->d_scratch = nullptr;
+        p->scratch_bytes = 0;
+        if (hipMalloc(&p->d_scratch, need) != hipSuccess) return ROCKET_ERR_OOM;
+        p->scratch_bytes = need;
+    }
+    // the previous transform of this plan (on any stream) is done with it
+    if (hipStreamWaitEvent(s, p->scratch_done, 0) != hipSuccess) return ROCKET_ERR_HIP;
+    const rocket_status st = enqueue_series(p, X, n, F, s, p->d_scratch, chunk);
+    // recorded after the tail, also after a failure part-way
+    const bool rec_ok = hipEventRecord(p->scratch_done, s) == hipSuccess;
+    if (st != ROCKET_OK) return st;
+    return rec_ok ? ROCKET_OK : ROCKET_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of rocket_transform_plan_noalloc: the series-lane feature
+// buffer of callers that cannot allocate device memory.  Every GPU the
+// library runs on holds its own copy of the array (from the first use of the
+// library's code there until the process ends).  Host code uses the device
+// address that hipGetSymbolAddress returns for the current device, never the
+// array's name (a host-side stand-in).
+// ---------------------------------------------------------------------------
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;  // ROCKET_NOALLOC_SCRATCH_BYTES
+static_assert(kNoAllocScratchBytes == (size_t)ROCKET_NOALLOC_SCRATCH_BYTES, "header and library agree");
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+static std::mutex g_scratch_mu;
+static float *g_scratch_ptr[kMaxDevices];
+
+// The device address of `scratch` on `device` (which must be current),
+// looked up once per device.
+static rocket_status noalloc_scratch(int device, float **out) {
+    if (device < 0 || device >= kMaxDevices) return ROCKET_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return ROCKET_ERR_HIP;
+        g_scratch_ptr[device] = (float *)ptr;
+    }
+    *out = g_scratch_ptr[device];
+    return ROCKET_OK;
+}
+
+// The series-lane chunk loop over the static scratch (two halves of 32 MiB).
+static rocket_status launch_series_noalloc(const rocket_plan *p, const float *X, int64_t n, float *F,
+                                           hipStream_t s, float *buf) {
+    const int64_t chunk = series_chunk_rows(p, n, kNoAllocScratchBytes / 2);
+    if (chunk == 0) return ROCKET_ERR_SCRATCH;
+    std::lock_guard<std::mutex> lock(p->scratch_mu);
+    return enqueue_series(p, X, n, F, s, buf, chunk);
 }
 
 static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t n, float *F,
@@ -2022,6 +2086,23 @@ extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float
     if (!X_dev || !F_dev) return ROCKET_ERR_INVALID_ARG;
     hipStream_t s = (hipStream_t)hip_stream;
     return p->direct ? launch_direct(p, X_dev, n, F_dev, s) : launch_fused(p, X_dev, n, F_dev, s);
+}
+
+extern "C" rocket_status rocket_transform_plan_noalloc(const rocket_plan *p, const float *X_dev, int64_t n,
+                                                       float *F_dev, void *hip_stream) {
+    if (!p || n < 0) return ROCKET_ERR_INVALID_ARG;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return ROCKET_ERR_HIP;
+    if (dev != p->device) return ROCKET_ERR_INVALID_ARG;  // the plan's device must be current
+    float *buf = nullptr;
+    const rocket_status st = noalloc_scratch(dev, &buf);
+    if (st != ROCKET_OK) return st;
+    if (n == 0) return ROCKET_OK;
+    if (!X_dev || !F_dev) return ROCKET_ERR_INVALID_ARG;
+    hipStream_t s = (hipStream_t)hip_stream;
+    if (p->direct) return launch_direct(p, X_dev, n, F_dev, s);
+    if (p->series && n >= p->series_min_rows) return launch_series_noalloc(p, X_dev, n, F_dev, s, buf);
+    return launch_groups(p, false, X_dev, n, F_dev, nullptr, 0, s);
 }
 
 // Host-to-host transform with copies overlapped against the transform:

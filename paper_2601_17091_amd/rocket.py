@@ -21,6 +21,7 @@ ROCKET_ERR_LENGTH = -2
 ROCKET_ERR_OOM = -3
 ROCKET_ERR_HIP = -4
 ROCKET_ERR_INTERNAL = -5
+ROCKET_ERR_SCRATCH = -6
 ROCKET_PLAN_DEFAULT = 0
 ROCKET_PLAN_DIRECT = 1
 ROCKET_PLAN_CLAMPED = 2
@@ -38,6 +39,7 @@ EXPORTED = (
     "rocket_plan_create_ex",
     "rocket_plan_destroy",
     "rocket_transform_plan",
+    "rocket_transform_plan_noalloc",
     "rocket_transform",
     "rocket_transform_host",
     "rocket_plan_info",
@@ -127,6 +129,7 @@ def _signatures() -> dict:
         "rocket_plan_create_ex": ([kp, i32, ctypes.c_uint32, ctypes.POINTER(vp)], st),
         "rocket_plan_destroy": ([vp], None),
         "rocket_transform_plan": ([vp, vp, i64, vp, vp], st),
+        "rocket_transform_plan_noalloc": ([vp, vp, i64, vp, vp], st),
         "rocket_transform": ([vp, i64, i32, kp, vp, vp], st),
         "rocket_transform_host": ([vp, vp, i64, vp, i64, vp], st),
         "rocket_plan_info": ([vp, ctypes.POINTER(CPlanFacts)], st),
@@ -357,6 +360,13 @@ class Plan:
     def transform_into(self, X, F, stream=None):
         """F[n, fK] <- features of X[n, L] (f = 2, or 3 with MPV);
         asynchronous on `stream`."""
+        self._check_io(X, F)
+        _check(library().rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
+                                               ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
+               "rocket_transform_plan")
+        return F
+
+    def _check_io(self, X, F):
         import torch
         _check_series(X, self.L, self.n_channels)
         n = X.shape[0]
@@ -365,15 +375,21 @@ class Plan:
             raise ValueError("F must be contiguous float32 [n, %d] on the GPU" % self.n_features)
         if X.device != F.device:
             raise ValueError("X and F must be on the same device")
-        _check(library().rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), n,
-                                               ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
-               "rocket_transform_plan")
-        return F
 
     def transform(self, X, stream=None):
         import torch
         F = torch.empty((X.shape[0], self.n_features), dtype=torch.float32, device=X.device)
         return self.transform_into(X, F, stream)
+
+    def transform_into_noalloc(self, X, F, stream=None):
+        """transform_into through rocket_transform_plan_noalloc: no device
+        allocation in the library (the series-lane layout uses its static
+        scratch); the caller allocates F."""
+        self._check_io(X, F)
+        _check(library().rocket_transform_plan_noalloc(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
+                                                       ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
+               "rocket_transform_plan_noalloc")
+        return F
 
     def transform_host(self, X_host, F_host, batch_rows: int = 0, stream=None):
         """F_host[n, fK] <- features of X_host[n, L], both in host memory

@@ -44,7 +44,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings(lib):
-    for code in (0, -1, -2, -3, -4, -5):
+    for code in (0, -1, -2, -3, -4, -5, -6):
         assert rk.status_string(code) not in ("", "unknown status")
     assert rk.status_string(7) == "unknown status"
 
@@ -136,6 +136,7 @@ def test_transform_validation(lib):
     # n == 0 is a no-op that never touches memory
     assert lib.rocket_transform(None, 0, 100, ctypes.byref(c), None, None) == rb.ROCKET_OK
     assert lib.rocket_transform_plan(None, dummy, 1, dummy, None) == rb.ROCKET_ERR_INVALID_ARG
+    assert lib.rocket_transform_plan_noalloc(None, dummy, 1, dummy, None) == rb.ROCKET_ERR_INVALID_ARG
     assert lib.rocket_plan_info(None, None) == rb.ROCKET_ERR_INVALID_ARG
     assert lib.rocket_transform_host(None, dummy, 1, dummy, 0, None) == rb.ROCKET_ERR_INVALID_ARG
 
