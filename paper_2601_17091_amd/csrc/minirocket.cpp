@@ -12,6 +12,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <limits>
 #include <new>
 #include <vector>
 
@@ -200,6 +201,7 @@ rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan 
         }
         P.tail_pad = kTile;
         P.n_buckets = 2 * (int64_t)m->n_dilations;
+        const float inf = std::numeric_limits<float>::infinity();
         int64_t fstart = 0;  // first feature of the current dilation
         for (int32_t i = 0; i < m->n_dilations; ++i) {
             const int32_t d = m->dilations[i];
@@ -208,62 +210,40 @@ rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan 
                 const int32_t p = padded ? 4 * d : 0;
                 const int64_t O = L + 2 * (int64_t)p - 8 * (int64_t)d;
                 const int64_t n_tiles = (O + kTile - 1) / kTile;
-                std::vector<int> ks;
-                for (int k = 0; k < kMrKernels; ++k)
-                    if ((((i + k) % 2) == 0) == (padded == 1)) ks.push_back(k);
-                for (size_t pos = 0; pos < ks.size(); pos += kSlotsPerGroup) {
-                    const size_t take = std::min<size_t>(kSlotsPerGroup, ks.size() - pos);
-                    for (int32_t q0 = 0; q0 < nf; q0 += kMrMaxThresholds) {
-                        const int32_t nq = std::min(kMrMaxThresholds, nf - q0);
-                        ItemDesc it;
-                        std::memset(&it, 0, sizeof(it));
-                        it.variant = nq - 1;
-                        it.d = d;
-                        it.p = p;
-                        it.O = (int32_t)O;
-                        it.n_tiles = (int32_t)n_tiles;
-                        it.w_off = (int32_t)P.wpk.size();
-                        it.k_off = (int32_t)P.kid.size();
-                        it.cost = (int32_t)std::min<int64_t>(n_tiles * kMrTaps, INT32_MAX);
-                        it.n_ch = 1;
-                        it.ch_off = (int32_t)P.chan.size();
-                        P.chan.push_back(0);
-                        it.t_off = (int32_t)P.thr.size();
-                        it.nq = nq;
-                        it.inv_O = 1.0 / (double)O;
-                        // A-operand weights [tap][slot]; zeros for empty slots
-                        for (int j = 0; j < kMrTaps; ++j)
-                            for (int v = 0; v < kSlotsPerGroup; ++v) {
-                                double w[kMrTaps];
-                                float wv = 0.0f;
-                                if ((size_t)v < take) {
-                                    kernel_weights(ks[pos + v], w);
-                                    wv = (float)w[j];
-                                }
-                                P.wpk.push_back(wv);
-                            }
-                        // per slot: the feature of its first threshold here
-                        for (int v = 0; v < kSlotsPerGroup; ++v) {
-                            if ((size_t)v < take) {
-                                P.kid.push_back((int32_t)(fstart + (int64_t)ks[pos + v] * nf + q0));
-                            } else {
-                                P.kid.push_back(-1);
-                            }
-                            P.bias.push_back(0.0f);
-                        }
-                        // thresholds [q][slot]; empty slots never write
+                // kernels k = 2 kappa + par have i + k even (padded) or odd
+                const int par = padded ? (i & 1) : ((i + 1) & 1);
+                for (int32_t q0 = 0; q0 < nf;) {
+                    // chunks of 8 biases; a remainder of 1..4 takes a chunk of 4
+                    const int32_t rest = nf - q0;
+                    const int32_t nq = rest > kMrQSmall ? kMrQLarge : kMrQSmall;
+                    ItemDesc it;
+                    std::memset(&it, 0, sizeof(it));
+                    it.variant = 2 * par + (nq == kMrQLarge ? 1 : 0);
+                    it.d = d;
+                    it.p = p;
+                    it.O = (int32_t)O;
+                    it.n_tiles = (int32_t)n_tiles;
+                    it.w_off = (int32_t)fstart;
+                    it.k_off = q0;
+                    it.n_ch = nf;
+                    // per series: one compare per (kernel, bias, output)
+                    // plus the shared dot products (about 3 per kernel)
+                    it.cost = (int32_t)std::min<int64_t>(n_tiles * kMrKappa * (nq + 3), INT32_MAX);
+                    it.t_off = (int32_t)P.thr.size();
+                    it.nq = nq;
+                    it.inv_O = 1.0 / (double)O;
+                    // biases [kappa][q]; +inf for the dummies past nf
+                    for (int kappa = 0; kappa < kMrKappa; ++kappa)
                         for (int32_t q = 0; q < nq; ++q)
-                            for (int v = 0; v < kSlotsPerGroup; ++v)
-                                P.thr.push_back((size_t)v < take
-                                                    ? m->biases[fstart + (int64_t)ks[pos + v] * nf + q0 + q]
-                                                    : 0.0f);
-                        P.items.push_back(it);
-                        P.mfma_per_row += n_tiles * kMrTaps;
-                    }
+                            P.thr.push_back(q0 + q < nf ? m->biases[fstart + (int64_t)(2 * kappa + par) * nf + q0 + q]
+                                                        : inf);
+                    P.items.push_back(it);
+                    q0 += std::min(nq, rest);
                 }
             }
             fstart += (int64_t)kMrKernels * nf;
         }
+        P.n_variants = kMrNumVariants;
         build_item_orders(P);
         *out = std::move(P);
         return ROCKET_OK;

@@ -139,7 +139,7 @@ void build_item_orders(HostPlan &P) {
     for (int li = 0; li < kNumSplitLayouts; ++li) {
         const int ns = kSplitCounts[li];
         P.layout_off.push_back((int32_t)P.split_begin.size());
-        for (int v = 0; v < kNumVariants; ++v) {
+        for (int v = 0; v < P.n_variants; ++v) {
             std::vector<std::vector<int32_t>> lists(ns);
             std::vector<int64_t> load(ns, 0);
             for (int32_t it : by_cost) {

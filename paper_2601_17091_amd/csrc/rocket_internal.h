@@ -46,6 +46,10 @@ constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
 
 // One work item: up to 4*G kernels that share (length, dilation, padding),
 // so every slot has the same O outputs and reads the same series values.
+// MINIROCKET items use d, p, O, n_tiles, cost, t_off, nq and inv_O as named,
+// and three fields for their feature numbering: w_off = the first feature of
+// the item's dilation, k_off = the item's first bias (of each kernel), n_ch =
+// the dilation's features per kernel; variant = 2 * parity + (nq == 8).
 struct alignas(16) ItemDesc {
     int32_t variant;   // ell_index * 2 + (G - 1)
     int32_t d;         // dilation
@@ -57,8 +61,8 @@ struct alignas(16) ItemDesc {
     int32_t cost;      // MFMA instructions per series (scheduling weight)
     int32_t n_ch;      // channels the item's kernels read (their union; 1 if univariate)
     int32_t ch_off;    // first entry of the item's channel list
-    int32_t t_off;     // MINIROCKET: first threshold, [nq][4] floats
-    int32_t nq;        // MINIROCKET: thresholds (features) per slot in this item
+    int32_t t_off;     // MINIROCKET: first threshold, [kMrKappa][nq] floats
+    int32_t nq;        // MINIROCKET: thresholds per kernel in this item (kMrQSmall or kMrQLarge)
     uint32_t ch_mask[2];  // multichannel: the item's channels as a bit mask (lo, hi words)
     double inv_O;      // 1 / O rounded to double (exact PPV, see transform.hip)
 };
@@ -84,12 +88,17 @@ constexpr int kSeriesMaxL = 128;
 constexpr int kNumSplitLayouts = 6;  // 1, 2, 4, 8, 16, 32 splits
 constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 
-// MINIROCKET (Sec. 5 names it): 84 kernels of 9 taps; an item holds 4 of
-// them at one (dilation, padding) and up to kMrMaxThresholds of each pair's
-// biases, compared against the pair's dot products computed once.
+// MINIROCKET (Sec. 5 names it): 84 kernels of 9 taps.  Pair (dilation i,
+// kernel k) is padded when i + k is even, so at one (dilation, padding) the
+// kernels are those of one parity of k: an item holds those 42 kernels and
+// kMrQSmall or kMrQLarge of each kernel's biases (dummy biases of +inf fill
+// the last chunk; C > +inf never holds).
 constexpr int kMrKernels = 84;
 constexpr int kMrTaps = 9;
-constexpr int kMrMaxThresholds = 4;
+constexpr int kMrKappa = kMrKernels / 2;
+constexpr int kMrQSmall = 4;
+constexpr int kMrQLarge = 8;
+constexpr int kMrNumVariants = 4;  // parity x {kMrQSmall, kMrQLarge}
 
 struct HostPlan {
     bool minirocket = false;
@@ -112,7 +121,8 @@ struct HostPlan {
     std::vector<int32_t> chan;    // per item, its channel list (ascending)
     std::vector<float> thr;       // MINIROCKET: per item [nq][4] thresholds
     std::vector<int32_t> order;   // kNumSplitLayouts concatenated item orders
-    std::vector<int32_t> split_begin;  // per layout: kNumVariants*nsplit + 1 offsets into order
+    int32_t n_variants = kNumVariants;  // code variants of the plan's kernel (kMrNumVariants for MINIROCKET)
+    std::vector<int32_t> split_begin;  // per layout: n_variants*nsplit + 1 offsets into order
     std::vector<int32_t> layout_off;   // per layout: offset into split_begin
 };
 
@@ -126,8 +136,9 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
 rocket_status validate_minirocket(const rocket_minirocket_params *m);
 rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan *out);
 
-// Item orders: per variant, longest-processing-time split of the items into
-// every layout's split count (fills order, split_begin, layout_off).
+// Item orders: per variant (0 .. n_variants - 1), longest-processing-time
+// split of the items into every layout's split count (fills order,
+// split_begin, layout_off).
 void build_item_orders(HostPlan &P);
 
 // Element `index` of the SplitMix64 sequence started at `seed`.

@@ -23,10 +23,11 @@
 //      only the two counters per pair as well);
 //   6. PPV = count / O and MAX are written to F in the original kernel order.
 //
-// MINIROCKET kernel (the variant Sec. 5 names): the same staging, tiles and
-// MFMA contraction over 4 of its 84 fixed kernels at one (dilation,
-// padding), the chains starting from 0; each pair's dot products are then
-// compared with up to 4 of its biases, and PPV = count / O per (pair, bias).
+// MINIROCKET kernel (the variant Sec. 5 names): the same staging and tiles;
+// the dot products of its 42 kernels of one (dilation, padding) come from
+// the 9 shared tap values and their sum on the vector unit, and each is
+// compared with the item's biases of its kernel; PPV = count / O per
+// (kernel, bias).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -227,7 +228,7 @@ struct FusedArgs {
     const float *bias;
     const int32_t *kid;
     const int32_t *order;
-    const int32_t *split_begin;  // kNumVariants * nsplit + 1 offsets into order
+    const int32_t *split_begin;  // n_variants * nsplit + 1 offsets into order
     int32_t nsplit;
     int32_t n_variants;          // variants that have items, launched variant-major
     int32_t variants[rocket::kNumVariants];
@@ -1261,142 +1262,179 @@ __global__ __launch_bounds__(kBlock) void rocket_slot_permute_kernel(const float
 
 // ---------------------------------------------------------------------------
 // MINIROCKET (Dempster, Schmidt and Webb, KDD 2021; Sec. 5 names it as a
-// variant the same principle carries over to).  An item holds 4 of the 84
-// 9-tap kernels at one (dilation, padding) and NQ (1..4) of each pair's
-// biases.  The tiles' dot products are computed once, starting from 0, and
-// compared with each bias: feature (slot v, bias q) counts C_t > b_{v,q}.
+// variant the same principle carries over to).  Its 84 kernels have 9 taps,
+// weight 2 on a choice of 3 taps (a, b, c) and -1 on the other six, so a dot
+// product is
+//     C = 3 (x_a + x_b + x_c) - (x_0 + ... + x_8).
+// An item holds the 42 kernels of one parity at one (dilation, padding)
+// (the pair (dilation i, kernel k) is padded when i + k is even) and NQ (4 or
+// 8) of each kernel's biases.  For each tile of 64 output positions the nine
+// tap values are read from LDS once and their sum S is formed once, by a
+// pairwise tree, for all 42 kernels; a kernel then costs two adds and one
+// fma on the vector unit,
+//     C = fma(3, (x_a + x_b) + x_c, -S),
+// instead of nine multiply-adds.  Rounding: |C - C_exact| <= 3 gamma_2
+// sum_chosen |x| + gamma_4 sum_all |x| + u |C|, about 12u sum_chosen |x| +
+// 5u sum_others |x| (u = 2^-24), inside the gamma_9 sum_j |w_j x_j| = 18u
+// sum_chosen |x| + 9u sum_others |x| that bounds any 9-term fp32 evaluation
+// (additions of subnormals are exact, so no underflow term is added).
+// Feature (kernel, bias b) counts C > b: one compare per tile, a ballot
+// popcounted on the scalar unit.
 // ---------------------------------------------------------------------------
 
-// Fold NT tiles into the counts: the count of (slot V, bias Q) over the
-// block is a ballot popcount summed on the scalar unit, then written into
-// lane V*NQ + Q of a vector register (the counts of all (slot, bias) pairs
-// would not fit the scalar registers; v_writelane takes a constant lane).
-template <int V, int Q, int NQ, int NT>
-struct MrFold {
-    __device__ __forceinline__ static void run(const v4f (&acc)[NT][1], const float (&thr)[4][NQ],
-                                               uint32_t &part) {
-        uint32_t s = 0;
+using rocket::kMrKappa;
+constexpr int kMrTiles = 4;  // tiles per block (the last 0..3 tiles run one at a time)
+
+// Tap `which` (0, 1, 2 for a < b < c) of MINIROCKET kernel k: the k-th choice
+// of 3 of the 9 taps in lexicographic order.
+constexpr int mr_tap(int k, int which) {
+    int n = 0;
+    for (int a = 0; a < 9; ++a)
+        for (int b = a + 1; b < 9; ++b)
+            for (int c = b + 1; c < 9; ++c) {
+                if (n == k) return which == 0 ? a : (which == 1 ? b : c);
+                ++n;
+            }
+    return -1;
+}
+static_assert(mr_tap(0, 0) == 0 && mr_tap(0, 2) == 2 && mr_tap(83, 0) == 6 && mr_tap(83, 2) == 8,
+              "84 lexicographic choices of 3 of 9 taps");
+
+// Count registers of an item: feature g = kappa * NQ + q (kernel 2 kappa +
+// parity, bias q) lives in lane g % 64 of register g / 64.
+template <int NQ>
+constexpr int mr_regs() { return (kMrKappa * NQ + 63) / 64; }
+
+// The count of feature G over the block's NT tiles (a ballot popcount per
+// tile, summed on the scalar unit) into its lane of the block's partial
+// counts.
+template <int G, int NT>
+__device__ __forceinline__ void mr_count(const float (&C)[NT], float b, uint32_t &part) {
+    uint32_t s = 0;
 #pragma unroll
-        for (int u = 0; u < NT; ++u) s += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(acc[u][0][V] > thr[V][Q]));
-        asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(part) : "s"(s), "i"(V * NQ + Q));
-        constexpr int V2 = Q + 1 < NQ ? V : V + 1;
-        constexpr int Q2 = Q + 1 < NQ ? Q + 1 : 0;
-        MrFold<V2, Q2, NQ, NT>::run(acc, thr, part);
-    }
-};
-template <int Q, int NQ, int NT>
-struct MrFold<4, Q, NQ, NT> {
-    __device__ __forceinline__ static void run(const v4f (&)[NT][1], const float (&)[4][NQ], uint32_t &) {}
-};
-
-// part: lanes past 4*NQ stay 0 (set once per item), the others are
-// overwritten by every block
-template <int NT, int NQ>
-__device__ __forceinline__ void mr_reduce(const v4f (&acc)[NT][1], const float (&thr)[4][NQ],
-                                          uint32_t &part, uint32_t &cnt) {
-    MrFold<0, 0, NQ, NT>::run(acc, thr, part);
-    cnt += part;
+    for (int u = 0; u < NT; ++u) s += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(C[u] > b));
+    asm volatile("v_writelane_b32 %0, %1, %2" : "+v"(part) : "s"(s), "i"(G % 64));
 }
 
-template <int NT, bool LAST, int NQ, typename Src>
-__device__ __forceinline__ void mr_block(const Src &src, const float (&wa)[1][rocket::kMrTaps],
-                                         const v4f (&z)[1], const v4f (&zlast)[1],
-                                         const float (&thr)[4][NQ], uint32_t &part, uint32_t &cnt) {
-    v4f acc[NT][1];
-    tile_mfma<rocket::kMrTaps, 1, NT, LAST, true>(src, wa, z, zlast, acc);
-    __builtin_amdgcn_sched_barrier(0);
-    // raised wave priority over the compares, as in the fused kernel's
-    // block reduction (measured: 1.5 % faster MINIROCKET passes)
-    __builtin_amdgcn_s_setprio(1);
-    mr_reduce<NT, NQ>(acc, thr, part, cnt);
-    __builtin_amdgcn_s_setprio(0);
-}
-
-// The last block of a series: its tile count nv (1..N) selects a code copy.
-template <int N, int NQ, typename Src>
-struct MrTail {
-    __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[1][rocket::kMrTaps],
-                                               const v4f (&z)[1], const v4f (&zlast)[1],
-                                               const float (&thr)[4][NQ], uint32_t &part, uint32_t &cnt) {
-        if (nv == N)
-            mr_block<N, true, NQ>(src, wa, z, zlast, thr, part, cnt);
-        else
-            MrTail<N - 1, NQ, Src>::run(nv, src, wa, z, zlast, thr, part, cnt);
+template <int KAPPA, int Q, int NQ, int NT, int R>
+struct MrCounts {
+    __device__ __forceinline__ static void run(const float (&C)[NT], const float (&b)[NQ], uint32_t (&part)[R]) {
+        constexpr int G = KAPPA * NQ + Q;
+        mr_count<G, NT>(C, b[Q], part[G / 64]);
+        MrCounts<KAPPA, Q + 1, NQ, NT, R>::run(C, b, part);
     }
 };
-template <int NQ, typename Src>
-struct MrTail<0, NQ, Src> {
-    __device__ __forceinline__ static void run(int, const Src &, const float (&)[1][rocket::kMrTaps],
-                                               const v4f (&)[1], const v4f (&)[1], const float (&)[4][NQ],
-                                               uint32_t &, uint32_t &) {}
+template <int KAPPA, int NQ, int NT, int R>
+struct MrCounts<KAPPA, NQ, NQ, NT, R> {
+    __device__ __forceinline__ static void run(const float (&)[NT], const float (&)[NQ], uint32_t (&)[R]) {}
 };
 
-template <int NQ, bool CLAMP>
+// Kernels 2 KAPPA + PAR, KAPPA = KAPPA0 .. 41, over the block's NT tiles: the
+// dot products from the shared tap values and sum, then the compares.  Each
+// kernel's section is closed by a scheduling barrier and loads the next
+// kernel's biases (scalar loads) while its own compares run, so only two
+// kernels' biases are live in scalar registers.
+template <int PAR, int KAPPA, int NQ, int NT, int R>
+struct MrKernels {
+    __device__ __forceinline__ static void run(const float (&x)[9][NT], const float (&S)[NT],
+                                               ConstPtr<float> thr, const float (&b)[NQ], uint32_t (&part)[R]) {
+        constexpr int k = 2 * KAPPA + PAR;
+        constexpr int ta = mr_tap(k, 0), tb = mr_tap(k, 1), tc = mr_tap(k, 2);
+        float bn[NQ];
+        if constexpr (KAPPA + 1 < kMrKappa) {
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) bn[q] = thr[(KAPPA + 1) * NQ + q];
+        }
+        float C[NT];
+#pragma unroll
+        for (int u = 0; u < NT; ++u) C[u] = fmaf(3.0f, (x[ta][u] + x[tb][u]) + x[tc][u], -S[u]);
+        MrCounts<KAPPA, 0, NQ, NT, R>::run(C, b, part);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (KAPPA + 1 < kMrKappa) MrKernels<PAR, KAPPA + 1, NQ, NT, R>::run(x, S, thr, bn, part);
+    }
+};
+
+// One block of NT tiles of an item over one series.  rem = outputs of the
+// block's last tile (64 unless it is the series' last tile): lanes past it
+// get S = +inf, so C = -inf there and no bias is exceeded.
+template <int PAR, int NQ, int NT, typename Src>
+__device__ __forceinline__ void mr_block(const Src &src, ConstPtr<float> thr, int rem, int lane,
+                                         uint32_t (&part)[mr_regs<NQ>()], uint32_t (&cnt)[mr_regs<NQ>()]) {
+    float x[9][NT];
+#pragma unroll
+    for (int j = 0; j < 9; ++j) lds_tiles<NT>(src.m0(j), x[j]);
+    float S[NT];
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+        S[u] = (((x[0][u] + x[1][u]) + (x[2][u] + x[3][u])) + ((x[4][u] + x[5][u]) + (x[6][u] + x[7][u]))) +
+               x[8][u];
+    S[NT - 1] = lane < rem ? S[NT - 1] : INFINITY;
+    // a fresh copy of the bias pointer per block keeps the bias loads inside
+    // the block (hoisted out of the row loop, 42 * NQ biases would not fit
+    // the scalar registers)
+    uint64_t tp = (uint64_t)(__UINTPTR_TYPE__)thr;
+    asm volatile("" : "+s"(tp));
+    const ConstPtr<float> tb = (ConstPtr<float>)(__UINTPTR_TYPE__)tp;
+    float b0[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) b0[q] = tb[q];
+    MrKernels<PAR, 0, NQ, NT, mr_regs<NQ>()>::run(x, S, tb, b0, part);
+#pragma unroll
+    for (int r = 0; r < mr_regs<NQ>(); ++r) cnt[r] += part[r];
+}
+
+template <int PAR, int NQ, bool CLAMP>
 __device__ __forceinline__ void run_mr_item(const ItemDesc &it, const float *rows0, int nrows,
                                             const FusedArgs &a, float *F0, int lane) {
-    constexpr int ELL = rocket::kMrTaps;
-    constexpr int NT = rocket::kTilesPerBlock[0];
-    float wa[1][ELL];
+    constexpr int NT = kMrTiles;
+    constexpr int R = mr_regs<NQ>();
+    const ConstPtr<float> thr = as_const(a.thr) + it.t_off;
+    // the feature each lane writes from each count register (-1: none)
+    int64_t fidx[R];
 #pragma unroll
-    for (int j = 0; j < ELL; ++j) wa[0][j] = a.wpk[it.w_off + j * 4 + (lane & 3)];
-    // the biases, copied into vector registers once per item (opaque
-    // copies, so the compiler keeps them there rather than in scalar
-    // registers it would have to spill)
-    float thr[4][NQ];
-#pragma unroll
-    for (int q = 0; q < NQ; ++q)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const float t = as_const(a.thr)[it.t_off + q * 4 + v];
-            asm volatile("v_mov_b32 %0, %1" : "=v"(thr[v][q]) : "s"(t));
-        }
-    // start values: 0, and -inf on the lanes past the last output in the
-    // last tile of a series
-    const int rem = it.O - (it.n_tiles - 1) * kTile;
-    v4f z[1], zlast[1];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        float zv;
-        asm volatile("v_mov_b32 %0, 0" : "=v"(zv));
-        z[0][v] = zv;
-        zlast[0][v] = lane < rem ? zv : -INFINITY;
+    for (int r = 0; r < R; ++r) {
+        const int g = 64 * r + lane;
+        const int kappa = g / NQ, q = g % NQ;
+        fidx[r] = (kappa < kMrKappa && it.k_off + q < it.n_ch)
+                      ? (int64_t)it.w_off + (int64_t)(2 * kappa + PAR) * it.n_ch + it.k_off + q
+                      : -1;
     }
-    // lane v*NQ + q writes feature (slot v, bias q) of the item
-    int myf = -1;
-    if (lane < 4 * NQ) {
-        const int k0 = a.kid[it.k_off + lane / NQ];
-        myf = k0 >= 0 ? k0 + lane % NQ : -1;
-    }
+    uint32_t part[R], cnt[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) part[r] = cnt[r] = 0;  // lanes past 42 * NQ stay 0
+    const int rem = it.O - (it.n_tiles - 1) * kTile;  // outputs in the last tile, 1..64
+    const int nfull = it.n_tiles / NT;                // blocks of NT tiles
+    const int ntail = it.n_tiles - nfull * NT;        // then 0..NT-1 single tiles
     const int row_pitch = a.row_stride;
-    const int nfull = (it.n_tiles - 1) / NT;
-    const int nv = it.n_tiles - nfull * NT;
     const int64_t f_stride = (int64_t)a.nf * a.K;
-    uint32_t part = 0;
     for (int r = 0; r < nrows; ++r) {
-        // lane v*NQ + q counts the outputs above bias q of slot v
-        uint32_t cnt = 0;
         const uint32_t row = lds_addr(rows0 + r * row_pitch);
         for (int blk = 0; blk < nfull; ++blk) {
             const int b0 = blk * (NT * kTile) - it.p;
+            const int rb = (ntail == 0 && blk == nfull - 1) ? rem : kTile;
             if constexpr (CLAMP)
-                mr_block<NT, false, NQ>(ClampedTiles{row, b0, it.d, a.L}, wa, z, zlast, thr, part, cnt);
+                mr_block<PAR, NQ, NT>(ClampedTiles{row, b0, it.d, a.L}, thr, rb, lane, part, cnt);
             else
-                mr_block<NT, false, NQ>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, z, zlast, thr, part,
-                                        cnt);
+                mr_block<PAR, NQ, NT>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, thr, rb, lane, part, cnt);
         }
-        const int b0 = nfull * (NT * kTile) - it.p;
-        if constexpr (CLAMP)
-            MrTail<NT, NQ, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, z, zlast, thr, part,
-                                              cnt);
-        else
-            MrTail<NT, NQ, PaddedTiles>::run(nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, z, zlast,
-                                             thr, part, cnt);
-        // PPV = count / O, correctly rounded as in write_row
-        if (myf >= 0) F0[r * f_stride + myf] = (float)((double)cnt * it.inv_O);
+        for (int t = 0; t < ntail; ++t) {
+            const int b0 = (nfull * NT + t) * kTile - it.p;
+            const int rb = t == ntail - 1 ? rem : kTile;
+            if constexpr (CLAMP)
+                mr_block<PAR, NQ, 1>(ClampedTiles{row, b0, it.d, a.L}, thr, rb, lane, part, cnt);
+            else
+                mr_block<PAR, NQ, 1>(PaddedTiles{row + 4u * (uint32_t)b0, it.d}, thr, rb, lane, part, cnt);
+        }
+        // PPV = count / O, correctly rounded as in write_features
+#pragma unroll
+        for (int rr = 0; rr < R; ++rr) {
+            if (fidx[rr] >= 0) F0[r * f_stride + fidx[rr]] = (float)((double)cnt[rr] * it.inv_O);
+            cnt[rr] = 0;
+        }
     }
 }
 
-template <int NQ, bool CLAMP>
+template <int PAR, int NQ, bool CLAMP>
 __device__ __forceinline__ void run_mr_items(int *next_item, int beg, int cnt_items, const float *rows0,
                                              int nrows, const FusedArgs &a, float *F0, int lane) {
     while (true) {
@@ -1405,11 +1443,11 @@ __device__ __forceinline__ void run_mr_items(int *next_item, int beg, int cnt_it
         idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
         if (idx >= cnt_items) break;
         const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
-        run_mr_item<NQ, CLAMP>(it, rows0, nrows, a, F0, lane);
+        run_mr_item<PAR, NQ, CLAMP>(it, rows0, nrows, a, F0, lane);
     }
 }
 
-// MINIROCKET workgroup: as rocket_fused_kernel; the variant is NQ - 1.
+// MINIROCKET workgroup: as rocket_fused_kernel; variant = 2 * parity + (NQ == 8).
 template <int BLOCK, bool CLAMP>
 __global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
     extern __shared__ float smem[];
@@ -1421,10 +1459,10 @@ __global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
     const float *rows0 = smem + a.halo_lo;
     const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
     switch (w.variant) {
-        case 0: run_mr_items<1, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 1: run_mr_items<2, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 2: run_mr_items<3, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        default: run_mr_items<4, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 0: run_mr_items<0, rocket::kMrQSmall, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 1: run_mr_items<0, rocket::kMrQLarge, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 2: run_mr_items<1, rocket::kMrQSmall, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        default: run_mr_items<1, rocket::kMrQLarge, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
     }
 }
 
@@ -1870,8 +1908,9 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     // while others finish)
     const bool big_group = !series && row_bytes * p->C > kBigLds;
     const int min_items = big_group ? 4 * (kBigBlock / 64) : 2 * (kBlock / 64);
+    const int n_var = p->host.n_variants;
     int64_t n_present = 0;
-    for (int v = 0; v < rocket::kNumVariants; ++v)
+    for (int v = 0; v < n_var; ++v)
         if (p->host.split_begin[v + 1] > p->host.split_begin[v]) ++n_present;
     n_present = std::max<int64_t>(n_present, 1);
     const int64_t per_variant = (int64_t)p->host.items.size() / n_present;
@@ -1899,7 +1938,7 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     a.split_begin = p->d_split_begin + p->host.layout_off[li];
     a.nsplit = nsplit;
     a.n_variants = 0;
-    for (int v = 0; v < rocket::kNumVariants; ++v) {
+    for (int v = 0; v < n_var; ++v) {
         const int32_t *sb = p->host.split_begin.data() + p->host.layout_off[li];
         if (sb[(v + 1) * nsplit] > sb[v * nsplit]) a.variants[a.n_variants++] = v;
     }
