@@ -198,6 +198,11 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             halo_hi = std::max<int64_t>(halo_hi, (int64_t)p + (ell_eff - len) * (int64_t)d);
         }
         P.n_buckets = (int64_t)buckets.size();
+        // margins rounded so that the series starts, and every staged row
+        // spans, a whole number of 16-byte words: rows are then staged with
+        // 16-byte loads and LDS writes (for series lengths divisible by 4)
+        halo_lo = (halo_lo + 3) / 4 * 4;
+        halo_hi += (4 - (halo_lo + L + halo_hi) % 4) % 4;
         const int64_t stride = halo_lo + L + halo_hi;
         if (stride > (int64_t)1 << 30) {
             // cannot be staged; the plan will use the direct kernel

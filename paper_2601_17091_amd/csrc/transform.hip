@@ -237,6 +237,8 @@ struct FusedArgs {
     int32_t row_stride;
     int32_t tail_pad;        // zero floats staged after the last row
     int32_t rows_per_block;  // series staged together in one workgroup's LDS
+    int32_t vec4;            // 1: rows are staged with 16-byte loads and LDS writes (L, halo_lo and
+                             // row_stride multiples of 4 floats, X 16-byte aligned)
     float *S;                // series-lane layout: features in slot order (see below)
     int64_t s_rows;          // rows one slot column of S holds
 };
@@ -923,12 +925,26 @@ template <int BLOCK>
 __device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int *next_item,
                                             GroupWork &w) {
     if (!group_work(a, w)) return false;
-    for (int rc = 0; rc < w.nrows * a.C; ++rc) {
-        const float *x = a.X + ((w.grow * a.C) + rc) * (int64_t)a.L;
-        float *dst = smem + rc * a.row_stride;
-        for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
-            const int m = e - a.halo_lo;
-            dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
+    if (a.vec4) {
+        // 4 floats per lane: the series and both margins are whole 16-byte
+        // words, so no word straddles a margin
+        const int stride4 = a.row_stride >> 2, lo4 = a.halo_lo >> 2, L4 = a.L >> 2;
+        for (int rc = 0; rc < w.nrows * a.C; ++rc) {
+            const float4 *x = reinterpret_cast<const float4 *>(a.X + ((w.grow * a.C) + rc) * (int64_t)a.L);
+            float4 *dst = reinterpret_cast<float4 *>(smem + rc * a.row_stride);
+            for (int e = threadIdx.x; e < stride4; e += BLOCK) {
+                const int m = e - lo4;
+                dst[e] = (m >= 0 && m < L4) ? x[m] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            }
+        }
+    } else {
+        for (int rc = 0; rc < w.nrows * a.C; ++rc) {
+            const float *x = a.X + ((w.grow * a.C) + rc) * (int64_t)a.L;
+            float *dst = smem + rc * a.row_stride;
+            for (int e = threadIdx.x; e < a.row_stride; e += BLOCK) {
+                const int m = e - a.halo_lo;
+                dst[e] = (m >= 0 && m < a.L) ? x[m] : 0.0f;
+            }
         }
     }
     // zeros after the last row: lanes past the last output of an item read
@@ -943,7 +959,7 @@ __device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int
 // group in LDS and runs the items of one variant over it.
 template <int BLOCK, bool CLAMP, bool MPV, bool MC>
 __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
-    extern __shared__ float smem[];
+    extern __shared__ __align__(16) float smem[];
     __shared__ int next_item;
     GroupWork w;
     if (!stage_group<BLOCK>(a, smem, &next_item, w)) return;
@@ -1450,7 +1466,7 @@ __device__ __forceinline__ void run_mr_items(int *next_item, int beg, int cnt_it
 // MINIROCKET workgroup: as rocket_fused_kernel; variant = 2 * parity + (NQ == 8).
 template <int BLOCK, bool CLAMP>
 __global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
-    extern __shared__ float smem[];
+    extern __shared__ __align__(16) float smem[];
     __shared__ int next_item;
     GroupWork w;
     if (!stage_group<BLOCK>(a, smem, &next_item, w)) return;
@@ -1597,9 +1613,15 @@ struct rocket_plan {
     mutable size_t scratch_bytes = 0;
     mutable hipEvent_t scratch_done = nullptr;
     hipStream_t aux = nullptr;
+    // the series kernels of odd chunks run on this stream (even ones on the
+    // caller's), so that consecutive chunks overlap instead of draining the
+    // GPU between them
+    hipStream_t odd = nullptr;
     hipEvent_t half_full[2] = {nullptr, nullptr};
     hipEvent_t half_free[2] = {nullptr, nullptr};
     hipEvent_t aux_done = nullptr;
+    hipEvent_t call_start = nullptr;  // the caller's stream at the start of a call (odd waits on it)
+    hipEvent_t odd_done = nullptr;    // the odd stream's last chunk of a call
     bool mpv = false;        // third feature per kernel: mean of positive values
     bool minirocket = false; // MINIROCKET plan: F [n, n_features], PPV only
     int64_t f_cols = 0;      // columns of F
@@ -1629,9 +1651,11 @@ struct rocket_plan {
 
 static void plan_free_device(rocket_plan *p) {
     if (p->scratch_done) (void)hipEventDestroy(p->scratch_done);
-    for (hipEvent_t ev : {p->half_full[0], p->half_full[1], p->half_free[0], p->half_free[1], p->aux_done})
+    for (hipEvent_t ev : {p->half_full[0], p->half_full[1], p->half_free[0], p->half_free[1], p->aux_done,
+                          p->call_start, p->odd_done})
         if (ev) (void)hipEventDestroy(ev);
     if (p->aux) (void)hipStreamDestroy(p->aux);
+    if (p->odd) (void)hipStreamDestroy(p->odd);
     void *ptrs[] = {p->d_scratch, p->d_slot_of, p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
                     p->d_split_begin, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
@@ -1774,9 +1798,10 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
         }
         e = upload(slot_of, &p->d_slot_of);
         for (hipEvent_t *ev : {&p->scratch_done, &p->half_full[0], &p->half_full[1], &p->half_free[0],
-                               &p->half_free[1], &p->aux_done})
+                               &p->half_free[1], &p->aux_done, &p->call_start, &p->odd_done})
             if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->odd, hipStreamNonBlocking);
     }
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
@@ -1946,6 +1971,10 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     a.row_stride = p->row_stride;
     a.tail_pad = p->tail_pad;
     a.rows_per_block = R;
+    a.vec4 = (a.L % 4 == 0 && a.halo_lo % 4 == 0 && a.row_stride % 4 == 0 && a.tail_pad % 4 == 0 &&
+              ((uintptr_t)X % 16) == 0)
+                 ? 1
+                 : 0;
     a.S = S;
     a.s_rows = s_rows;
     const int64_t max_rows =
@@ -1996,9 +2025,12 @@ static int64_t series_chunk_rows(const rocket_plan *p, int64_t n, size_t half_by
     return std::min(chunk, (n + kSeriesLanes - 1) / kSeriesLanes * kSeriesLanes);
 }
 
-// The chunk loop over a two-half buffer of `chunk` rows per half.  The
-// caller holds p->scratch_mu (the plan's stream and events are shared by
-// every transform of the plan).
+// The chunk loop over a two-half buffer of `chunk` rows per half.  Chunk i
+// runs its series kernel on the caller's stream (i even) or on the plan's
+// odd-chunk stream (i odd), so each stream only ever uses its own half, and
+// consecutive chunks overlap; the permutations run in chunk order on the
+// plan's permutation stream.  The caller holds p->scratch_mu (the plan's
+// streams and events are shared by every transform of the plan).
 static rocket_status enqueue_series(const rocket_plan *p, const float *X, int64_t n, float *F,
                                     hipStream_t s, float *buf, int64_t chunk) {
     const int64_t K = p->host.n_kernels;
@@ -2009,18 +2041,23 @@ static rocket_status enqueue_series(const rocket_plan *p, const float *X, int64_
     // a failure part-way still ends with the tail below, so that the next
     // transform of this plan waits for whatever this one enqueued
     rocket_status st = ROCKET_OK;
+    // the odd-chunk stream starts after the caller's earlier work (X ready,
+    // the previous user of the buffer done)
+    if (hipEventRecord(p->call_start, s) != hipSuccess || hipStreamWaitEvent(p->odd, p->call_start, 0) != hipSuccess)
+        st = ROCKET_ERR_HIP;
     int i = 0;
-    for (int64_t r0 = 0; r0 < n; r0 += chunk, ++i) {
+    for (int64_t r0 = 0; r0 < n && st == ROCKET_OK; r0 += chunk, ++i) {
         const int h = i & 1;
+        hipStream_t sh = h ? p->odd : s;
         const int64_t m = std::min(chunk, n - r0);
         float *Sh = buf + h * half;
-        if (i >= 2 && hipStreamWaitEvent(s, p->half_free[h], 0) != hipSuccess) {
+        if (i >= 2 && hipStreamWaitEvent(sh, p->half_free[h], 0) != hipSuccess) {
             st = ROCKET_ERR_HIP;
             break;
         }
-        st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, Sh, chunk, s);
+        st = launch_groups(p, true, X + r0 * p->host.L, m, nullptr, Sh, chunk, sh);
         if (st != ROCKET_OK) break;
-        if (hipEventRecord(p->half_full[h], s) != hipSuccess ||
+        if (hipEventRecord(p->half_full[h], sh) != hipSuccess ||
             hipStreamWaitEvent(p->aux, p->half_full[h], 0) != hipSuccess) {
             st = ROCKET_ERR_HIP;
             break;
@@ -2044,7 +2081,9 @@ static rocket_status enqueue_series(const rocket_plan *p, const float *X, int64_
         }
     }
     const bool tail_ok = hipEventRecord(p->aux_done, p->aux) == hipSuccess &&
-                         hipStreamWaitEvent(s, p->aux_done, 0) == hipSuccess;
+                         hipStreamWaitEvent(s, p->aux_done, 0) == hipSuccess &&
+                         hipEventRecord(p->odd_done, p->odd) == hipSuccess &&
+                         hipStreamWaitEvent(s, p->odd_done, 0) == hipSuccess;
     if (st != ROCKET_OK) return st;
     return tail_ok ? ROCKET_OK : ROCKET_ERR_HIP;
 }
