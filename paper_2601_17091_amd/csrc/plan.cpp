@@ -159,7 +159,106 @@ void build_item_orders(HostPlan &P) {
     }
 }
 
+// Toeplitz items (variants kToepVariant0..): the one (sigma = 4) or two
+// (sigma = 2) leftover kernels of a bucket at dilation d.  Per super-tile of
+// sigma * d outputs per kernel: ceil(d / 64) chunks of ell + sigma - 1 MFMAs,
+// each computing 4 x 64 outputs; the last super-tile covers what is left of
+// O.  A VALU item costs ell fp32 FMAs per kernel per 64 outputs.
+struct ToepShape {
+    int sigma;
+    int64_t nc;       // chunks per super-tile
+    int64_t s_full;   // whole super-tiles
+    int64_t n_last;   // chunks of the last, partial super-tile
+    int64_t chunks;   // chunks per series
+};
+static ToepShape toeplitz_shape(int nk, int32_t d, int64_t O) {
+    ToepShape t;
+    t.sigma = 4 / nk;
+    t.nc = ceil_div(d, kTile);
+    const int64_t span = (int64_t)t.sigma * d;
+    t.s_full = O / span;
+    const int64_t rest = O - t.s_full * span;
+    t.n_last = rest > 0 ? ceil_div(std::min<int64_t>(rest, d), kTile) : 0;
+    t.chunks = t.s_full * t.nc + t.n_last;
+    return t;
+}
+
+template <typename KS>
+static bool toeplitz_pays(const KS &ks, size_t pos, size_t nk, int ell, int32_t d, int64_t O,
+                          const rocket_kernels *k) {
+    // the kernels must fill their frame (first frame tap 0, full length)
+    for (size_t s = 0; s < nk; ++s)
+        if (ks[pos + s].second != 0 || k->length[ks[pos + s].first] != ell) return false;
+    const ToepShape t = toeplitz_shape((int)nk, d, O);
+    // issue cycles per series: fp32 FMA 4.5, 4x4x1 fp32 MFMA 8.7, 1.5 vector
+    // instructions to reduce a result register; the chunks of the last
+    // super-tile also build their per-slot start values (about 10 more)
+    const double valu = (double)ceil_div(O, kTile) * nk * (ell * 4.5 + 1.5 * 4.5);
+    const double toep = (double)t.chunks * ((ell + t.sigma - 1) * 8.7 + 4 * 1.5 * 4.5) + (double)t.n_last * 45.0;
+    return toep < 0.9 * valu;
+}
+
+template <typename KS>
+static void add_toeplitz_item(HostPlan &P, const KS &ks, size_t pos, int nk, int eidx, int32_t d, int32_t p,
+                              int64_t O, int32_t L, const rocket_kernels *k) {
+    const int ell = kEllValues[eidx];
+    const ToepShape t = toeplitz_shape(nk, d, O);
+    const int taps = ell + t.sigma - 1;
+    ItemDesc it;
+    std::memset(&it, 0, sizeof(it));
+    it.variant = kToepVariant0 + eidx * 2 + (nk - 1);
+    it.d = d;
+    it.p = p;
+    it.O = (int32_t)O;
+    it.n_tiles = (int32_t)t.nc;
+    it.w_off = (int32_t)P.wpk.size();
+    it.k_off = (int32_t)P.kid.size();
+    it.cost = (int32_t)std::min<int64_t>(t.chunks * taps, INT32_MAX);
+    it.n_ch = 1;
+    it.ch_off = (int32_t)P.chan.size();
+    P.chan.push_back(0);
+    it.ch_mask[0] = 1u;
+    it.inv_O = 1.0 / (double)O;
+    // weights [tap m][slot s]: kernel s / sigma at shift s % sigma
+    for (int m = 0; m < taps; ++m)
+        for (int s = 0; s < 4; ++s) {
+            const int32_t kk = ks[pos + (size_t)(s / t.sigma)].first;
+            const int j = m - s % t.sigma;
+            P.wpk.push_back(j >= 0 && j < ell ? k->weights[(int64_t)kk * k->max_len + j] : 0.0f);
+        }
+    // slots: the kernel id on the first slot of each kernel (its writer),
+    // every slot carries its kernel's bias
+    for (int s = 0; s < 4; ++s) {
+        const int32_t kk = ks[pos + (size_t)(s / t.sigma)].first;
+        P.kid.push_back(s % t.sigma == 0 ? kk : -1);
+        P.bias.push_back(k->bias[kk]);
+    }
+    P.items.push_back(it);
+    P.mfma_per_row += t.chunks * taps;
+    (void)L;
+}
+
+static rocket_status build_plan(const rocket_kernels *k, int32_t L, bool allow_toeplitz, HostPlan *out);
+
+// Toeplitz items run in a launch of their own, which stages every row group
+// again: they are kept only where they carry a real share of the work (at
+// least kToepMinShare of the items' cost), else their kernels stay in VALU
+// items.
+constexpr double kToepMinShare = 0.03;
+
 rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out) {
+    rocket_status st = build_plan(k, L, true, out);
+    if (st != ROCKET_OK) return st;
+    double toep = 0.0, total = 0.0;
+    for (const ItemDesc &it : out->items) {
+        total += it.cost;
+        if (it.variant >= kToepVariant0) toep += it.cost;
+    }
+    if (toep > 0.0 && toep < kToepMinShare * total) st = build_plan(k, L, false, out);
+    return st;
+}
+
+static rocket_status build_plan(const rocket_kernels *k, int32_t L, bool allow_toeplitz, HostPlan *out) {
     try {
         HostPlan P;
         P.n_kernels = k->n_kernels;
@@ -307,6 +406,11 @@ rocket_status build_host_plan(const rocket_kernels *k, int32_t L, HostPlan *out)
             while (pos < ks.size()) {
                 const size_t rem = ks.size() - pos;
                 const int nk_valu = (valu_ok && rem <= 2) ? (int)rem : 0;
+                if (nk_valu && allow_toeplitz && toeplitz_pays(ks, pos, (size_t)nk_valu, ell, d, O, k)) {
+                    add_toeplitz_item(P, ks, pos, nk_valu, eidx, d, p, O, L, k);
+                    pos += (size_t)nk_valu;
+                    continue;
+                }
                 const int G = (C > 1 || rem <= 4 || (valu_ok && rem == 5)) ? 1 : 2;
                 const size_t take = C > 1 ? (size_t)item_sizes[next_item++]
                                           : std::min<size_t>(rem, (size_t)(4 * G));

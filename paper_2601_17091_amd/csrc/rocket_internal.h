@@ -55,7 +55,7 @@ struct alignas(16) ItemDesc {
     int32_t d;         // dilation
     int32_t p;         // padding
     int32_t O;         // number of dot products (outputs)
-    int32_t n_tiles;   // ceil(O / 64)
+    int32_t n_tiles;   // ceil(O / 64); Toeplitz items: chunks per super-tile, ceil(d / 64)
     int32_t w_off;     // first packed weight: [n_ch][G][ell][4] floats
     int32_t k_off;     // first slot entry: kernel ids and biases, [4G]
     int32_t cost;      // MFMA instructions per series (scheduling weight)
@@ -79,8 +79,21 @@ constexpr int kItemWords = (int)(sizeof(ItemDesc) / sizeof(int32_t));
 // empty, 6 + 2 * ell_index + (nk - 1); their weights keep the 4-slot packing
 // of a one-group item.
 constexpr int kNumMfmaVariants = 2 * kNumEll;
-constexpr int kNumVariants = 4 * kNumEll;
+constexpr int kNumVariants = 6 * kNumEll;
 constexpr int kValuVariant0 = kNumMfmaVariants;
+
+// Variants 12..17 are Toeplitz items: the one or two kernels left over in a
+// bucket at a large dilation d, 12 + 2 * ell_index + (nk - 1).  The 4 slots
+// of one MFMA group hold the same kernel shifted by sigma = 4 / nk taps:
+// slot s is kernel s / sigma at shift h = s % sigma, whose weight at tap m is
+// w[m - h], over ell + sigma - 1 taps; lane l of chunk c of super-tile st
+// then computes, in slot s, the output at position
+//     st * sigma * d + 64 c + l + h * d,
+// valid when 64 c + l < d (the chunks of a super-tile cover d positions per
+// shift) and the position is below O.  A super-tile covers sigma * d
+// consecutive outputs per kernel in ceil(d / 64) chunks; each chunk is one
+// tile of 64 consecutive series reads per tap, as in an MFMA item.
+constexpr int kToepVariant0 = 4 * kNumEll;
 
 // Series of at most this length can run in the series-lane layout, which
 // takes MFMA items only; VALU items are made for longer series.

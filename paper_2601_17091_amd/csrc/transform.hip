@@ -289,6 +289,19 @@ struct ClampedTiles {
     }
 };
 
+// The padded layout with each block's series offset clamped to at most L
+// (Toeplitz items' last super-tile, whose taps reach up to (sigma - 1) d past
+// the other blocks): a block that starts at or past L holds no real output
+// that reads a series value, only zero padding, so it reads the zeros at L
+// instead and every read stays inside the row's margins and the tail pad.
+struct RightClampedTiles {
+    uint32_t row;  // LDS byte address of series index 0
+    int b0;        // series index under tap 0 of lane 0
+    int d;
+    int L;
+    __device__ __forceinline__ uint32_t m0(int j) const { return row + 4u * (uint32_t)min(b0 + j * d, L); }
+};
+
 // Per-series accumulators of one work item, per lane and kernel slot: the
 // running max, the positive count (wavefront-uniform, scalar registers) and,
 // when MPV is computed, the sum of the positive values.
@@ -886,6 +899,126 @@ __device__ __forceinline__ void run_valu_items(int *next_item, int beg, int cnt_
     }
 }
 
+// ---------------------------------------------------------------------------
+// Toeplitz items: the one (NK = 1) or two (NK = 2) kernels left over in a
+// bucket at a large dilation d.  The 4 slots of one MFMA group hold the same
+// kernel at SIGMA = 4 / NK shifts: slot s is kernel s / SIGMA shifted by
+// h = s % SIGMA taps (weight w[m - h] at tap m, ELL + SIGMA - 1 taps), so the
+// MFMA chain of lane l reading series index t0 - p + m d + l at tap m
+// computes, in slot s, the output at position t0 + l + h d.  Outputs come in
+// super-tiles of SIGMA d consecutive positions per kernel: ceil(d / 64)
+// chunks at t0 = T + 64 c cover positions T .. T + d - 1 for shift 0 and the
+// same plus h d for shift h; lanes with 64 c + l >= d (the last chunk) start
+// from -inf, as lanes past O do in an MFMA item's last tile.  The last,
+// partial super-tile masks each slot on its own (positions below O) and, in
+// the padded layout, clamps its block offsets to at most L (its taps reach
+// past the row's margin; see RightClampedTiles).  One
+// MFMA chain of ELL + SIGMA - 1 taps thus yields 4 x 64 outputs, where a
+// VALU item spends ELL fp32 FMAs per 64 outputs and kernel.
+// ---------------------------------------------------------------------------
+template <int ELL, int NK, bool CLAMP, bool MPV>
+__device__ __forceinline__ void run_toep_item(const ItemDesc &it, const float *rows0, int nrows,
+                                              const FusedArgs &a, float *F0, int lane) {
+    constexpr int SIGMA = 4 / NK;
+    constexpr int TAPS = ELL + SIGMA - 1;
+    constexpr int NT = rocket::kTilesPerBlock[0];
+    float wa[1][TAPS];
+#pragma unroll
+    for (int j = 0; j < TAPS; ++j) wa[0][j] = a.wpk[it.w_off + j * 4 + (lane & 3)];
+    const int d = it.d;
+    const int nc = it.n_tiles;                // chunks per super-tile
+    const int remc = d - (nc - 1) * kTile;    // positions of a super-tile's last chunk, 1..64
+    v4f binit[1], blast[1];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        const float b = as_const(a.bias)[it.k_off + v];
+        float bv;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(bv) : "s"(b));
+        binit[0][v] = bv;
+        blast[0][v] = lane < remc ? bv : -INFINITY;
+    }
+    int kid[NK];
+#pragma unroll
+    for (int q = 0; q < NK; ++q) kid[q] = as_const(a.kid)[it.k_off + q * SIGMA];
+    const int span = SIGMA * d;
+    const int s_full = it.O / span;
+    const int rest = it.O - s_full * span;
+    const int nlast = rest > 0 ? (min(rest, d) + kTile - 1) / kTile : 0;
+    const int nfull = (nc - 1) / NT;
+    const int nv = nc - nfull * NT;
+    const McCtx mc{};
+    const int row_pitch = a.row_stride;
+    const int64_t f_stride = (int64_t)a.nf * a.K;
+    for (int r = 0; r < nrows; ++r) {
+        RowAcc<1> ra;
+        init_row<1, MPV>(ra);
+        const uint32_t row = lds_addr(rows0 + r * row_pitch);
+        for (int st = 0; st < s_full; ++st) {
+            const int T = st * span;
+            for (int blk = 0; blk < nfull; ++blk) {
+                const int b0 = T + blk * (NT * kTile) - it.p;
+                if constexpr (CLAMP)
+                    tile_block<TAPS, 1, NT, false, MPV, false>(ClampedTiles{row, b0, d, a.L}, wa, mc, binit, blast, ra);
+                else
+                    tile_block<TAPS, 1, NT, false, MPV, false>(PaddedTiles{row + 4u * (uint32_t)b0, d}, wa, mc, binit,
+                                                               blast, ra);
+            }
+            const int b0 = T + nfull * (NT * kTile) - it.p;
+            if constexpr (CLAMP)
+                TailTiles<TAPS, 1, NT, MPV, false, ClampedTiles>::run(nv, ClampedTiles{row, b0, d, a.L}, wa, mc, binit,
+                                                                      blast, ra);
+            else
+                TailTiles<TAPS, 1, NT, MPV, false, PaddedTiles>::run(nv, PaddedTiles{row + 4u * (uint32_t)b0, d}, wa,
+                                                                     mc, binit, blast, ra);
+        }
+        // the last, partial super-tile: chunk by chunk, each slot valid on
+        // the lanes whose position is in its chunk's d and below O
+        const int T = s_full * span;
+        for (int c = 0; c < nlast; ++c) {
+            v4f bm[1];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int lim = min(d - c * kTile, it.O - T - c * kTile - (v % SIGMA) * d);
+                bm[0][v] = lane < lim ? binit[0][v] : -INFINITY;
+            }
+            const int b0 = T + c * kTile - it.p;
+            if constexpr (CLAMP)
+                tile_block<TAPS, 1, 1, true, MPV, false>(ClampedTiles{row, b0, d, a.L}, wa, mc, binit, bm, ra);
+            else
+                tile_block<TAPS, 1, 1, true, MPV, false>(RightClampedTiles{row, b0, d, a.L}, wa, mc, binit, bm, ra);
+        }
+        // each kernel's features from its SIGMA slots
+#pragma unroll
+        for (int q = 0; q < NK; ++q) {
+            uint32_t cnt = 0;
+            float m = ra.mx[0][q * SIGMA], ps = MPV ? ra.ps[0][q * SIGMA] : 0.0f;
+#pragma unroll
+            for (int h = 0; h < SIGMA; ++h) cnt += ra.cnt[0][q * SIGMA + h];
+#pragma unroll
+            for (int h = 1; h < SIGMA; ++h) {
+                m = fmaxf(m, ra.mx[0][q * SIGMA + h]);
+                if (MPV) ps += ra.ps[0][q * SIGMA + h];
+            }
+            m = wave_all<OpMax>(m);
+            if (MPV) ps = wave_all<OpSum>(ps);
+            if (lane == 0 && kid[q] >= 0) write_features<MPV>(cnt, m, ps, kid[q], it.inv_O, F0 + r * f_stride);
+        }
+    }
+}
+
+template <int ELL, int NK, bool CLAMP, bool MPV>
+__device__ __forceinline__ void run_toep_items(int *next_item, int beg, int cnt_items, const float *rows0, int nrows,
+                                               const FusedArgs &a, float *F0, int lane) {
+    while (true) {
+        int idx = 0;
+        if (lane == 0) idx = atomicAdd(next_item, 1);
+        idx = __builtin_amdgcn_readfirstlane(__shfl(idx, 0, 64));
+        if (idx >= cnt_items) break;
+        const ItemDesc it = load_item(as_const(a.items) + as_const(a.order)[beg + idx]);
+        run_toep_item<ELL, NK, CLAMP, MPV>(it, rows0, nrows, a, F0, lane);
+    }
+}
+
 struct GroupWork {
     int variant;
     int beg;        // first entry of the items' order
@@ -990,6 +1123,30 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
             case 10: run_valu_items<11, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
             default: run_valu_items<11, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
         }
+    }
+}
+
+// Toeplitz items (univariate long-series plans) in a kernel of their own,
+// launched after the fused kernel over the same row groups: in the fused
+// kernel's code their extra tap counts raise the scalar-register pressure of
+// every variant's loop.
+template <int BLOCK, bool CLAMP, bool MPV>
+__global__ __launch_bounds__(BLOCK) void rocket_toeplitz_kernel(FusedArgs a) {
+    extern __shared__ __align__(16) float smem[];
+    __shared__ int next_item;
+    GroupWork w;
+    if (!stage_group<BLOCK>(a, smem, &next_item, w)) return;
+    const int lane = threadIdx.x & (rocket::kWave - 1);
+    float *F0 = a.F + w.grow * (int64_t)a.nf * a.K;
+    const float *rows0 = smem + a.halo_lo;
+    const int beg = w.beg, cnt = w.cnt_items, nr = w.nrows;
+    switch (w.variant) {
+        case 12: run_toep_items<7, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 13: run_toep_items<7, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 14: run_toep_items<9, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 15: run_toep_items<9, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 16: run_toep_items<11, 1, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        default: run_toep_items<11, 2, CLAMP, MPV>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
     }
 }
 
@@ -1589,6 +1746,23 @@ static const void *mr_fn(int sel) {
     return fns[sel];
 }
 
+// The Toeplitz kernel's instances: bit 0 the 1024-thread block, bit 1
+// clamped indices, bit 2 MPV.
+constexpr int kToepInstances = 8;
+static const void *toep_fn(int sel) {
+    static const void *const fns[kToepInstances] = {
+        (const void *)rocket_toeplitz_kernel<kBlock, false, false>,
+        (const void *)rocket_toeplitz_kernel<kBigBlock, false, false>,
+        (const void *)rocket_toeplitz_kernel<kBlock, true, false>,
+        (const void *)rocket_toeplitz_kernel<kBigBlock, true, false>,
+        (const void *)rocket_toeplitz_kernel<kBlock, false, true>,
+        (const void *)rocket_toeplitz_kernel<kBigBlock, false, true>,
+        (const void *)rocket_toeplitz_kernel<kBlock, true, true>,
+        (const void *)rocket_toeplitz_kernel<kBigBlock, true, true>,
+    };
+    return fns[sel];
+}
+
 static const void *series_fn(bool mpv) {
     return mpv ? (const void *)rocket_series_kernel<true> : (const void *)rocket_series_kernel<false>;
 }
@@ -1708,17 +1882,19 @@ static bool choose_layout(rocket_plan *p, bool clamped, const hipDeviceProp_t &p
 // launches with.
 constexpr int kMaxDevices = 64;
 static std::mutex g_lds_attr_mu;
-static int g_lds_attr[kMaxDevices][kFusedInstances + kMrInstances];
+static int g_lds_attr[kMaxDevices][kFusedInstances + kMrInstances + kToepInstances];
 
 static hipError_t allow_lds(int device, int64_t lds) {
     if (lds <= 64 * 1024) return hipSuccess;
     if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
     std::lock_guard<std::mutex> lock(g_lds_attr_mu);
     hipError_t e = hipSuccess;
-    for (int sel = 0; sel < kFusedInstances + kMrInstances && e == hipSuccess; ++sel) {
+    for (int sel = 0; sel < kFusedInstances + kMrInstances + kToepInstances && e == hipSuccess; ++sel) {
         int &granted = g_lds_attr[device][sel];
         if (granted >= lds) continue;
-        const void *fn = sel < kFusedInstances ? fused_fn(sel) : mr_fn(sel - kFusedInstances);
+        const void *fn = sel < kFusedInstances ? fused_fn(sel)
+                         : sel < kFusedInstances + kMrInstances ? mr_fn(sel - kFusedInstances)
+                                                                 : toep_fn(sel - kFusedInstances - kMrInstances);
         e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e == hipSuccess) granted = (int)lds;
     }
@@ -1977,23 +2153,46 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
                  : 0;
     a.S = S;
     a.s_rows = s_rows;
-    const int64_t max_rows =
-        ((int64_t)INT_MAX / (nsplit * std::max(a.n_variants, 1)) / kXcds - 1) * kXcds * R;
-    for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
-        a.row0 = r0;
-        a.n_rows = std::min<int64_t>(max_rows, n - r0);
-        const int64_t groups_now = (a.n_rows + R - 1) / R;
-        a.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
-        const unsigned nb = (unsigned)(kXcds * a.groups_per_xcd * nsplit * a.n_variants);
-        const size_t lds = (size_t)(series ? p->series_lds : p->lds_bytes);
-        const bool big = big_group;
-        const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
-        const void *fn = series ? series_fn(p->mpv) : (p->minirocket ? mr_fn(sel & 3) : fused_fn(sel));
-        void *args[] = {&a};
-        if (hipLaunchKernel(fn, dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) !=
-            hipSuccess)
-            return ROCKET_ERR_HIP;
-        if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+    const size_t lds = (size_t)(series ? p->series_lds : p->lds_bytes);
+    const bool big = big_group;
+    const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
+    // ROCKET plans: the Toeplitz items' variants go to a kernel of their
+    // own, launched after the fused kernel's
+    FusedArgs parts[2] = {a, a};
+    const void *fns[2] = {nullptr, nullptr};
+    int nparts = 0;
+    if (series || p->minirocket) {
+        fns[nparts++] = series ? series_fn(p->mpv) : mr_fn(sel & 3);
+    } else {
+        parts[0].n_variants = parts[1].n_variants = 0;
+        for (int i = 0; i < a.n_variants; ++i) {
+            FusedArgs &q = parts[a.variants[i] >= rocket::kToepVariant0 ? 1 : 0];
+            q.variants[q.n_variants++] = a.variants[i];
+        }
+        if (parts[0].n_variants > 0) {
+            parts[nparts] = parts[0];
+            fns[nparts++] = fused_fn(sel);
+        }
+        if (parts[1].n_variants > 0) {
+            parts[nparts] = parts[1];
+            fns[nparts++] = toep_fn(sel & 7);
+        }
+    }
+    for (int part = 0; part < nparts; ++part) {
+        FusedArgs &q = parts[part];
+        const int64_t max_rows =
+            ((int64_t)INT_MAX / (nsplit * std::max(q.n_variants, 1)) / kXcds - 1) * kXcds * R;
+        for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
+            q.row0 = r0;
+            q.n_rows = std::min<int64_t>(max_rows, n - r0);
+            const int64_t groups_now = (q.n_rows + R - 1) / R;
+            q.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
+            const unsigned nb = (unsigned)(kXcds * q.groups_per_xcd * nsplit * q.n_variants);
+            void *args[] = {&q};
+            if (hipLaunchKernel(fns[part], dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) != hipSuccess)
+                return ROCKET_ERR_HIP;
+            if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+        }
     }
     return ROCKET_OK;
 }

@@ -244,3 +244,37 @@ def test_valu_items(torch_gpu, rk, oracle, mode, mpv):
     torch_gpu.cuda.synchronize()
     ref = oracle.transform(X, ks)
     (assert_mpv_parity if mpv else assert_parity)(F.cpu().numpy(), ref, "valu items")
+
+
+@pytest.mark.parametrize("mode", ["fused", "clamped"])
+@pytest.mark.parametrize("mpv", [False, True])
+def test_toeplitz_items(torch_gpu, rk, oracle, mode, mpv):
+    """The one or two kernels left over in a bucket at a large dilation run
+    as Toeplitz items (one MFMA group holding the kernel at 4 or 2 tap
+    shifts): single and paired kernels at dilations around multiples of 64,
+    padded and not, beside MFMA and VALU items, against the oracle."""
+    from _util import assert_mpv_parity
+    rng = np.random.default_rng(41)
+    L = 1300
+    lengths, dil, pad, bias, weights = [], [], [], [], []
+    for ln in (7, 9, 11):
+        for d in (20, 60, 64, 65, 100, 127, 128, 129):
+            if (ln - 1) * d >= L:
+                continue
+            for padded in (0, 1):
+                for _ in range(1 + (d % 2) + 8 * (d == 20)):
+                    lengths.append(ln)
+                    dil.append(d)
+                    pad.append((ln - 1) * d // 2 if padded else 0)
+                    bias.append(float(rng.uniform(-1, 1)))
+                    weights.append(rng.standard_normal(ln))
+    ks = kernel_set(lengths, dil, pad, bias, weights)
+    v = rk.plan_tables(ks, L)["items"][:, 0]
+    assert ((v >= 12) & (v % 2 == 0)).any() and ((v >= 12) & (v % 2 == 1)).any() and (v < 12).any()
+    X = np.cumsum(rng.standard_normal((5, L)), axis=1).astype(np.float32)
+    _log("Toeplitz items mode=%s mpv=%s, %d kernels" % (mode, mpv, len(lengths)))
+    Xd = torch_gpu.from_numpy(X).cuda()
+    plan = rk.Plan(ks, L, clamped=mode == "clamped", mpv=mpv)
+    F = plan.transform(Xd)
+    torch_gpu.cuda.synchronize()
+    (assert_mpv_parity if mpv else assert_parity)(F.cpu().numpy(), oracle.transform(X, ks), "toeplitz")

@@ -26,7 +26,8 @@ ELLS = (7, 9, 11)
 TILE = 64
 TILES_PER_BLOCK = {1: 8, 2: 4}
 CLAMP_MARGIN = 512
-N_VARIANTS = 12      # 0..5 MFMA items, 6..11 VALU items
+N_VARIANTS = 18      # 0..5 MFMA items, 6..11 VALU items, 12..17 Toeplitz items
+TOEP0 = 12
 SERIES_MAX_L = 128   # VALU items only for longer series
 
 
@@ -70,6 +71,95 @@ def tile_reads(f, ell, L, clamped):
     return off[:, None, :] + (u * TILE)[:, None, None] + np.arange(TILE)[None, :, None]
 
 
+def walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows, clamped, cover, F):
+    """A Toeplitz item (one or two leftover kernels at dilation d): slot s is
+    kernel s // sigma shifted by h = s % sigma taps over ell + sigma - 1 taps;
+    super-tiles of sigma*d outputs per kernel in ceil(d/64) chunks, run in
+    blocks of 8 chunks (the last super-tile, if partial, one chunk at a
+    time); lane l of the chunk at t0 reads t0 - p + m*d + l at tap m and, in
+    slot s, computes the output at t0 + l + h*d, valid when it lies in the
+    chunk's first d positions per shift and below O."""
+    v = f["variant"] - TOEP0
+    ell, nk = ELLS[v // 2], v % 2 + 1
+    sigma = 4 // nk
+    taps = ell + sigma - 1
+    d, p, O = f["d"], f["p"], f["O"]
+    nc = -(-d // TILE)
+    assert f["n_tiles"] == nc and L > SERIES_MAX_L and f["n_ch"] == 1
+    kid = tables["slot_kernel"][f["k_off"]:f["k_off"] + 4]
+    bias = tables["slot_bias"][f["k_off"]:f["k_off"] + 4]
+    W = tables["wpk"][f["w_off"]:f["w_off"] + taps * 4].reshape(taps, 4)
+    kern = []
+    for q in range(nk):
+        k = int(kid[q * sigma])
+        assert k >= 0 and np.all(kid[q * sigma + 1:(q + 1) * sigma] < 0)
+        assert int(kernels["length"][k]) == ell and int(kernels["dilation"][k]) == d
+        assert int(kernels["padding"][k]) == p
+        assert L + 2 * p - (ell - 1) * d == O
+        for h in range(sigma):
+            s_ = q * sigma + h
+            col = np.zeros(taps, np.float32)
+            col[h:h + ell] = kernels["weights"][k][:ell]
+            assert np.array_equal(W[:, s_], col) and bias[s_] == np.float32(kernels["bias"][k])
+        kern.append(k)
+    span = sigma * d
+    s_full = O // span
+    rest = O - s_full * span
+    nlast = -(-min(rest, d) // TILE) if rest > 0 else 0
+    assert f["cost"] == (s_full * nc + nlast) * taps
+    # chunks as (t0, block offset of tap 0, tile within block, last super-tile)
+    chunks = []
+    for st in range(s_full):
+        for c in range(nc):
+            chunks.append((st * span + c * TILE, st * span + (c // 8) * 8 * TILE, c % 8, False))
+    for c in range(nlast):
+        t0 = s_full * span + c * TILE
+        chunks.append((t0, t0, 0, True))
+    t0 = np.array([c_[0] for c_ in chunks])
+    boff = np.array([c_[1] for c_ in chunks])
+    u = np.array([c_[2] for c_ in chunks])
+    last = np.array([c_[3] for c_ in chunks])
+    lane = np.arange(TILE)
+    off = boff[:, None] - p + np.arange(taps)[None, :] * d          # [chunk, tap]
+    if clamped:
+        off = np.clip(off, -CLAMP_MARGIN, L)
+    else:
+        # the last super-tile's block offsets are clamped to at most L
+        off = np.where(last[:, None], np.minimum(off, L), off)
+    idx = off[:, None, :] + (u * TILE)[:, None, None] + lane[None, :, None]   # [chunk, lane, tap]
+    assert (halo_lo + idx).min() >= 0 and (halo_lo + idx).max() < stride + pad, (d, p, O)
+    for q, k in enumerate(kern):
+        cov = np.zeros(O, np.int64)
+        vals = []
+        for h in range(sigma):
+            s_ = q * sigma + h
+            pos = t0[:, None] + lane[None, :] + h * d                 # [chunk, lane]
+            within = ((t0 - (t0 // span) * span)[:, None] + lane[None, :]) < d
+            real = within & (pos < O)
+            np.add.at(cov, pos[real], 1)
+            # taps with a weight for this slot read the zero-padded series at the true index
+            ri = idx[real][:, h:h + ell]
+            ti = pos[real][:, None] - p + np.arange(ell)[None, :] * d
+            inside = (ti >= 0) & (ti < L)
+            assert np.array_equal(ri[inside], ti[inside])
+            assert np.all((ri[~inside] < 0) | (ri[~inside] >= L))
+            assert (halo_lo + ri).max() < stride
+            vals.append((s_, real, pos))
+        cover[k] = cov
+        if rows is not None:
+            n = rows.shape[0]
+            ys, ms = [], []
+            for s_, real, pos in vals:
+                acc = np.full((n, int(real.sum())), bias[s_], np.float32)
+                xr = rows[:, 0][:, halo_lo + idx[real]]                  # [n, output, tap]
+                for m in range(taps):
+                    acc = (acc + xr[..., m] * W[m, s_]).astype(np.float32)
+                ys.append(acc)
+            y = np.concatenate(ys, axis=1)
+            F[:, 2 * k] = (y > 0).sum(axis=1) / O
+            F[:, 2 * k + 1] = y.max(axis=1)
+
+
 def walk(tables, kernels, L, X=None, clamped=False):
     """Replay the fused kernel's schedule; returns per-kernel coverage and,
     if X is given, fp32 features [n, 2K]."""
@@ -90,6 +180,10 @@ def walk(tables, kernels, L, X=None, clamped=False):
         rows[:, :, halo_lo:halo_lo + L] = Xc
     for row in tables["items"]:
         f = item_fields(row)
+        if f["variant"] >= TOEP0:
+            walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows if X is not None else None, clamped,
+                          cover, F)
+            continue
         d, p, O = f["d"], f["p"], f["O"]
         ell, G, nk = variant_info(f["variant"])
         nslot = 4 * G
@@ -233,7 +327,8 @@ def test_hand_built_lengths_and_extremes(oracle):
 def test_item_cost_and_groups():
     ks = rk.generate_kernels(203, 10000, 1000)
     t = rk.plan_tables(ks, 1000)
-    items = t["items"]
+    toep = t["items"][:, 0] >= TOEP0       # Toeplitz items: checked by walk_toeplitz
+    items = t["items"][~toep]
     info = np.array([variant_info(int(v)) for v in items[:, 0]])
     ell, G, nk = info[:, 0], info[:, 1], info[:, 2]
     O, n_tiles = items[:, 3], items[:, 4]
@@ -242,12 +337,14 @@ def test_item_cost_and_groups():
     np.testing.assert_array_equal(items[mf, 7], (n_tiles * ell * G * items[:, 8])[mf])
     np.testing.assert_array_equal(items[~mf, 7], ((n_tiles * ell * nk + 1) // 2)[~mf])
     # a bucket is split into groups of 8 with at most one smaller group,
-    # whose one or two last kernels run as a VALU item
+    # whose one or two last kernels run as a VALU or a Toeplitz item
     assert (G[mf] == 2).sum() > (G[mf] == 1).sum() and (~mf).sum() > 0
-    # FMA work issued (an MFMA: 4 slots x 64 lanes; a VALU FMA: 64 lanes)
-    # stays within 12% of the nominal taps x outputs
+    # FMA work issued (an MFMA: 4 slots x 64 lanes; a VALU FMA: 64 lanes;
+    # a Toeplitz item's cost counts its MFMAs) stays within 12% of the
+    # nominal taps x outputs
     nominal = (ks["length"] * (1000 + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
-    issued = (n_tiles * ell * G * 256)[mf].sum() + (n_tiles * ell * nk * 64)[~mf].sum()
+    issued = ((n_tiles * ell * G * 256)[mf].sum() + (n_tiles * ell * nk * 64)[~mf].sum()
+              + (t["items"][toep, 7] * 256).sum())
     assert issued < 1.12 * nominal
 
 
@@ -362,3 +459,43 @@ def test_multichannel_issued_work():
     valid = (ks["channel_count"].astype(np.int64) * ks["length"] *
              (w.L + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
     assert items[:, 7].sum() * 256 < 1.5 * valid
+
+
+@pytest.mark.parametrize("seed,K,L", [(15, 300, 3000), (16, 400, 1500)])
+def test_toeplitz_items_walk_matches_oracle(oracle, seed, K, L):
+    """Long series: the one or two kernels left over in a bucket at a large
+    dilation become Toeplitz items (one MFMA group, the kernel at 4 or 2 tap
+    shifts); their walk covers every output once and lands in the oracle's
+    certified bounds."""
+    ks = rk.generate_kernels(seed, K, L)
+    t = rk.plan_tables(ks, L)
+    v = t["items"][:, 0]
+    assert ((v >= 12) & (v % 2 == 0)).any() and ((v >= 12) & (v % 2 == 1)).any()
+    X = np.random.default_rng(seed).standard_normal((3, L)).cumsum(axis=1).astype(np.float32)
+    check_tables(ks, L, X, oracle)
+
+
+def test_toeplitz_hand_built_dilations(oracle):
+    """Singles and pairs at dilations around multiples of 64 (chunks filled
+    exactly, or with 1 or 63 positions in the last chunk), padded and not,
+    with O just above and below multiples of the super-tile span."""
+    rng = np.random.default_rng(17)
+    L = 1300
+    lengths, dil, pad, bias, weights = [], [], [], [], []
+    for ln in (7, 9, 11):
+        for d in (60, 64, 65, 100, 127, 128, 129):
+            if (ln - 1) * d >= L:
+                continue
+            for padded in (0, 1):
+                for _ in range(1 + (d % 2)):          # singles and pairs
+                    lengths.append(ln)
+                    dil.append(d)
+                    pad.append((ln - 1) * d // 2 if padded else 0)
+                    bias.append(float(rng.uniform(-1, 1)))
+                    weights.append(rng.standard_normal(ln))
+    ks = kernel_set(lengths, dil, pad, bias, weights)
+    t = rk.plan_tables(ks, L)
+    v = t["items"][:, 0]
+    assert ((v >= 12) & (v % 2 == 0)).sum() >= 2 and ((v >= 12) & (v % 2 == 1)).sum() >= 2
+    X = rng.standard_normal((4, L)).astype(np.float32)
+    check_tables(ks, L, X, oracle)
