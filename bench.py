@@ -71,7 +71,7 @@ class ClockSampler:
             try:
                 v = self._read()
                 if v is not None:
-                    self.samples.append(v)
+                    self.samples.append((time.perf_counter(), v))
             except Exception as e:
                 self.error = "%s: %s" % (type(e).__name__, e)
                 return
@@ -84,7 +84,10 @@ class ClockSampler:
             self._thread.start()
         return self
 
-    def stop(self):
+    def stop(self, t_end=None, min_samples=5):
+        """Samples taken after t_end (a perf_counter time: when the device went
+        idle) are dropped; with fewer than min_samples left the timed region
+        was too short to say what the clock was, and mhz is None."""
         if self._thread is not None:
             self._stop.set()
             self._thread.join()
@@ -93,9 +96,14 @@ class ClockSampler:
                 self._smi.amdsmi_shut_down()
             except Exception:
                 pass
-        if not self.samples:
+        if self._handle is None:
             return {"mhz": None, "source": "amdsmi (unavailable: %s)" % self.error}
-        a = np.array(self.samples)
+        vals = [v for t, v in self.samples if t_end is None or t <= t_end]
+        if len(vals) < min_samples:
+            return {"mhz": None, "samples": len(vals),
+                    "source": "amdsmi GFX clock: timed region too short for %d samples at %d ms"
+                              % (min_samples, int(self.interval_s * 1e3))}
+        a = np.array(vals)
         return {"mhz": float(np.median(a)), "min": float(a.min()), "max": float(a.max()),
                 "samples": int(a.size), "source": "amdsmi GFX clock, sampled every %d ms during the timed passes"
                                                   % int(self.interval_s * 1e3)}
@@ -106,14 +114,16 @@ def timed_passes(torch, stream, one_pass, steps):
     consecutive passes (all on the launch stream), synchronised before and
     after.  Returns (total ms, per-pass ms list, clock record)."""
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    clock = ClockSampler().start()
+    clock = ClockSampler()
     torch.cuda.synchronize()
     evs[0].record(stream)
     for i in range(steps):
         one_pass()
         evs[i + 1].record(stream)
+        if i == 0:
+            clock.start()  # the device is busy from here on
     torch.cuda.synchronize()
-    clk = clock.stop()
+    clk = clock.stop(t_end=time.perf_counter())
     per = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
     return evs[0].elapsed_time(evs[-1]), per, clk
 

@@ -2116,10 +2116,21 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     n_present = std::max<int64_t>(n_present, 1);
     const int64_t per_variant = (int64_t)p->host.items.size() / n_present;
     const int64_t few_groups = 2 * (int64_t)std::max(p->n_cu, 1);
-    while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target &&
-           (per_variant / rocket::kSplitCounts[li + 1] >= min_items ||
-            groups * n_present * rocket::kSplitCounts[li] < few_groups))
-        ++li;
+    if (series) {
+        // a series-lane chunk's workgroups are few and short: split them only
+        // as far as about 4 workgroups per CU, so that the whole grid is
+        // resident at once and no partial second round of workgroups trails
+        // each chunk
+        while (li + 1 < rocket::kNumSplitLayouts &&
+               groups * rocket::kSplitCounts[li + 1] <= 4 * (int64_t)std::max(p->n_cu, 1) &&
+               per_variant / rocket::kSplitCounts[li + 1] >= min_items)
+            ++li;
+    } else {
+        while (li + 1 < rocket::kNumSplitLayouts && groups * rocket::kSplitCounts[li] < target &&
+               (per_variant / rocket::kSplitCounts[li + 1] >= min_items ||
+                groups * n_present * rocket::kSplitCounts[li] < few_groups))
+            ++li;
+    }
     const int nsplit = rocket::kSplitCounts[li];
     FusedArgs a;
     a.X = X;
