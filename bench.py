@@ -277,7 +277,11 @@ def main():
     mfma_fma_per_pass = 256.0 * info["mfma_per_row"] * w.n
     pairs_per_s = w.n * w.n_kernels / (ms_per_step * 1e-3)
     digest = source_digest()
-    traffic = None if (args.direct or args.mpv) else traffic_from_profile(w.name, digest)
+    # the layout the timed calls ran: series-lane for short univariate series
+    # in calls of at least 4,096 series (then a permutation kernel writes F)
+    series_path = bool(info.get("series_lane")) and batch >= 4096
+    traffic = None if (args.direct or args.mpv) else traffic_from_profile(
+        w.name, digest, "rocket_series_kernel" if series_path else "rocket_fused_kernel")
 
     # parity of sampled rows and the CPU baseline on the same rows
     cpu = None
@@ -334,12 +338,11 @@ def main():
             parity["mpv_max_excess_over_rule"] = float(max(0.0, excess[same].max()))
         log("parity %s" % parity)
 
-    # the layout the timed calls ran: series-lane for short univariate series
-    # in calls of at least 4,096 series (then a permutation kernel writes F)
-    series_path = bool(info.get("series_lane")) and batch >= 4096
     path = "direct" if info["direct"] else ("series-lane-mfma" if series_path else "fused-mfma")
     kernel_name = ("rocket_direct_kernel" if info["direct"] else
-                   ("rocket_series_kernel + rocket_slot_permute_kernel" if series_path else "rocket_fused_kernel"))
+                   ("rocket_series_kernel + rocket_slot_permute_kernel" if series_path else
+                    ("rocket_fused_kernel + rocket_toeplitz_kernel" if info.get("toeplitz_items") else
+                     "rocket_fused_kernel")))
     out = {
         "metric": "series*kernels/s (ROCKET transform, fp32, 1 MI355X)",
         "value": pairs_per_s,

@@ -314,6 +314,10 @@ rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, i
  *                in VALU items: the one or two kernels left over in a bucket
  *                of a univariate plan for series longer than 128 samples,
  *                run without MFMA
+ *   toeplitz_items  work items of the shifted-kernel (Toeplitz) form: the
+ *                one or two kernels left over in a bucket at a large
+ *                dilation, run in a second kernel launch of each call
+ *                (0: one launch per call)
  */
 typedef struct {
     int64_t n_items;
@@ -328,6 +332,7 @@ typedef struct {
     int32_t minirocket;
     int32_t series_lane;
     int64_t valu_fma_per_row;
+    int64_t toeplitz_items;
 } rocket_plan_facts;
 
 /* Fill *out with the plan's facts.  Errors: ROCKET_ERR_INVALID_ARG if p or
@@ -352,7 +357,12 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                7/9/11 taps, G kernel groups of 4 slots (MFMA items), or
  *                6 + 2 * ell_index + (nk - 1) for VALU items of nk = 1 or 2
  *                kernels in slots 0..nk-1 (G = 1 packing; univariate plans
- *                for series longer than 128 samples);
+ *                for series longer than 128 samples), or
+ *                12 + 2 * ell_index + (nk - 1) for Toeplitz items: nk = 1 or
+ *                2 leftover kernels at a large dilation d, slot s holding
+ *                kernel s / sigma (sigma = 4 / nk) shifted by s % sigma taps
+ *                over ell + sigma - 1 taps, tiles = ceil(d / 64) chunks per
+ *                super-tile of sigma * d outputs;
  *                the O outputs are computed in tiles = ceil(O / 64) tiles
  *                of 64 consecutive positions (lane l of tile k computes
  *                output 64k + l; lanes past O compute nothing that counts);
@@ -364,7 +374,7 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                split_counts[n_layouts]: the items of variant v in split s
  *                of layout i (ns = split_counts[i] splits) are
  *                order[split_begin[layout_off[i] + v*ns + s] ..
- *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..11
+ *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..17
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
  *                of the padded layout (every tap of every real output lands
  *                inside the row)

@@ -2067,6 +2067,11 @@ extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_fact
     out->series_lane = p->series ? 1 : 0;
     out->valu_fma_per_row = p->host.valu_fma_per_row;
     out->rows_per_block = p->direct ? 0 : (p->series ? kSeriesLanes : p->rows_per_block);
+    int64_t toep = 0;
+    if (!p->minirocket)
+        for (const rocket::ItemDesc &it : p->host.items)
+            if (it.variant >= rocket::kToepVariant0) ++toep;
+    out->toeplitz_items = toep;
     return ROCKET_OK;
 }
 

@@ -81,7 +81,7 @@ class CPlanFacts(ctypes.Structure):
         ("direct", ctypes.c_int32), ("clamped", ctypes.c_int32),
         ("features_per_kernel", ctypes.c_int32), ("rows_per_block", ctypes.c_int32),
         ("n_features", ctypes.c_int64), ("minirocket", ctypes.c_int32), ("series_lane", ctypes.c_int32),
-        ("valu_fma_per_row", ctypes.c_int64),
+        ("valu_fma_per_row", ctypes.c_int64), ("toeplitz_items", ctypes.c_int64),
     ]
 
 
@@ -349,7 +349,8 @@ class Plan:
                     lds_bytes=f.lds_bytes, direct=bool(f.direct), clamped=bool(f.clamped),
                     features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block,
                     n_features=f.n_features, minirocket=bool(f.minirocket),
-                    series_lane=bool(f.series_lane), valu_fma_per_row=f.valu_fma_per_row)
+                    series_lane=bool(f.series_lane), valu_fma_per_row=f.valu_fma_per_row,
+                    toeplitz_items=f.toeplitz_items)
 
     @property
     def n_features(self) -> int:

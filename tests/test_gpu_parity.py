@@ -275,6 +275,7 @@ def test_toeplitz_items(torch_gpu, rk, oracle, mode, mpv):
     _log("Toeplitz items mode=%s mpv=%s, %d kernels" % (mode, mpv, len(lengths)))
     Xd = torch_gpu.from_numpy(X).cuda()
     plan = rk.Plan(ks, L, clamped=mode == "clamped", mpv=mpv)
+    assert plan.info()["toeplitz_items"] == int((v >= 12).sum())
     F = plan.transform(Xd)
     torch_gpu.cuda.synchronize()
     (assert_mpv_parity if mpv else assert_parity)(F.cpu().numpy(), oracle.transform(X, ks), "toeplitz")
