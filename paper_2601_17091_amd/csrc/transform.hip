@@ -202,6 +202,68 @@ __device__ __forceinline__ void lds_tiles_rest<8>(float (&xv)[8]) {
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]), "+v"(xv[5]), "+v"(xv[6]), "+v"(xv[7]) : : "memory");
 }
 
+// NC tiles (256 bytes apart) at each of P bases sb bytes apart, the first at
+// m: P runs of reads under one M0 each, M0 advanced by sb between runs (one
+// wait state after every M0 write).  Tiles are numbered base-major.  As for
+// lds_tiles, at most NC * P - 4 reads are left in flight on return when
+// NC * P > 4 (lds_tiles_rest then waits for the rest).
+template <int NC, int P>
+__device__ __forceinline__ void lds_multi(uint32_t m, uint32_t sb, float (&xv)[NC * P]);
+template <>
+__device__ __forceinline__ void lds_multi<1, 4>(uint32_t m, uint32_t sb, float (&xv)[4]) {
+    asm volatile(
+        "s_mov_b32 m0, %4\n\ts_nop 0\n\tds_read_addtid_b32 %0\n\t"
+        "s_add_u32 m0, m0, %5\n\ts_nop 0\n\tds_read_addtid_b32 %1\n\t"
+        "s_add_u32 m0, m0, %5\n\ts_nop 0\n\tds_read_addtid_b32 %2\n\t"
+        "s_add_u32 m0, m0, %5\n\ts_nop 0\n\tds_read_addtid_b32 %3\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3])
+        : "s"(m), "s"(sb)
+        : "memory", "scc");
+}
+template <>
+__device__ __forceinline__ void lds_multi<2, 4>(uint32_t m, uint32_t sb, float (&xv)[8]) {
+    asm volatile(
+        "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "s_add_u32 m0, m0, %9\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %2\n\tds_read_addtid_b32 %3 offset:256\n\t"
+        "s_add_u32 m0, m0, %9\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %4\n\tds_read_addtid_b32 %5 offset:256\n\t"
+        "s_add_u32 m0, m0, %9\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %6\n\tds_read_addtid_b32 %7 offset:256\n\t"
+        "s_waitcnt lgkmcnt(4)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5]), "=&v"(xv[6]), "=&v"(xv[7])
+        : "s"(m), "s"(sb)
+        : "memory", "scc");
+}
+template <>
+__device__ __forceinline__ void lds_multi<3, 2>(uint32_t m, uint32_t sb, float (&xv)[6]) {
+    asm volatile(
+        "s_mov_b32 m0, %6\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\tds_read_addtid_b32 %2 offset:512\n\t"
+        "s_add_u32 m0, m0, %7\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %3\n\tds_read_addtid_b32 %4 offset:256\n\tds_read_addtid_b32 %5 offset:512\n\t"
+        "s_waitcnt lgkmcnt(2)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5])
+        : "s"(m), "s"(sb)
+        : "memory", "scc");
+}
+template <>
+__device__ __forceinline__ void lds_multi<4, 2>(uint32_t m, uint32_t sb, float (&xv)[8]) {
+    asm volatile(
+        "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\tds_read_addtid_b32 %3 offset:768\n\t"
+        "s_add_u32 m0, m0, %9\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %4\n\tds_read_addtid_b32 %5 offset:256\n\t"
+        "ds_read_addtid_b32 %6 offset:512\n\tds_read_addtid_b32 %7 offset:768\n\t"
+        "s_waitcnt lgkmcnt(4)"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3]), "=&v"(xv[4]), "=&v"(xv[5]), "=&v"(xv[6]), "=&v"(xv[7])
+        : "s"(m), "s"(sb)
+        : "memory", "scc");
+}
+
 namespace {
 
 constexpr int kBlock = 256;       // 4 wavefronts per workgroup
@@ -302,6 +364,41 @@ struct RightClampedTiles {
     __device__ __forceinline__ uint32_t m0(int j) const { return row + 4u * (uint32_t)min(b0 + j * d, L); }
 };
 
+// The padded layout for P runs of NC tiles each, run k sb bytes after run 0
+// (P super-tiles of a Toeplitz item whose super-tiles hold NC chunks): tile
+// u is chunk u % NC of run u / NC.
+template <int NC, int P>
+struct MultiTiles {
+    uint32_t base;  // LDS byte address of lane 0's value under tap 0, run 0
+    int d;
+    uint32_t sb;    // bytes from one run to the next
+    __device__ __forceinline__ uint32_t m0(int j) const { return base + 4u * (uint32_t)(j * d); }
+};
+
+// How the tiles of one block group: 0 for one run (the block's last tile is
+// the row's or super-tile's last), NC for MultiTiles (every run's last
+// tile is its super-tile's last chunk).
+template <typename Src>
+struct TileRuns {
+    static constexpr int nc = 0;
+};
+template <int NC, int P>
+struct TileRuns<MultiTiles<NC, P>> {
+    static constexpr int nc = NC;
+};
+__device__ constexpr bool run_last(int u, int nt, int nc) { return nc ? (u % nc == nc - 1) : (u == nt - 1); }
+
+// The series values of a block's tiles under tap j.
+template <int NT, typename Src>
+__device__ __forceinline__ void read_tiles(const Src &src, int j, float (&xv)[NT]) {
+    lds_tiles<NT>(src.m0(j), xv);
+}
+template <int NT, int NC, int P>
+__device__ __forceinline__ void read_tiles(const MultiTiles<NC, P> &src, int j, float (&xv)[NT]) {
+    static_assert(NT == NC * P, "one block reads all of its runs");
+    lds_multi<NC, P>(src.m0(j), src.sb, xv);
+}
+
 // Per-series accumulators of one work item, per lane and kernel slot: the
 // running max, the positive count (wavefront-uniform, scalar registers) and,
 // when MPV is computed, the sum of the positive values.
@@ -346,7 +443,7 @@ __device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][E
 #pragma unroll
     for (int j = 0; j < ELL; ++j) {
         float xv[NT];
-        lds_tiles<NT>(src.m0(j), xv);
+        read_tiles<NT>(src, j, xv);
         constexpr int NA = NT > 4 ? 4 : NT;  // tiles ready after lds_tiles
 #pragma unroll
         for (int u = 0; u < NT; ++u) {
@@ -358,8 +455,9 @@ __device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][E
             }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                const v4f c = (FIRST && j == 0) ? ((LAST && u == NT - 1) ? blast[g] : binit[g])
-                                                : acc[u][g];
+                const v4f c = (FIRST && j == 0)
+                                  ? ((LAST && run_last(u, NT, TileRuns<Src>::nc)) ? blast[g] : binit[g])
+                                  : acc[u][g];
                 acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xv[u], c, 0, 0, 0);
             }
         }
@@ -454,20 +552,21 @@ __device__ __forceinline__ void tile_block(const Src &src, const float (&wa)[G][
 }
 
 // The last block of a row: its tile count nv (1..N) selects a code copy.
-template <int ELL, int G, int N, bool MPV, bool MC, typename Src>
+// (LASTB false: a block of nv tiles whose last tile is not the row's last.)
+template <int ELL, int G, int N, bool MPV, bool MC, typename Src, bool LASTB = true>
 struct TailTiles {
     __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
                                                const McCtx &mc, const v4f (&binit)[G],
                                                const v4f (&blast)[G], RowAcc<G> &ra) {
         if (nv == N)
-            tile_block<ELL, G, N, true, MPV, MC>(src, wa, mc, binit, blast, ra);
+            tile_block<ELL, G, N, LASTB, MPV, MC>(src, wa, mc, binit, blast, ra);
         else
-            TailTiles<ELL, G, N - 1, MPV, MC, Src>::run(nv, src, wa, mc, binit, blast, ra);
+            TailTiles<ELL, G, N - 1, MPV, MC, Src, LASTB>::run(nv, src, wa, mc, binit, blast, ra);
     }
 };
 
-template <int ELL, int G, bool MPV, bool MC, typename Src>
-struct TailTiles<ELL, G, 0, MPV, MC, Src> {
+template <int ELL, int G, bool MPV, bool MC, typename Src, bool LASTB>
+struct TailTiles<ELL, G, 0, MPV, MC, Src, LASTB> {
     __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL],
                                                const McCtx &, const v4f (&)[G], const v4f (&)[G],
                                                RowAcc<G> &) {}
@@ -916,6 +1015,25 @@ __device__ __forceinline__ void run_valu_items(int *next_item, int beg, int cnt_
 // MFMA chain of ELL + SIGMA - 1 taps thus yields 4 x 64 outputs, where a
 // VALU item spends ELL fp32 FMAs per 64 outputs and kernel.
 // ---------------------------------------------------------------------------
+// Whole super-tiles of NC chunks, P per block (padded rows): the block's
+// tiles are the NC chunks of each of P consecutive super-tiles, each
+// super-tile's last chunk starting from blast.  Returns the super-tiles
+// done, a multiple of P; the caller runs the rest one per block.
+template <int TAPS, int NC, int P, bool MPV>
+__device__ __forceinline__ int toep_runs(uint32_t row, int p, int d, int span, int s_full,
+                                         const float (&wa)[1][TAPS], const v4f (&binit)[1],
+                                         const v4f (&blast)[1], RowAcc<1> &ra) {
+    const McCtx mc{};
+    const int groups = s_full / P;
+    const uint32_t sb = 4u * (uint32_t)span;
+    for (int gi = 0; gi < groups; ++gi) {
+        const int b0 = gi * P * span - p;
+        tile_block<TAPS, 1, NC * P, true, MPV, false>(MultiTiles<NC, P>{row + 4u * (uint32_t)b0, d, sb}, wa, mc,
+                                                       binit, blast, ra);
+    }
+    return groups * P;
+}
+
 template <int ELL, int NK, bool CLAMP, bool MPV>
 __device__ __forceinline__ void run_toep_item(const ItemDesc &it, const float *rows0, int nrows,
                                               const FusedArgs &a, float *F0, int lane) {
@@ -944,8 +1062,8 @@ __device__ __forceinline__ void run_toep_item(const ItemDesc &it, const float *r
     const int s_full = it.O / span;
     const int rest = it.O - s_full * span;
     const int nlast = rest > 0 ? (min(rest, d) + kTile - 1) / kTile : 0;
-    const int nfull = (nc - 1) / NT;
-    const int nv = nc - nfull * NT;
+    const int nblk = (nc + NT - 1) / NT;  // blocks per super-tile
+    const int bsz = nc / nblk, bextra = nc % nblk;
     const McCtx mc{};
     const int row_pitch = a.row_stride;
     const int64_t f_stride = (int64_t)a.nf * a.K;
@@ -953,23 +1071,40 @@ __device__ __forceinline__ void run_toep_item(const ItemDesc &it, const float *r
         RowAcc<1> ra;
         init_row<1, MPV>(ra);
         const uint32_t row = lds_addr(rows0 + r * row_pitch);
-        for (int st = 0; st < s_full; ++st) {
-            const int T = st * span;
-            for (int blk = 0; blk < nfull; ++blk) {
-                const int b0 = T + blk * (NT * kTile) - it.p;
-                if constexpr (CLAMP)
-                    tile_block<TAPS, 1, NT, false, MPV, false>(ClampedTiles{row, b0, d, a.L}, wa, mc, binit, blast, ra);
-                else
-                    tile_block<TAPS, 1, NT, false, MPV, false>(PaddedTiles{row + 4u * (uint32_t)b0, d}, wa, mc, binit,
-                                                               blast, ra);
+        // super-tiles of at most 4 chunks: several per block (padded rows)
+        int st0 = 0;
+        if constexpr (!CLAMP) {
+            switch (nc) {
+                case 1: st0 = toep_runs<TAPS, 1, 4, MPV>(row, it.p, d, span, s_full, wa, binit, blast, ra); break;
+                case 2: st0 = toep_runs<TAPS, 2, 4, MPV>(row, it.p, d, span, s_full, wa, binit, blast, ra); break;
+                case 3: st0 = toep_runs<TAPS, 3, 2, MPV>(row, it.p, d, span, s_full, wa, binit, blast, ra); break;
+                case 4: st0 = toep_runs<TAPS, 4, 2, MPV>(row, it.p, d, span, s_full, wa, binit, blast, ra); break;
+                default: break;
             }
-            const int b0 = T + nfull * (NT * kTile) - it.p;
+        }
+        for (int st = st0; st < s_full; ++st) {
+            const int T = st * span;
+            // nblk blocks of nearly equal size (the first nc % nblk one tile
+            // larger), so that no block is left with one or two tiles
+            int c0 = 0;
+            for (int blk = 0; blk + 1 < nblk; ++blk) {
+                const int sz = bsz + (blk < bextra ? 1 : 0);
+                const int b0 = T + c0 * kTile - it.p;
+                if constexpr (CLAMP)
+                    TailTiles<TAPS, 1, NT, MPV, false, ClampedTiles, false>::run(sz, ClampedTiles{row, b0, d, a.L}, wa,
+                                                                                 mc, binit, blast, ra);
+                else
+                    TailTiles<TAPS, 1, NT, MPV, false, PaddedTiles, false>::run(
+                        sz, PaddedTiles{row + 4u * (uint32_t)b0, d}, wa, mc, binit, blast, ra);
+                c0 += sz;
+            }
+            const int b0 = T + c0 * kTile - it.p;
             if constexpr (CLAMP)
-                TailTiles<TAPS, 1, NT, MPV, false, ClampedTiles>::run(nv, ClampedTiles{row, b0, d, a.L}, wa, mc, binit,
-                                                                      blast, ra);
+                TailTiles<TAPS, 1, NT, MPV, false, ClampedTiles>::run(nc - c0, ClampedTiles{row, b0, d, a.L}, wa, mc,
+                                                                      binit, blast, ra);
             else
-                TailTiles<TAPS, 1, NT, MPV, false, PaddedTiles>::run(nv, PaddedTiles{row + 4u * (uint32_t)b0, d}, wa,
-                                                                     mc, binit, blast, ra);
+                TailTiles<TAPS, 1, NT, MPV, false, PaddedTiles>::run(nc - c0, PaddedTiles{row + 4u * (uint32_t)b0, d},
+                                                                     wa, mc, binit, blast, ra);
         }
         // the last, partial super-tile: chunk by chunk, each slot valid on
         // the lanes whose position is in its chunk's d and below O
