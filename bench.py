@@ -33,16 +33,20 @@ def log(msg):
 
 
 class ClockSampler:
-    """The GPU's shader (GFX) clock, sampled from the AMD SMI library in a
+    """The GPU's shader (GFX) clock, read from the AMD SMI library in a
     background thread while the timed passes run (the device is found by its
-    PCI address).  stop() returns the median, min and max of the samples in
-    MHz and how many were taken, or None where the SMI library is not
-    usable."""
+    PCI address).  The SMI refreshes its readings about once a second, and
+    the first refresh after the start may still cover idle time before it,
+    so only the readings from the second refresh inside the timed region on
+    count: a region shorter than about two refreshes reports no clock.  The
+    reading is the mean over the XCDs of their current GFX clocks (the
+    per-XCD list of the GPU metrics table; the single clock reading where
+    the table lacks it)."""
 
     def __init__(self, device_index=0, interval_s=0.02):
         import threading
         self.interval_s = interval_s
-        self.samples = []
+        self.samples = []  # (time, value in MHz, refresh signature)
         self._stop = threading.Event()
         self._thread = None
         self._smi = None
@@ -56,22 +60,30 @@ class ClockSampler:
             amdsmi.amdsmi_init()
             self._smi = amdsmi
             self._handle = amdsmi.amdsmi_get_processor_handle_from_bdf(bdf)
-            self._read()  # one read up front: fail here, not in the thread
+            if self._read() is None:  # one read up front: fail here, not in the thread
+                raise RuntimeError("no GFX clock reading")
         except Exception as e:  # no SMI access: the line says so
             self.error = "%s: %s" % (type(e).__name__, e)
             self._handle = None
 
     def _read(self):
+        try:
+            m = self._smi.amdsmi_get_gpu_metrics_info(self._handle)
+            xcd = [float(c) for c in (m.get("current_gfxclks") or []) if isinstance(c, (int, float)) and c > 0]
+            if xcd:
+                return float(np.mean(xcd)), tuple(xcd)
+        except Exception:
+            pass
         info = self._smi.amdsmi_get_clock_info(self._handle, self._smi.AmdSmiClkType.GFX)
         clk = info.get("clk")
-        return float(clk) if isinstance(clk, (int, float)) and clk > 0 else None
+        return (float(clk), (float(clk),)) if isinstance(clk, (int, float)) and clk > 0 else None
 
     def _run(self):
         while not self._stop.is_set():
             try:
-                v = self._read()
-                if v is not None:
-                    self.samples.append((time.perf_counter(), v))
+                r = self._read()
+                if r is not None:
+                    self.samples.append((time.perf_counter(), r[0], r[1]))
             except Exception as e:
                 self.error = "%s: %s" % (type(e).__name__, e)
                 return
@@ -84,10 +96,9 @@ class ClockSampler:
             self._thread.start()
         return self
 
-    def stop(self, t_end=None, min_samples=5):
-        """Samples taken after t_end (a perf_counter time: when the device went
-        idle) are dropped; with fewer than min_samples left the timed region
-        was too short to say what the clock was, and mhz is None."""
+    def stop(self, t_end=None):
+        """Readings taken after t_end (a perf_counter time: when the device
+        went idle) are dropped."""
         if self._thread is not None:
             self._stop.set()
             self._thread.join()
@@ -98,15 +109,17 @@ class ClockSampler:
                 pass
         if self._handle is None:
             return {"mhz": None, "source": "amdsmi (unavailable: %s)" % self.error}
-        vals = [v for t, v in self.samples if t_end is None or t <= t_end]
-        if len(vals) < min_samples:
-            return {"mhz": None, "samples": len(vals),
-                    "source": "amdsmi GFX clock: timed region too short for %d samples at %d ms"
-                              % (min_samples, int(self.interval_s * 1e3))}
-        a = np.array(vals)
+        pts = [(v, sig) for t, v, sig in self.samples if t_end is None or t <= t_end]
+        refresh = [i for i in range(1, len(pts)) if pts[i][1] != pts[i - 1][1]]
+        if len(refresh) < 2:
+            return {"mhz": None, "refreshes": len(refresh),
+                    "source": "amdsmi GFX clock: the timed region saw fewer than two refreshes of the "
+                              "SMI readings (about one a second)"}
+        a = np.array([v for v, _ in pts[refresh[1]:]])
         return {"mhz": float(np.median(a)), "min": float(a.min()), "max": float(a.max()),
-                "samples": int(a.size), "source": "amdsmi GFX clock, sampled every %d ms during the timed passes"
-                                                  % int(self.interval_s * 1e3)}
+                "refreshes": len(refresh) - 1,
+                "source": "amdsmi GFX clock (mean over XCDs), read every %d ms during the timed passes, "
+                          "from the second SMI refresh inside them on" % int(self.interval_s * 1e3)}
 
 
 def timed_passes(torch, stream, one_pass, steps):
@@ -176,10 +189,17 @@ def traffic_from_profile(workload, digest, kernel="rocket_fused_kernel"):
     return rec.get("hbm_bytes_per_launch")
 
 
+def add_clock_frac(out):
+    """The roofline fraction against the peak at the shader clock the timed
+    passes ran at (the published peak assumes 2.4 GHz), when it was read."""
+    mhz = out.get("sclk_mhz")
+    out["roofline"]["frac_at_sclk"] = (out["roofline"]["frac"] * 2400.0 / mhz) if mhz else None
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="manufacturing")
     ap.add_argument("--batch-rows", type=int, default=0,
@@ -382,6 +402,7 @@ def main():
         "cpu_baseline": cpu,
         "parity": parity,
     }
+    add_clock_frac(out)
     print(json.dumps(out), flush=True)
 
 
@@ -546,6 +567,7 @@ def bench_minirocket(args):
         "cpu_baseline": cpu,
         "parity": parity,
     }
+    add_clock_frac(out)
     print(json.dumps(out), flush=True)
 
 
