@@ -219,6 +219,10 @@ void rocket_plan_destroy(rocket_plan *p);
  * n == 0 is a no-op.  Rows are independent; any row range of X may be
  * passed (row batching is the caller's loop over pointer offsets).
  * X must be finite (see the rules at the top of this file).
+ * Work may run on streams the plan owns (the Toeplitz items' kernel of a
+ * plan that has them, the series-lane chunks); it starts after the work
+ * queued on hip_stream before the call, and hip_stream waits for all of it,
+ * so the call behaves as one stream-ordered operation on hip_stream.
  * A call that runs the series-lane layout (short series, n >= 4,096 or
  * ROCKET_PLAN_SERIES) allocates the plan's feature buffer on first use, or
  * grows it (hipMalloc, at most 1 GiB; growing first waits for the device),

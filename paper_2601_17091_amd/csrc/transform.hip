@@ -1931,6 +1931,12 @@ struct rocket_plan {
     hipEvent_t aux_done = nullptr;
     hipEvent_t call_start = nullptr;  // the caller's stream at the start of a call (odd waits on it)
     hipEvent_t odd_done = nullptr;    // the odd stream's last chunk of a call
+    // plans with Toeplitz items: their kernel runs on this stream, beside the
+    // fused kernel on the caller's (they write disjoint features)
+    mutable std::mutex side_mu;
+    hipStream_t side = nullptr;
+    hipEvent_t side_start = nullptr;
+    hipEvent_t side_done = nullptr;
     bool mpv = false;        // third feature per kernel: mean of positive values
     bool minirocket = false; // MINIROCKET plan: F [n, n_features], PPV only
     int64_t f_cols = 0;      // columns of F
@@ -1961,10 +1967,11 @@ struct rocket_plan {
 static void plan_free_device(rocket_plan *p) {
     if (p->scratch_done) (void)hipEventDestroy(p->scratch_done);
     for (hipEvent_t ev : {p->half_full[0], p->half_full[1], p->half_free[0], p->half_free[1], p->aux_done,
-                          p->call_start, p->odd_done})
+                          p->call_start, p->odd_done, p->side_start, p->side_done})
         if (ev) (void)hipEventDestroy(ev);
     if (p->aux) (void)hipStreamDestroy(p->aux);
     if (p->odd) (void)hipStreamDestroy(p->odd);
+    if (p->side) (void)hipStreamDestroy(p->side);
     void *ptrs[] = {p->d_scratch, p->d_slot_of, p->d_items, p->d_wpk, p->d_bias, p->d_kid, p->d_order,
                     p->d_split_begin, p->d_thr, p->d_len, p->d_dil, p->d_pad, p->d_b,
                     p->d_w, p->d_cc, p->d_ci};
@@ -2113,6 +2120,13 @@ extern "C" rocket_status rocket_plan_create_ex(const rocket_kernels *k, int32_t 
             if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->aux, hipStreamNonBlocking);
         if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->odd, hipStreamNonBlocking);
+    }
+    if (!p->direct && !p->minirocket &&
+        std::any_of(p->host.items.begin(), p->host.items.end(),
+                    [](const rocket::ItemDesc &it) { return it.variant >= rocket::kToepVariant0; })) {
+        for (hipEvent_t *ev : {&p->side_start, &p->side_done})
+            if (e == hipSuccess) e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipStreamCreateWithFlags(&p->side, hipStreamNonBlocking);
     }
     const int32_t K = k->n_kernels;
     p->max_len = k->max_len;
@@ -2308,7 +2322,7 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     const bool big = big_group;
     const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);
     // ROCKET plans: the Toeplitz items' variants go to a kernel of their
-    // own, launched after the fused kernel's
+    // own
     FusedArgs parts[2] = {a, a};
     const void *fns[2] = {nullptr, nullptr};
     int nparts = 0;
@@ -2329,8 +2343,20 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
             fns[nparts++] = toep_fn(sel & 7);
         }
     }
-    for (int part = 0; part < nparts; ++part) {
+    // a Toeplitz part runs on the plan's side stream, concurrently with the
+    // fused part: it starts after the caller's earlier work and the call
+    // ends on the caller's stream after both
+    const bool side = nparts == 2 && p->side != nullptr;
+    std::unique_lock<std::mutex> side_lock(p->side_mu, std::defer_lock);
+    if (side) {
+        side_lock.lock();
+        if (hipEventRecord(p->side_start, s) != hipSuccess || hipStreamWaitEvent(p->side, p->side_start, 0) != hipSuccess)
+            return ROCKET_ERR_HIP;
+    }
+    rocket_status st = ROCKET_OK;
+    for (int part = nparts - 1; part >= 0 && st == ROCKET_OK; --part) {
         FusedArgs &q = parts[part];
+        hipStream_t sq = (side && part == 1) ? p->side : s;
         const int64_t max_rows =
             ((int64_t)INT_MAX / (nsplit * std::max(q.n_variants, 1)) / kXcds - 1) * kXcds * R;
         for (int64_t r0 = 0; r0 < n; r0 += max_rows) {
@@ -2340,12 +2366,19 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
             q.groups_per_xcd = (groups_now + kXcds - 1) / kXcds;
             const unsigned nb = (unsigned)(kXcds * q.groups_per_xcd * nsplit * q.n_variants);
             void *args[] = {&q};
-            if (hipLaunchKernel(fns[part], dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, s) != hipSuccess)
-                return ROCKET_ERR_HIP;
-            if (hipGetLastError() != hipSuccess) return ROCKET_ERR_HIP;
+            if (hipLaunchKernel(fns[part], dim3(nb), dim3(big ? kBigBlock : kBlock), args, lds, sq) != hipSuccess ||
+                hipGetLastError() != hipSuccess) {
+                st = ROCKET_ERR_HIP;
+                break;
+            }
         }
     }
-    return ROCKET_OK;
+    // also after a failure part-way: the caller's stream waits for whatever
+    // the side stream holds
+    if (side && (hipEventRecord(p->side_done, p->side) != hipSuccess ||
+                 hipStreamWaitEvent(s, p->side_done, 0) != hipSuccess))
+        return ROCKET_ERR_HIP;
+    return st;
 }
 
 // Series-lane layout: the rows go in chunks; for each chunk the series

@@ -145,6 +145,49 @@ def test_integer_series_exact(env, oracle, mode, L, mpv):
     _log("  exact, %d features with some non-positive output" % zeros)
 
 
+# unpadded buckets of one and two kernels at large dilations, and padded
+# ones of one length per dilation (centred kernels of several lengths at one
+# dilation would share longer frames instead)
+TOEP_CASES = {
+    # super-tiles of 1 to 4 chunks (several per block in the padded layout)
+    4000: ([(ln, d, 0, 1 + i % 2) for ln in (7, 9, 11) for i, d in enumerate((60, 64, 65, 100, 129, 190, 200))]
+           + [(11, 70, 1, 1), (9, 90, 1, 2), (7, 140, 1, 1), (11, 110, 1, 2), (9, 1, 1, 16), (7, 1, 0, 8)]),
+    # super-tiles of 9 to 24 chunks (blocks of nearly equal size)
+    16384: [(11, 600, 1, 1), (11, 560, 1, 2), (9, 700, 0, 1), (9, 1000, 1, 2), (7, 900, 0, 2), (11, 1500, 1, 1),
+            (9, 1, 1, 16)],
+}
+
+
+@pytest.mark.parametrize("mpv", [False, True])
+@pytest.mark.parametrize("mode", ["fused", "clamped"])
+@pytest.mark.parametrize("L", sorted(TOEP_CASES))
+def test_integer_toeplitz_exact(env, oracle, L, mode, mpv):
+    """Toeplitz items (a bucket's one or two kernels at a large dilation, the
+    kernel at 4 or 2 tap shifts in one MFMA group), beside MFMA items of
+    8 kernels at dilation 1, on integer data: every feature exact, including
+    the zero and -0 rows.  Super-tiles of 1 to 10 chunks: in the padded
+    layout those of up to 4 chunks run several to a block, longer ones in
+    blocks of nearly equal size; the Toeplitz kernel runs on the plan's own
+    stream beside the fused kernel."""
+    torch, rk = env
+    rng = np.random.default_rng(4242 + L)
+    ks = _int_kernels(rng, L, TOEP_CASES[L])
+    v = rk.plan_tables(ks, L)["items"][:, 0]
+    assert ((v >= 12) & (v % 2 == 0)).any() and ((v >= 12) & (v % 2 == 1)).any() and (v < 6).any()
+    plan = _plan(rk, ks, L, mode, mpv)
+    assert plan.info()["toeplitz_items"] == int((v >= 12).sum())
+    assert plan.info()["clamped"] == (mode == "clamped")
+    X = _int_series(rng, 7, L)
+    _log("integer Toeplitz items L=%d mode=%s mpv=%s, %d kernels" % (L, mode, mpv, ks["length"].shape[0]))
+    F = _transform(env, plan, X)
+    nf = 3 if mpv else 2
+    _assert_exact(F, oracle.transform(X, ks), ks["length"].shape[0], nf, "toeplitz " + mode)
+    b = ks["bias"]
+    for r in (1, 2):
+        np.testing.assert_array_equal(F[r, 1::nf], b)
+        np.testing.assert_array_equal(F[r, 0::nf], (b > 0).astype(np.float32))
+
+
 @pytest.mark.parametrize("mpv", [False, True])
 def test_integer_series_lane_by_call_size(env, oracle, mpv):
     """At least 4,096 short series: the default plan runs the series-lane
