@@ -627,18 +627,31 @@ def sweep(args):
               "host_matches_device": same, "tflops": flops / (dev_ms * 1e-3) / 1e12,
               "series_kernels_per_s": n * K / (dev_ms * 1e-3),
               "ns_per_series_kernel_sample": dev_ms * 1e6 / (n * K * L),
-              "clamped": info["clamped"], "direct": info["direct"]}
+              "clamped": info["clamped"], "direct": info["direct"], "toeplitz_items": info["toeplitz_items"]}
         log("sweep %s" % json.dumps(pt))
         points.append(pt)
         plan.close()
         del X, F, Xh, Fh
     base = points[0]["ns_per_series_kernel_sample"]
     rel = [p["ns_per_series_kernel_sample"] / base for p in points]
+    for p, r in zip(points, rel):
+        p["time_per_unit_vs_default"] = r
+    # per factor: the exponent of a least-squares fit log(time) = a + e log(x)
+    # over the points that vary it (with the default point); 1 is linear
+    exponents = {}
+    d0 = SWEEP_POINTS[0]
+    for i, name in enumerate(("n", "L", "K")):
+        sel = [p for p, q in zip(points, SWEEP_POINTS)
+               if all(q[j] == d0[j] for j in range(3) if j != i)]
+        x = np.log([float(p[name]) for p in sel])
+        y = np.log([p["device_ms"] for p in sel])
+        exponents[name] = float(np.polyfit(x, y, 1)[0]) if len(sel) > 1 else None
     out = {"metric": "ROCKET transform time over the paper's n/L/K sweep (fp32, 1 MI355X)",
            "unit": "ms", "dtype": "fp32", "data": "synthetic (seeded random walks; seeded ROCKET kernels)",
            "config": {"workload": "paper_sweep", "default": {"n": 1000, "L": 10000, "K": 10000}},
            "points": points,
-           "linearity": {"time_per_unit_vs_default_min": min(rel), "time_per_unit_vs_default_max": max(rel)},
+           "linearity": {"time_per_unit_vs_default_min": min(rel), "time_per_unit_vs_default_max": max(rel),
+                         "time_exponent": exponents},
            "source_digest": source_digest()}
     print(json.dumps(out), flush=True)
 
