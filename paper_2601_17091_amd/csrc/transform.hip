@@ -572,6 +572,31 @@ struct TailTiles<ELL, G, 0, MPV, MC, Src, LASTB> {
                                                RowAcc<G> &) {}
 };
 
+// The last block of a row and then the row's epilogue, a code copy per
+// tile count nv (1..N): each copy reduces and writes the features from the
+// registers its own block left the accumulators in (one epilogue after the
+// copies would first have to move them into common registers).
+template <int ELL, int G, int N, bool MPV, bool MC, typename Src>
+struct TailTilesThen {
+    template <typename Epi>
+    __device__ __forceinline__ static void run(int nv, const Src &src, const float (&wa)[G][ELL],
+                                               const McCtx &mc, const v4f (&binit)[G],
+                                               const v4f (&blast)[G], RowAcc<G> &ra, const Epi &epi) {
+        if (nv == N) {
+            tile_block<ELL, G, N, true, MPV, MC>(src, wa, mc, binit, blast, ra);
+            epi(ra);
+        } else {
+            TailTilesThen<ELL, G, N - 1, MPV, MC, Src>::run(nv, src, wa, mc, binit, blast, ra, epi);
+        }
+    }
+};
+template <int ELL, int G, bool MPV, bool MC, typename Src>
+struct TailTilesThen<ELL, G, 0, MPV, MC, Src> {
+    template <typename Epi>
+    __device__ __forceinline__ static void run(int, const Src &, const float (&)[G][ELL], const McCtx &,
+                                               const v4f (&)[G], const v4f (&)[G], RowAcc<G> &, const Epi &) {}
+};
+
 // Combining operations of the wavefront reductions: max for MAX, sum for
 // the MPV numerator.
 struct OpMax {
@@ -737,6 +762,19 @@ __device__ __forceinline__ void write_row(const RowAcc<G> &ra, int okid, double 
     }
 }
 
+// The row epilogue of run_item as a function object (write_row with the
+// item's writer lane, 1/O and the row's F pointer).
+template <int G, bool MPV>
+struct RowWriter {
+    int okid;
+    double inv_O;
+    float *Frow;
+    bool hi8;
+    __device__ __forceinline__ void operator()(const RowAcc<G> &ra) const {
+        write_row<G, MPV>(ra, okid, inv_O, Frow, hi8);
+    }
+};
+
 // One work item over the `nrows` series staged in LDS: the item's weights
 // are loaded once and reused for every series.  Each series runs the item's
 // tiles in blocks of NT (the last block holds the remaining 1..NT tiles).
@@ -801,13 +839,13 @@ __device__ __forceinline__ void run_item(const ItemDesc &it, const float *rows0,
                                                        mc, binit, blast, ra);
         }
         const int b0 = nfull * (NT * kTile) - it.p;
+        const RowWriter<G, MPV> epi{okid, it.inv_O, F0 + r * f_stride, hi8};
         if constexpr (CLAMP)
-            TailTiles<ELL, G, NT, MPV, MC, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, mc,
-                                                              binit, blast, ra);
+            TailTilesThen<ELL, G, NT, MPV, MC, ClampedTiles>::run(nv, ClampedTiles{row, b0, it.d, a.L}, wa, mc,
+                                                                  binit, blast, ra, epi);
         else
-            TailTiles<ELL, G, NT, MPV, MC, PaddedTiles>::run(
-                nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra);
-        write_row<G, MPV>(ra, okid, it.inv_O, F0 + r * f_stride, hi8);
+            TailTilesThen<ELL, G, NT, MPV, MC, PaddedTiles>::run(
+                nv, PaddedTiles{row + 4u * (uint32_t)b0, it.d}, wa, mc, binit, blast, ra, epi);
     }
 }
 
