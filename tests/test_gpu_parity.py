@@ -279,3 +279,35 @@ def test_toeplitz_items(torch_gpu, rk, oracle, mode, mpv):
     F = plan.transform(Xd)
     torch_gpu.cuda.synchronize()
     (assert_mpv_parity if mpv else assert_parity)(F.cpu().numpy(), oracle.transform(X, ks), "toeplitz")
+
+
+def test_toeplitz_plan_two_streams(torch_gpu, rk):
+    """A plan with Toeplitz items runs their kernel on a stream of its own,
+    beside the fused kernel on the caller's stream.  Transforms of one such
+    plan issued on two streams at once (and a third waiting on neither) each
+    equal the one-stream result, bit for bit; the features of every call are
+    complete when its own stream is synchronised."""
+    torch = torch_gpu
+    L = 5000
+    ks = rk.generate_kernels(31, 2000, L)
+    plan = rk.Plan(ks, L)
+    assert plan.info()["toeplitz_items"] > 0
+    rng = np.random.default_rng(31)
+    Xa = torch.from_numpy(np.cumsum(rng.standard_normal((40, L)), axis=1).astype(np.float32)).cuda()
+    Xb = torch.from_numpy(np.cumsum(rng.standard_normal((70, L)), axis=1).astype(np.float32)).cuda()
+    want_a = plan.transform(Xa)
+    want_b = plan.transform(Xb)
+    torch.cuda.synchronize()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    Fa = torch.empty_like(want_a)
+    Fb = torch.empty_like(want_b)
+    for _ in range(3):
+        Fa.fill_(float("nan"))
+        Fb.fill_(float("nan"))
+        torch.cuda.synchronize()
+        plan.transform_into(Xa, Fa, sa)
+        plan.transform_into(Xb, Fb, sb)
+        sa.synchronize()
+        assert torch.equal(Fa, want_a)
+        sb.synchronize()
+        assert torch.equal(Fb, want_b)
