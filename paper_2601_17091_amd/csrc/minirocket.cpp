@@ -213,12 +213,13 @@ rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan 
                 // kernels k = 2 kappa + par have i + k even (padded) or odd
                 const int par = padded ? (i & 1) : ((i + 1) & 1);
                 for (int32_t q0 = 0; q0 < nf;) {
-                    // chunks of 8 biases; a remainder of 1..4 takes a chunk of 4
+                    // chunks of 8 biases; a remainder of 4 takes a chunk of 4,
+                    // one of 1..3 a chunk of 3 (5..7: 8)
                     const int32_t rest = nf - q0;
-                    const int32_t nq = rest > kMrQSmall ? kMrQLarge : kMrQSmall;
+                    const int32_t nq = rest > kMrQSmall ? kMrQLarge : (rest == kMrQSmall ? kMrQSmall : kMrQTiny);
                     ItemDesc it;
                     std::memset(&it, 0, sizeof(it));
-                    it.variant = 2 * par + (nq == kMrQLarge ? 1 : 0);
+                    it.variant = mr_variant(par, nq);
                     it.d = d;
                     it.p = p;
                     it.O = (int32_t)O;

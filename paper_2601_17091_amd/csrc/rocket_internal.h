@@ -49,7 +49,7 @@ constexpr int64_t kMaxOutputs = (int64_t)1 << 24;  // O must stay below 2^24
 // MINIROCKET items use d, p, O, n_tiles, cost, t_off, nq and inv_O as named,
 // and three fields for their feature numbering: w_off = the first feature of
 // the item's dilation, k_off = the item's first bias (of each kernel), n_ch =
-// the dilation's features per kernel; variant = 2 * parity + (nq == 8).
+// the dilation's features per kernel; variant = mr_variant(parity, nq).
 struct alignas(16) ItemDesc {
     int32_t variant;   // ell_index * 2 + (G - 1)
     int32_t d;         // dilation
@@ -62,7 +62,7 @@ struct alignas(16) ItemDesc {
     int32_t n_ch;      // channels the item's kernels read (their union; 1 if univariate)
     int32_t ch_off;    // first entry of the item's channel list
     int32_t t_off;     // MINIROCKET: first threshold, [kMrKappa][nq] floats
-    int32_t nq;        // MINIROCKET: thresholds per kernel in this item (kMrQSmall or kMrQLarge)
+    int32_t nq;        // MINIROCKET: thresholds per kernel in this item (kMrQTiny, kMrQSmall or kMrQLarge)
     uint32_t ch_mask[2];  // multichannel: the item's channels as a bit mask (lo, hi words)
     double inv_O;      // 1 / O rounded to double (exact PPV, see transform.hip)
 };
@@ -104,14 +104,19 @@ constexpr int kSplitCounts[kNumSplitLayouts] = {1, 2, 4, 8, 16, 32};
 // MINIROCKET (Sec. 5 names it): 84 kernels of 9 taps.  Pair (dilation i,
 // kernel k) is padded when i + k is even, so at one (dilation, padding) the
 // kernels are those of one parity of k: an item holds those 42 kernels and
-// kMrQSmall or kMrQLarge of each kernel's biases (dummy biases of +inf fill
-// the last chunk; C > +inf never holds).
+// kMrQTiny, kMrQSmall or kMrQLarge of each kernel's biases (dummy biases of
+// +inf fill the last chunk; C > +inf never holds).  Variant = 3 * parity +
+// bias class (0: kMrQSmall, 1: kMrQLarge, 2: kMrQTiny).
 constexpr int kMrKernels = 84;
 constexpr int kMrTaps = 9;
 constexpr int kMrKappa = kMrKernels / 2;
+constexpr int kMrQTiny = 3;
 constexpr int kMrQSmall = 4;
 constexpr int kMrQLarge = 8;
-constexpr int kMrNumVariants = 4;  // parity x {kMrQSmall, kMrQLarge}
+constexpr int kMrNumVariants = 6;  // parity x {kMrQSmall, kMrQLarge, kMrQTiny}
+constexpr int mr_variant(int parity, int nq) {
+    return 3 * parity + (nq == kMrQLarge ? 1 : (nq == kMrQTiny ? 2 : 0));
+}
 
 struct HostPlan {
     bool minirocket = false;

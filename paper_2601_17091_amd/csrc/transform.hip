@@ -1793,7 +1793,7 @@ __device__ __forceinline__ void run_mr_items(int *next_item, int beg, int cnt_it
     }
 }
 
-// MINIROCKET workgroup: as rocket_fused_kernel; variant = 2 * parity + (NQ == 8).
+// MINIROCKET workgroup: as rocket_fused_kernel; variant = mr_variant(parity, NQ).
 template <int BLOCK, bool CLAMP>
 __global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
     extern __shared__ __align__(16) float smem[];
@@ -1807,8 +1807,10 @@ __global__ __launch_bounds__(BLOCK) void rocket_minirocket_kernel(FusedArgs a) {
     switch (w.variant) {
         case 0: run_mr_items<0, rocket::kMrQSmall, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
         case 1: run_mr_items<0, rocket::kMrQLarge, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        case 2: run_mr_items<1, rocket::kMrQSmall, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
-        default: run_mr_items<1, rocket::kMrQLarge, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 2: run_mr_items<0, rocket::kMrQTiny, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 3: run_mr_items<1, rocket::kMrQSmall, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        case 4: run_mr_items<1, rocket::kMrQLarge, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
+        default: run_mr_items<1, rocket::kMrQTiny, CLAMP>(&next_item, beg, cnt, rows0, nr, a, F0, lane); break;
     }
 }
 
