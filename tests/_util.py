@@ -186,7 +186,11 @@ def parity_report(F_gpu, ref):
     return dict(
         max_abs_err=float(dmax.max()) if dmax.size else 0.0,
         max_count_err=int(dcnt.max()) if dcnt.size else 0,
-        ppv_not_integral=int((np.abs(ppv * O - cnt) > 1e-3).sum()),
+        # PPV must be the fp32 quotient (float)count / (float)O, correctly
+        # rounded (exact at any O; a fixed tolerance on PPV * O - count
+        # would not be: half an ulp of PPV times O reaches 1e-3 at O ~ 33,500)
+        ppv_not_integral=int((F_gpu[:, 0::2].astype(np.float32)
+                              != cnt.astype(np.float32) / O.astype(np.float32)).sum()),
         outside_count_interval=int(((cnt < ref["cnt_lo"]) | (cnt > ref["cnt_hi"])).sum()),
         max_beyond_bound=int((dmax > ref["beta"]).sum()),
         nonfinite=int((~np.isfinite(F_gpu)).sum()),

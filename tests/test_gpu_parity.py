@@ -176,6 +176,25 @@ def test_longest_sweep_length_every_row(torch_gpu, rk, oracle, mode):
     assert_parity(F, oracle.transform(X, ks), "L20000")
 
 
+@pytest.mark.parametrize("L,layout", [(39000, "clamped"), (50000, "direct")])
+def test_longest_rows_layouts(torch_gpu, rk, oracle, L, layout):
+    """Rows near and past the LDS limit, with the default plan: at 39,000
+    samples even one padded row with its margins does not fit a workgroup's
+    LDS, so the plan takes the clamped layout by itself; at 50,000 not even
+    the clamped row fits and the plan falls back to the direct kernel.  Both
+    against the oracle on every row and kernel."""
+    from paper_2601_17091_amd.workloads import make_series
+    ks = rk.generate_kernels(208, 200, L)
+    X = make_series("random_walk", 2, L, 108)
+    plan = rk.Plan(ks, L)
+    info = plan.info()
+    assert info["clamped"] == (layout == "clamped") and info["direct"] == (layout == "direct"), info
+    _log("length %d, K=200, 2 rows, %s layout chosen by the plan" % (L, layout))
+    F = plan.transform(torch_gpu.from_numpy(X).cuda())
+    torch_gpu.cuda.synchronize()
+    assert_parity(F.cpu().numpy(), oracle.transform(X, ks), "L%d" % L)
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_all_lengths_and_extremes(torch_gpu, rk, oracle, mode):
     """Hand-built kernels of every length 1..11, with dilation 1, 2 and the
