@@ -195,6 +195,29 @@ def test_longest_rows_layouts(torch_gpu, rk, oracle, L, layout):
     assert_parity(F.cpu().numpy(), oracle.transform(X, ks), "L%d" % L)
 
 
+def test_largest_output_count(torch_gpu, rk, oracle):
+    """The largest number of dot products a kernel may have: O just below
+    2^24 (the bound that keeps counts exact in fp32), in a 16,777,215-sample
+    series that only the direct kernel can take.  PPV = count / O then needs
+    all 24 bits of the fp32 quotient."""
+    rng = np.random.default_rng(5)
+    L = (1 << 24) - 1
+    lengths = [9, 7, 11, 9]
+    dil = [1, 3, 2, 1]
+    pad = [0, 0, 0, 4]  # the last one centred: O = L
+    ks = kernel_set(lengths, dil, pad, [0.1, -0.2, 0.0, 0.05], [rng.standard_normal(n) for n in lengths])
+    X = np.cumsum(rng.standard_normal((1, L)), axis=1).astype(np.float32)
+    X = ((X - X.mean()) / X.std()).astype(np.float32)
+    plan = rk.Plan(ks, L)
+    assert plan.info()["direct"]
+    _log("one series of %d samples, O up to %d, direct kernel" % (L, L))
+    F = plan.transform(torch_gpu.from_numpy(X).cuda())
+    torch_gpu.cuda.synchronize()
+    ref = oracle.transform(X, ks)
+    assert int(ref["O"].max()) == L
+    assert_parity(F.cpu().numpy(), ref, "O = 2^24 - 1")
+
+
 @pytest.mark.parametrize("mode", MODES)
 def test_all_lengths_and_extremes(torch_gpu, rk, oracle, mode):
     """Hand-built kernels of every length 1..11, with dilation 1, 2 and the
