@@ -1300,9 +1300,10 @@ __global__ __launch_bounds__(BLOCK) void rocket_fused_kernel(FusedArgs a) {
 }
 
 // Toeplitz items (univariate long-series plans) in a kernel of their own,
-// launched after the fused kernel over the same row groups: in the fused
-// kernel's code their extra tap counts raise the scalar-register pressure of
-// every variant's loop.
+// launched over the same row groups on a stream of the plan, beside the
+// fused kernel (the two write disjoint features): in the fused kernel's code
+// their extra tap counts raise the scalar-register pressure of every
+// variant's loop.
 template <int BLOCK, bool CLAMP, bool MPV>
 __global__ __launch_bounds__(BLOCK) void rocket_toeplitz_kernel(FusedArgs a) {
     extern __shared__ __align__(16) float smem[];

@@ -162,6 +162,21 @@ def test_paper_sweep_sampled(torch_gpu, rk, oracle):
     _sampled(torch_gpu, rk, oracle, "paper_sweep", total=ROWS_PAPER_SWEEP)
 
 
+def test_largest_sweep_kernel_set(torch_gpu, rk, oracle):
+    """The largest kernel set of the paper's sweep (Sec. 4): 20,000 kernels on
+    series of 10,000 samples (the sweep's generator seeds), every feature of
+    3 rows against the oracle."""
+    from paper_2601_17091_amd.workloads import make_series
+    L, K = 10000, 20000
+    ks = rk.generate_kernels(206, K, L)
+    X = make_series("random_walk", 3, L, 106)
+    _log("sweep point K=%d L=%d, 3 rows" % (K, L))
+    plan = rk.Plan(ks, L)
+    F = plan.transform(torch_gpu.from_numpy(X).cuda())
+    torch_gpu.cuda.synchronize()
+    assert_parity(F.cpu().numpy(), oracle.transform(X, ks), "K20000")
+
+
 @pytest.mark.parametrize("mode", ["fused", "clamped"])
 def test_longest_sweep_length_every_row(torch_gpu, rk, oracle, mode):
     """Series of length 20,000, the longest of the paper's sweep: one staged
