@@ -228,9 +228,10 @@ void rocket_plan_destroy(rocket_plan *p);
  * grows it (hipMalloc, at most 1 GiB; growing first waits for the device),
  * and makes the stream wait on the device for the previous call that used
  * the buffer.
- * Errors: ROCKET_ERR_INVALID_ARG (p, X_dev or F_dev NULL with n > 0, n < 0);
- *         ROCKET_ERR_OOM (the feature buffer); ROCKET_ERR_HIP (launch
- *         failure).
+ * The plan's device must be the current HIP device.
+ * Errors: ROCKET_ERR_INVALID_ARG (p, X_dev or F_dev NULL with n > 0, n < 0,
+ *         the current device not the plan's); ROCKET_ERR_OOM (the feature
+ *         buffer); ROCKET_ERR_HIP (launch failure).
  */
 rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
                                     float *F_dev, void *hip_stream);
@@ -285,8 +286,10 @@ rocket_status rocket_transform(const float *X_dev, int64_t n, int32_t L, const r
  * pageable buffers work but the copies then serialise.  The function
  * allocates and frees its own device staging buffers (2 x batch of X and
  * of F).  n == 0 is a no-op.
+ * The plan's device must be the current HIP device.
  * Errors: ROCKET_ERR_INVALID_ARG (p NULL, n < 0, X_host or F_host NULL with
- *         n > 0, batch_rows < 0); ROCKET_ERR_OOM; ROCKET_ERR_HIP.
+ *         n > 0, batch_rows < 0, the current device not the plan's);
+ *         ROCKET_ERR_OOM; ROCKET_ERR_HIP.
  */
 rocket_status rocket_transform_host(const rocket_plan *p, const float *X_host, int64_t n,
                                     float *F_host, int64_t batch_rows, void *hip_stream);
@@ -380,11 +383,14 @@ rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out);
  *                order[split_begin[layout_off[i] + v*ns + s] ..
  *                      split_begin[layout_off[i] + v*ns + s + 1]), v = 0..17
  *   halo_lo, halo_hi, row_stride  zero margins and LDS row length (floats)
- *                of the padded layout (every tap of every real output lands
- *                inside the row)
- *   tail_pad     zeros staged after the last row of a workgroup, so that
- *                the lanes past O of an item's last tile read inside the
- *                staged memory
+ *                of the padded layout: a staged row is halo_lo zeros then
+ *                the series (row_stride floats in all), and its right
+ *                margin of halo_hi <= halo_lo zeros is the next row's left
+ *                margin (every tap of every real output reads the zero-
+ *                padded series)
+ *   tail_pad     zeros staged after the last row of a workgroup: its right
+ *                margin, then room for the lanes past O of an item's last
+ *                tile, so that every read stays inside the staged memory
  */
 typedef struct {
     int64_t n_items;

@@ -196,10 +196,11 @@ rocket_status build_minirocket_plan(const rocket_minirocket_params *m, HostPlan 
         if (L + 8 * dmax > ((int64_t)1 << 30)) {
             P.halo_lo = P.halo_hi = P.row_stride = 0;
         } else {
+            // rows share their zero margins, as in ROCKET plans
             P.halo_lo = P.halo_hi = (int32_t)(4 * dmax);
-            P.row_stride = (int32_t)(L + 8 * dmax);
+            P.row_stride = (int32_t)(L + 4 * dmax);
         }
-        P.tail_pad = kTile;
+        P.tail_pad = P.halo_hi + kTile;
         P.n_buckets = 2 * (int64_t)m->n_dilations;
         const float inf = std::numeric_limits<float>::infinity();
         int64_t fstart = 0;  // first feature of the current dilation

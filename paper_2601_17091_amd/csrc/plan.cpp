@@ -287,7 +287,9 @@ static rocket_status build_plan(const rocket_kernels *k, int32_t L, bool allow_t
         // the taps of real outputs reach from position -p to L-1+p, plus
         // (ell - length) taps of zero weight for kernels run at a longer
         // code length; lanes past O in an item's last tile read up to 63
-        // positions further (tail_pad, below)
+        // positions further (the next row's data, or after the last row the
+        // tail, tail_pad below: those lanes start from -inf, so what they
+        // read changes no feature)
         int64_t halo_lo = 0, halo_hi = 0;
         for (int32_t i = 0; i < k->n_kernels; ++i) {
             const int32_t len = k->length[i], d = k->dilation[i], p = k->padding[i];
@@ -297,18 +299,21 @@ static rocket_status build_plan(const rocket_kernels *k, int32_t L, bool allow_t
             halo_hi = std::max<int64_t>(halo_hi, (int64_t)p + (ell_eff - len) * (int64_t)d);
         }
         P.n_buckets = (int64_t)buckets.size();
-        // margins rounded so that the series starts, and every staged row
-        // spans, a whole number of 16-byte words: rows are then staged with
-        // 16-byte loads and LDS writes (for series lengths divisible by 4)
-        halo_lo = (halo_lo + 3) / 4 * 4;
-        halo_hi += (4 - (halo_lo + L + halo_hi) % 4) % 4;
-        const int64_t stride = halo_lo + L + halo_hi;
-        if (stride > (int64_t)1 << 30) {
+        // Consecutive staged rows share their zero margins: each row is a
+        // left margin of h zeros and the series, and its right margin is the
+        // next row's left margin (after the last row, the tail), so
+        // h = max(halo_lo, halo_hi).  The margin is rounded so that the
+        // series starts, and every staged row spans, a whole number of
+        // 16-byte words: rows are then staged with 16-byte loads and LDS
+        // writes (for series lengths divisible by 4).
+        const int64_t h = (std::max(halo_lo, halo_hi) + 3) / 4 * 4;
+        const int64_t stride = (h + L + 3) / 4 * 4;
+        if (stride + h > (int64_t)1 << 30) {
             // cannot be staged; the plan will use the direct kernel
             P.halo_lo = P.halo_hi = P.row_stride = 0;
         } else {
-            P.halo_lo = (int32_t)halo_lo;
-            P.halo_hi = (int32_t)halo_hi;
+            P.halo_lo = (int32_t)h;
+            P.halo_hi = (int32_t)h;
             P.row_stride = (int32_t)stride;
         }
 
@@ -479,7 +484,9 @@ static rocket_status build_plan(const rocket_kernels *k, int32_t L, bool allow_t
             }
         }
 
-        P.tail_pad = kTile;
+        // after the last row: its right margin, then the reads of lanes past
+        // O in an item's last tile (up to 63 positions further)
+        P.tail_pad = P.halo_hi + kTile;
 
         build_item_orders(P);
         *out = std::move(P);

@@ -270,7 +270,7 @@ constexpr int kBlock = 256;       // 4 wavefronts per workgroup
 constexpr int kBigBlock = 1024;   // 16 wavefronts share one large staged row
 constexpr int64_t kBigLds = 40 * 1024;  // staged rows above this use kBigBlock
 constexpr int64_t kRowsLdsBudget = 30 * 1024;  // LDS for the series of one workgroup (5 per CU)
-constexpr int kMaxRowsPerBlock = 8;
+constexpr int kMaxRowsPerBlock = 7;
 constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dealt round-robin
 constexpr int kTile = rocket::kTile;
 
@@ -2048,11 +2048,13 @@ static bool choose_layout(rocket_plan *p, bool clamped, const hipDeviceProp_t &p
         p->tail_pad = p->host.tail_pad;
         return true;
     }
-    if ((*lds = layout(L + 2 * rocket::kClampMargin, p->host.tail_pad, &p->rows_per_block)) <= limit) {
+    // the clamped layout: each row keeps both of its margins; zeros after
+    // the last row cover the reads of lanes past O
+    if ((*lds = layout(L + 2 * rocket::kClampMargin, rocket::kTile, &p->rows_per_block)) <= limit) {
         p->clamp = true;
         p->halo_lo = rocket::kClampMargin;
         p->row_stride = (int32_t)(L + 2 * rocket::kClampMargin);
-        p->tail_pad = p->host.tail_pad;
+        p->tail_pad = rocket::kTile;
         return true;
     }
     return false;
@@ -2581,9 +2583,19 @@ static rocket_status launch_fused(const rocket_plan *p, const float *X, int64_t 
                                                   : launch_groups(p, false, X, n, F, nullptr, 0, s);
 }
 
+// The plan's streams, events and tables live on the device it was created
+// on: that device must be the current one.
+static rocket_status check_plan_device(const rocket_plan *p) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return ROCKET_ERR_HIP;
+    return dev == p->device ? ROCKET_OK : ROCKET_ERR_INVALID_ARG;
+}
+
 extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float *X_dev, int64_t n,
                                                float *F_dev, void *hip_stream) {
     if (!p || n < 0) return ROCKET_ERR_INVALID_ARG;
+    const rocket_status dst = check_plan_device(p);
+    if (dst != ROCKET_OK) return dst;
     if (n == 0) return ROCKET_OK;
     if (!X_dev || !F_dev) return ROCKET_ERR_INVALID_ARG;
     hipStream_t s = (hipStream_t)hip_stream;
@@ -2593,9 +2605,9 @@ extern "C" rocket_status rocket_transform_plan(const rocket_plan *p, const float
 extern "C" rocket_status rocket_transform_plan_noalloc(const rocket_plan *p, const float *X_dev, int64_t n,
                                                        float *F_dev, void *hip_stream) {
     if (!p || n < 0) return ROCKET_ERR_INVALID_ARG;
-    int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess) return ROCKET_ERR_HIP;
-    if (dev != p->device) return ROCKET_ERR_INVALID_ARG;  // the plan's device must be current
+    const rocket_status dst = check_plan_device(p);
+    if (dst != ROCKET_OK) return dst;
+    const int dev = p->device;
     float *buf = nullptr;
     const rocket_status st = noalloc_scratch(dev, &buf);
     if (st != ROCKET_OK) return st;
@@ -2616,6 +2628,8 @@ extern "C" rocket_status rocket_transform_host(const rocket_plan *p, const float
                                                float *F_host, int64_t batch_rows,
                                                void *hip_stream) {
     if (!p || n < 0 || batch_rows < 0) return ROCKET_ERR_INVALID_ARG;
+    const rocket_status dst = check_plan_device(p);
+    if (dst != ROCKET_OK) return dst;
     if (n == 0) return ROCKET_OK;
     if (!X_host || !F_host) return ROCKET_ERR_INVALID_ARG;
     const int64_t L = (int64_t)p->host.L * p->C;  // floats per series (every channel)

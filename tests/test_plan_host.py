@@ -6,10 +6,12 @@ them: an item's O outputs are computed in ceil(O/64) tiles of 64 consecutive
 positions, lane l of tile k computing output 64k + l; tiles run in blocks of
 NT (8 for 4-kernel items, 4 for 8-kernel items); for tap j, lane l of tile u
 of the block that starts at output t0 reads series index t0 - p + j*d +
-64u + l.  In the padded layout that index is used as is (zero margins of
-halo_lo / halo_hi floats around the series, tail_pad zeros after the last
-row); in the clamped layout the block's offset t0 - p + j*d is clamped into
-[-512, L] first (512 zeros on each side of the series).  Lanes past O start
+64u + l.  In the padded layout that index is used as is (staged rows of
+halo_lo zeros and the series, consecutive rows sharing their margins, so a
+row's right margin of halo_hi zeros is the next row's left margin, and
+tail_pad zeros after the last row); in the clamped layout the block's
+offset t0 - p + j*d is clamped into [-512, L] first (512 zeros on each side
+of the series).  Lanes past O start
 from -inf on the GPU and change no feature.  The checks: every output of
 every kernel is computed by exactly one lane, every load stays inside the
 staged memory, every load of a real output reads the zero-padded series
@@ -71,7 +73,7 @@ def tile_reads(f, ell, L, clamped):
     return off[:, None, :] + (u * TILE)[:, None, None] + np.arange(TILE)[None, :, None]
 
 
-def walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows, clamped, cover, F):
+def walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows, clamped, cover, F, right_end):
     """A Toeplitz item (one or two leftover kernels at dilation d): slot s is
     kernel s // sigma shifted by h = s % sigma taps over ell + sigma - 1 taps;
     super-tiles of sigma*d outputs per kernel in ceil(d/64) chunks, run in
@@ -143,7 +145,7 @@ def walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows, clamped, co
             inside = (ti >= 0) & (ti < L)
             assert np.array_equal(ri[inside], ti[inside])
             assert np.all((ri[~inside] < 0) | (ri[~inside] >= L))
-            assert (halo_lo + ri).max() < stride
+            assert (halo_lo + ri).max() < right_end
             vals.append((s_, real, pos))
         cover[k] = cov
         if rows is not None:
@@ -168,8 +170,16 @@ def walk(tables, kernels, L, X=None, clamped=False):
     halo_lo, halo_hi, stride, pad = (tables["halo_lo"], tables["halo_hi"], tables["row_stride"],
                                      tables["tail_pad"])
     if clamped:
-        halo_lo, halo_hi, stride = CLAMP_MARGIN, CLAMP_MARGIN, L + 2 * CLAMP_MARGIN
-    assert stride == halo_lo + L + halo_hi and pad >= TILE - 1
+        # each row keeps both margins; TILE zeros after the last row
+        halo_lo, halo_hi, stride, pad = CLAMP_MARGIN, CLAMP_MARGIN, L + 2 * CLAMP_MARGIN, TILE
+        assert stride == halo_lo + L + halo_hi
+    else:
+        # consecutive rows share their margins: a row is halo_lo zeros and the
+        # series; its right margin is the next row's left margin or, after the
+        # last row, the first halo_hi zeros of the tail
+        assert stride >= halo_lo + L and halo_hi <= halo_lo and stride % 4 == 0 and halo_lo % 4 == 0
+        assert pad >= halo_hi + TILE - 1
+    right_end = halo_lo + L + halo_hi   # end of the zeros right of a row's series
     cover = [np.zeros(0, np.int64)] * K
     F = None
     if X is not None:
@@ -182,7 +192,7 @@ def walk(tables, kernels, L, X=None, clamped=False):
         f = item_fields(row)
         if f["variant"] >= TOEP0:
             walk_toeplitz(f, tables, kernels, L, halo_lo, stride, pad, rows if X is not None else None, clamped,
-                          cover, F)
+                          cover, F, right_end)
             continue
         d, p, O = f["d"], f["p"], f["O"]
         ell, G, nk = variant_info(f["variant"])
@@ -237,7 +247,7 @@ def walk(tables, kernels, L, X=None, clamped=False):
         # loads of real outputs inside the row, at the zero-padded series value
         true_idx = t[:, :, None] - p + np.arange(ell)[None, None, :] * d
         ri, ti = idx[real], true_idx[real]
-        assert (halo_lo + ri).max() < stride
+        assert (halo_lo + ri).max() < right_end
         inside = (ti >= 0) & (ti < L)
         assert np.array_equal(ri[inside], ti[inside])
         assert np.all((ri[~inside] < 0) | (ri[~inside] >= L))
