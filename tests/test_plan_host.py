@@ -305,6 +305,24 @@ def test_generated_sets_cover_every_output(seed, K, L):
     check_tables(rk.generate_kernels(seed, K, L), L)
 
 
+def _random_cases(n, seed=2024):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        L = int(np.exp(rng.uniform(np.log(11), np.log(20000))))
+        cases.append((int(rng.integers(0, 1 << 30)), int(rng.integers(1, 1500)), L))
+    return cases
+
+
+@pytest.mark.parametrize("seed,K,L", _random_cases(40))
+def test_random_sets_cover_every_output(seed, K, L):
+    """Generated sets at random sizes (L log-uniform from 11 to 20,000, K up
+    to 1,500): MFMA, VALU and Toeplitz items in every mix the planner makes;
+    every output computed once and every load inside the staged memory in
+    both row layouts."""
+    check_tables(rk.generate_kernels(seed, K, L), L)
+
+
 @pytest.mark.parametrize("seed,K,L", [(11, 120, 11), (12, 150, 64), (13, 200, 300)])
 def test_emulated_walk_matches_oracle(oracle, seed, K, L):
     rng = np.random.default_rng(seed)
