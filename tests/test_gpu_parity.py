@@ -270,6 +270,24 @@ def test_random_small_cases(torch_gpu, rk, oracle, seed, mode):
     assert_parity(F, oracle.transform(X, ks), "random")
 
 
+@pytest.mark.parametrize("seed,mode", [(20, "fused"), (21, "fused"), (22, "clamped"), (23, "fused"),
+                                       (24, "clamped"), (25, "fused")])
+def test_random_generated_sets(torch_gpu, rk, oracle, seed, mode):
+    """Generated kernel sets at random sizes (L log-uniform from 500 to
+    8,000, K from 200 to 1,500, 2 to 5 series): MFMA, VALU and Toeplitz items
+    in whatever mix the planner makes, against the oracle."""
+    from paper_2601_17091_amd.workloads import make_series
+    rng = np.random.default_rng(seed)
+    L = int(np.exp(rng.uniform(np.log(500), np.log(8000))))
+    K = int(rng.integers(200, 1500))
+    n = int(rng.integers(2, 6))
+    ks = rk.generate_kernels(1000 + seed, K, L)
+    X = make_series("random_walk", n, L, 2000 + seed)
+    _log("random generated set seed=%d L=%d K=%d n=%d mode=%s" % (seed, L, K, n, mode))
+    F, plan = run(rk, torch_gpu, X, ks, mode)
+    assert_parity(F, oracle.transform(X, ks), "random L=%d K=%d" % (L, K))
+
+
 @pytest.mark.parametrize("mode", ["fused", "clamped"])
 @pytest.mark.parametrize("mpv", [False, True])
 def test_valu_items(torch_gpu, rk, oracle, mode, mpv):
