@@ -503,6 +503,27 @@ rocket_status rocket_minirocket_plan_create(const rocket_minirocket_params *m, u
 /* Static, human-readable name of a status code ("unknown status" otherwise). */
 const char *rocket_status_string(rocket_status s);
 
+/*
+ * Checked builds, for debugging (a second library, librocket_checked.so,
+ * compiled with ROCKET_CHECKED=1; the Python binding loads it when the
+ * environment sets ROCKET_DEBUG=1).  Every entry point works as documented
+ * above; in addition the device code checks every LDS tile read against the
+ * bytes its workgroup staged and every feature store against the rows and
+ * columns of its launch.  A failed check sets a flag and the access is
+ * redirected inside its buffer (the features are then wrong, but no memory
+ * outside the buffers is touched).
+ *   rocket_checked_build  1 in a checked build, 0 in the product library.
+ *   rocket_check_flags    waits for the current device, stores the checks
+ *                         that failed there since the last call in *flags
+ *                         (bit 0: an LDS read, bit 1: a feature store;
+ *                         0 = none) and clears them.  The product library
+ *                         stores 0 and touches no device.
+ *                         Errors: ROCKET_ERR_INVALID_ARG (flags NULL);
+ *                         ROCKET_ERR_HIP.
+ */
+int32_t rocket_checked_build(void);
+rocket_status rocket_check_flags(uint32_t *flags);
+
 #ifdef __cplusplus
 }
 #endif

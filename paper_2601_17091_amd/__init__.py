@@ -7,7 +7,9 @@ Python-side entry points (argument marshalling over ctypes):
     minirocket_fit(X_train, num_features, seed) -> MINIROCKET parameters
     MiniRocketPlan(params)  .transform(X): PPV features [n, n_features]
 The seeded synthetic series live in ``paper_2601_17091_amd.workloads``.
+With ROCKET_DEBUG=1 in the environment the checked build is loaded
+(librocket_checked.so: device-side bounds checks, see check_flags).
 """
-from .rocket import (EXPORTED, MiniRocketPlan, Plan, RocketError, generate_kernels,  # noqa: F401
-                     generate_kernels_multi, library, minirocket_fit, plan_tables, status_string,
-                     transform, transform_batched)
+from .rocket import (EXPORTED, MiniRocketPlan, Plan, RocketError, check_flags, checked_build,  # noqa: F401
+                     generate_kernels, generate_kernels_multi, library, library_at, minirocket_fit,
+                     plan_tables, status_string, transform, transform_batched)

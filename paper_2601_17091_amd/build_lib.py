@@ -2,7 +2,8 @@
 
     python -m paper_2601_17091_amd.build_lib
 
-produces ``paper_2601_17091_amd/librocket.so`` from ``csrc/``.  hipcc
+produces ``paper_2601_17091_amd/librocket.so`` from ``csrc/`` (and the
+checked build ``librocket_checked.so``, for debugging).  hipcc
 cross-compiles the device code, so this runs on a machine without a GPU.
 """
 from __future__ import annotations
@@ -16,6 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "librocket.so")
+CHECKED_LIB = os.path.join(HERE, "librocket_checked.so")
 SOURCES = ["transform.hip", "plan.cpp", "generate.cpp", "minirocket.cpp"]
 ARCH = "gfx950"
 
@@ -52,22 +54,43 @@ def compile_flags() -> list[str]:
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link librocket.so (always rebuilds)."""
+    """Compile every source and link librocket.so, and the checked build
+    librocket_checked.so (transform.hip with ROCKET_CHECKED=1: device-side
+    bounds checks for debugging); always rebuilds.  The compilations run in
+    parallel."""
     os.makedirs(os.path.join(HERE, "_build"), exist_ok=True)
-    objs = []
-    for src in SOURCES:
-        obj = os.path.join(HERE, "_build", src + ".o")
-        cmd = [hipcc()] + compile_flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
+    jobs = []   # (command, object)
+    objs = {False: [], True: []}
+    for checked in (False, True):
+        for src in SOURCES:
+            if checked and src != "transform.hip":
+                objs[True].append(os.path.join(HERE, "_build", src + ".o"))
+                continue
+            obj = os.path.join(HERE, "_build", src + (".checked.o" if checked else ".o"))
+            cmd = [hipcc()] + compile_flags() + (["-DROCKET_CHECKED=1"] if checked else []) + \
+                ["-c", os.path.join(CSRC, src), "-o", obj]
+            jobs.append(cmd)
+            objs[checked].append(obj)
+    procs = []
+    for cmd in jobs:
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True, stderr=subprocess.PIPE if not verbose else None)
-        objs.append(obj)
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+        procs.append((cmd, subprocess.Popen(cmd, stderr=None if verbose else subprocess.PIPE)))
+    failed = []
+    for cmd, pr in procs:
+        _, err = pr.communicate()
+        if pr.returncode != 0:
+            failed.append((cmd, err))
+    if failed:
+        cmd, err = failed[0]
+        raise RuntimeError("compilation failed: %s\n%s" % (" ".join(cmd), (err or b"").decode(errors="replace")))
+    for checked, lib in ((False, LIB), (True, CHECKED_LIB)):
+        tmp = lib + ".tmp%d" % os.getpid()
+        cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs[checked]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, lib)
     return LIB
 
 

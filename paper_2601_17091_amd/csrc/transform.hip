@@ -45,6 +45,82 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
 constexpr uint64_t kNegInfPair = 0xff800000ff800000ull;  // two fp32 -inf
 
+// ---------------------------------------------------------------------------
+// Checked build (compiled with ROCKET_CHECKED=1 into librocket_checked.so):
+// every LDS tile read is checked against the bytes its workgroup staged and
+// every feature store against the rows and columns of its launch.  A failed
+// check sets a bit of g_rocket_checks (read and cleared by
+// rocket_check_flags) and the access is redirected inside the buffer, so a
+// wrong index never reads or writes outside it.  The product build compiles
+// none of this.
+// ---------------------------------------------------------------------------
+#ifndef ROCKET_CHECKED
+#define ROCKET_CHECKED 0
+#endif
+constexpr uint32_t kCheckLdsRead = 1u;  // an LDS tile read outside the staged bytes
+constexpr uint32_t kCheckStore = 2u;    // a feature store outside its rows / columns
+#if ROCKET_CHECKED
+__device__ unsigned int g_rocket_checks;
+__shared__ uint32_t g_check_lds_lo, g_check_lds_hi;  // staged LDS bytes [lo, hi) of the workgroup
+__shared__ float *g_check_out_lo;                     // the launch's output floats [lo, hi)
+__shared__ float *g_check_out_hi;
+__device__ __forceinline__ void check_failed(uint32_t bit) {
+    if ((threadIdx.x & 63) == 0) atomicOr(&g_rocket_checks, bit);
+}
+#endif
+
+// The LDS byte address m of a read of `bytes` bytes (wave-uniform), checked
+// in checked builds; a read outside the staged bytes goes to their start.
+__device__ __forceinline__ uint32_t lds_checked(uint32_t m, uint32_t bytes) {
+#if ROCKET_CHECKED
+    // the bounds come from LDS into vector registers; the result goes to a
+    // scalar operand (M0), so it is made wave-uniform explicitly (it is
+    // uniform: m and the bounds are)
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(g_check_lds_lo);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(g_check_lds_hi);
+    uint32_t r = m;
+    if (m < lo || m + bytes > hi) {
+        check_failed(kCheckLdsRead);
+        r = lo;
+    }
+    return __builtin_amdgcn_readfirstlane(r);
+#endif
+    (void)bytes;
+    return m;
+}
+
+// Whether the n floats at f lie in the launch's output (always true in the
+// product build).
+__device__ __forceinline__ bool store_checked(const float *f, int n) {
+#if ROCKET_CHECKED
+    if (f < g_check_out_lo || f + n > g_check_out_hi) {
+        check_failed(kCheckStore);
+        return false;
+    }
+#endif
+    (void)f;
+    (void)n;
+    return true;
+}
+
+// Record a workgroup's staged LDS bytes and its launch's output range
+// (checked builds; thread 0, before the workgroup's barrier).
+__device__ __forceinline__ void set_check_bounds(const float *smem, int64_t staged_floats, float *out_lo,
+                                                 float *out_hi) {
+#if ROCKET_CHECKED
+    if (threadIdx.x == 0) {
+        g_check_lds_lo = (uint32_t)(__UINTPTR_TYPE__)(__attribute__((address_space(3))) const float *)smem;
+        g_check_lds_hi = g_check_lds_lo + 4u * (uint32_t)staged_floats;
+        g_check_out_lo = out_lo;
+        g_check_out_hi = out_hi;
+    }
+#endif
+    (void)smem;
+    (void)staged_floats;
+    (void)out_lo;
+    (void)out_hi;
+}
+
 // Read-only tables indexed by wavefront-uniform values are read through the
 // constant address space, which lets the compiler use scalar loads.
 template <typename T>
@@ -69,9 +145,9 @@ __device__ __forceinline__ uint32_t lds_addr(const float *p) {
 // compiled code in these kernels.  The reads complete before the asm block
 // ends (lgkmcnt(0)), so the outputs are ready when the compiler sees them.
 template <int NT>
-__device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]);
+__device__ __forceinline__ void lds_tiles_raw(uint32_t m, float (&xv)[NT]);
 template <>
-__device__ __forceinline__ void lds_tiles<1>(uint32_t m, float (&xv)[1]) {
+__device__ __forceinline__ void lds_tiles_raw<1>(uint32_t m, float (&xv)[1]) {
     asm volatile(
         "s_mov_b32 m0, %1\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\t"
@@ -81,7 +157,7 @@ __device__ __forceinline__ void lds_tiles<1>(uint32_t m, float (&xv)[1]) {
         : "memory");
 }
 template <>
-__device__ __forceinline__ void lds_tiles<2>(uint32_t m, float (&xv)[2]) {
+__device__ __forceinline__ void lds_tiles_raw<2>(uint32_t m, float (&xv)[2]) {
     asm volatile(
         "s_mov_b32 m0, %2\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
@@ -91,7 +167,7 @@ __device__ __forceinline__ void lds_tiles<2>(uint32_t m, float (&xv)[2]) {
         : "memory");
 }
 template <>
-__device__ __forceinline__ void lds_tiles<3>(uint32_t m, float (&xv)[3]) {
+__device__ __forceinline__ void lds_tiles_raw<3>(uint32_t m, float (&xv)[3]) {
     asm volatile(
         "s_mov_b32 m0, %3\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
@@ -102,7 +178,7 @@ __device__ __forceinline__ void lds_tiles<3>(uint32_t m, float (&xv)[3]) {
         : "memory");
 }
 template <>
-__device__ __forceinline__ void lds_tiles<4>(uint32_t m, float (&xv)[4]) {
+__device__ __forceinline__ void lds_tiles_raw<4>(uint32_t m, float (&xv)[4]) {
     asm volatile(
         "s_mov_b32 m0, %4\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
@@ -121,7 +197,7 @@ template <int NT>
 __device__ __forceinline__ void lds_tiles_rest(float (&xv)[NT]);
 
 template <>
-__device__ __forceinline__ void lds_tiles<5>(uint32_t m, float (&xv)[5]) {
+__device__ __forceinline__ void lds_tiles_raw<5>(uint32_t m, float (&xv)[5]) {
     asm volatile(
         "s_mov_b32 m0, %5\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\t"
@@ -140,7 +216,7 @@ __device__ __forceinline__ void lds_tiles_rest<5>(float (&xv)[5]) {
 }
 
 template <>
-__device__ __forceinline__ void lds_tiles<6>(uint32_t m, float (&xv)[6]) {
+__device__ __forceinline__ void lds_tiles_raw<6>(uint32_t m, float (&xv)[6]) {
     asm volatile(
         "s_mov_b32 m0, %6\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\t"
@@ -160,7 +236,7 @@ __device__ __forceinline__ void lds_tiles_rest<6>(float (&xv)[6]) {
 }
 
 template <>
-__device__ __forceinline__ void lds_tiles<7>(uint32_t m, float (&xv)[7]) {
+__device__ __forceinline__ void lds_tiles_raw<7>(uint32_t m, float (&xv)[7]) {
     asm volatile(
         "s_mov_b32 m0, %7\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\t"
@@ -181,7 +257,7 @@ __device__ __forceinline__ void lds_tiles_rest<7>(float (&xv)[7]) {
 }
 
 template <>
-__device__ __forceinline__ void lds_tiles<8>(uint32_t m, float (&xv)[8]) {
+__device__ __forceinline__ void lds_tiles_raw<8>(uint32_t m, float (&xv)[8]) {
     asm volatile(
         "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\t"
@@ -202,15 +278,21 @@ __device__ __forceinline__ void lds_tiles_rest<8>(float (&xv)[8]) {
     asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(xv[4]), "+v"(xv[5]), "+v"(xv[6]), "+v"(xv[7]) : : "memory");
 }
 
+// The reads of lds_tiles_raw, with the address checked in checked builds.
+template <int NT>
+__device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]) {
+    lds_tiles_raw<NT>(lds_checked(m, 256u * NT), xv);
+}
+
 // NC tiles (256 bytes apart) at each of P bases sb bytes apart, the first at
 // m: P runs of reads under one M0 each, M0 advanced by sb between runs (one
 // wait state after every M0 write).  Tiles are numbered base-major.  As for
 // lds_tiles, at most NC * P - 4 reads are left in flight on return when
 // NC * P > 4 (lds_tiles_rest then waits for the rest).
 template <int NC, int P>
-__device__ __forceinline__ void lds_multi(uint32_t m, uint32_t sb, float (&xv)[NC * P]);
+__device__ __forceinline__ void lds_multi_raw(uint32_t m, uint32_t sb, float (&xv)[NC * P]);
 template <>
-__device__ __forceinline__ void lds_multi<1, 4>(uint32_t m, uint32_t sb, float (&xv)[4]) {
+__device__ __forceinline__ void lds_multi_raw<1, 4>(uint32_t m, uint32_t sb, float (&xv)[4]) {
     asm volatile(
         "s_mov_b32 m0, %4\n\ts_nop 0\n\tds_read_addtid_b32 %0\n\t"
         "s_add_u32 m0, m0, %5\n\ts_nop 0\n\tds_read_addtid_b32 %1\n\t"
@@ -222,7 +304,7 @@ __device__ __forceinline__ void lds_multi<1, 4>(uint32_t m, uint32_t sb, float (
         : "memory", "scc");
 }
 template <>
-__device__ __forceinline__ void lds_multi<2, 4>(uint32_t m, uint32_t sb, float (&xv)[8]) {
+__device__ __forceinline__ void lds_multi_raw<2, 4>(uint32_t m, uint32_t sb, float (&xv)[8]) {
     asm volatile(
         "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
@@ -238,7 +320,7 @@ __device__ __forceinline__ void lds_multi<2, 4>(uint32_t m, uint32_t sb, float (
         : "memory", "scc");
 }
 template <>
-__device__ __forceinline__ void lds_multi<3, 2>(uint32_t m, uint32_t sb, float (&xv)[6]) {
+__device__ __forceinline__ void lds_multi_raw<3, 2>(uint32_t m, uint32_t sb, float (&xv)[6]) {
     asm volatile(
         "s_mov_b32 m0, %6\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\tds_read_addtid_b32 %2 offset:512\n\t"
@@ -250,7 +332,7 @@ __device__ __forceinline__ void lds_multi<3, 2>(uint32_t m, uint32_t sb, float (
         : "memory", "scc");
 }
 template <>
-__device__ __forceinline__ void lds_multi<4, 2>(uint32_t m, uint32_t sb, float (&xv)[8]) {
+__device__ __forceinline__ void lds_multi_raw<4, 2>(uint32_t m, uint32_t sb, float (&xv)[8]) {
     asm volatile(
         "s_mov_b32 m0, %8\n\ts_nop 0\n\t"
         "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
@@ -303,6 +385,7 @@ struct FusedArgs {
                              // row_stride multiples of 4 floats, X 16-byte aligned)
     float *S;                // series-lane layout: features in slot order (see below)
     int64_t s_rows;          // rows one slot column of S holds
+    int64_t s_floats;        // floats of S this launch may write (bounds of checked builds)
 };
 
 // DPP controls (GFX9 encoding)
@@ -363,6 +446,24 @@ struct RightClampedTiles {
     int L;
     __device__ __forceinline__ uint32_t m0(int j) const { return row + 4u * (uint32_t)min(b0 + j * d, L); }
 };
+
+// The reads of lds_multi_raw, every run's address checked in checked
+// builds (a failed run sends every run to the start of the staged bytes).
+template <int NC, int P>
+__device__ __forceinline__ void lds_multi(uint32_t m, uint32_t sb, float (&xv)[NC * P]) {
+#if ROCKET_CHECKED
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < P; ++k) ok = ok && lds_checked(m + (uint32_t)k * sb, 256u * NC) == m + (uint32_t)k * sb;
+    if (!ok) {
+        m = g_check_lds_lo;
+        sb = 0;
+    }
+    m = __builtin_amdgcn_readfirstlane(m);
+    sb = __builtin_amdgcn_readfirstlane(sb);
+#endif
+    lds_multi_raw<NC, P>(m, sb, xv);
+}
 
 // The padded layout for P runs of NC tiles each, run k sb bytes after run 0
 // (P super-tiles of a Toeplitz item whose super-tiles hold NC chunks): tile
@@ -705,6 +806,7 @@ __device__ __forceinline__ void write_features(uint32_t c, float m, float psum, 
     // while c * fl64(1/O) is within 2^-52 of it, so rounding the double
     // product to float gives the same float as the fp32 division
     const float ppv = (float)((double)c * inv_O);
+    if (!store_checked(Frow + (MPV ? 3 : 2) * (int64_t)ok, MPV ? 3 : 2)) return;
     if (MPV) {
         // rows of 3 floats: 4-byte aligned only
         float *f = Frow + 3 * (int64_t)ok;
@@ -1256,6 +1358,8 @@ __device__ __forceinline__ bool stage_group(const FusedArgs &a, float *smem, int
     // zeros after the last row: lanes past the last output of an item read
     // up to tail_pad floats past it
     for (int e = threadIdx.x; e < a.tail_pad; e += BLOCK) smem[w.nrows * a.C * a.row_stride + e] = 0.0f;
+    set_check_bounds(smem, (int64_t)w.nrows * a.C * a.row_stride + a.tail_pad,
+                     a.F + a.row0 * (int64_t)a.nf * a.K, a.F + (a.row0 + a.n_rows) * (int64_t)a.nf * a.K);
     if (threadIdx.x == 0) *next_item = 0;
     __syncthreads();
     return true;
@@ -1357,6 +1461,7 @@ __device__ __forceinline__ bool stage_series(const FusedArgs &a, float *smem, in
         const int m = e / kSeriesLanes - kSeriesMargin;
         smem[e] = (r < w.nrows && m >= 0 && m < a.L) ? x[(int64_t)r * a.L + m] : 0.0f;
     }
+    set_check_bounds(smem, total, a.S, a.S + a.s_floats);
     if (threadIdx.x == 0) *next_item = 0;
     __syncthreads();
     return true;
@@ -1775,7 +1880,8 @@ __device__ __forceinline__ void run_mr_item(const ItemDesc &it, const float *row
         // PPV = count / O, correctly rounded as in write_features
 #pragma unroll
         for (int rr = 0; rr < R; ++rr) {
-            if (fidx[rr] >= 0) F0[r * f_stride + fidx[rr]] = (float)((double)cnt[rr] * it.inv_O);
+            if (fidx[rr] >= 0 && store_checked(F0 + r * f_stride + fidx[rr], 1))
+                F0[r * f_stride + fidx[rr]] = (float)((double)cnt[rr] * it.inv_O);
             cnt[rr] = 0;
         }
     }
@@ -2242,6 +2348,25 @@ extern "C" void rocket_plan_destroy(rocket_plan *p) {
     delete p;
 }
 
+extern "C" int32_t rocket_checked_build(void) { return ROCKET_CHECKED ? 1 : 0; }
+
+extern "C" rocket_status rocket_check_flags(uint32_t *flags) {
+    if (!flags) return ROCKET_ERR_INVALID_ARG;
+    *flags = 0;
+#if ROCKET_CHECKED
+    // the variable's own symbol, not its host-side name: the runtime resolves
+    // the current device's copy
+    if (hipDeviceSynchronize() != hipSuccess) return ROCKET_ERR_HIP;
+    unsigned int v = 0;
+    const unsigned int zero = 0;
+    if (hipMemcpyFromSymbol(&v, HIP_SYMBOL(g_rocket_checks), sizeof(v)) != hipSuccess ||
+        hipMemcpyToSymbol(HIP_SYMBOL(g_rocket_checks), &zero, sizeof(zero)) != hipSuccess)
+        return ROCKET_ERR_HIP;
+    *flags = v;
+#endif
+    return ROCKET_OK;
+}
+
 extern "C" rocket_status rocket_plan_info(const rocket_plan *p, rocket_plan_facts *out) {
     if (!p || !out) return ROCKET_ERR_INVALID_ARG;
     out->n_items = (int64_t)p->host.items.size();
@@ -2361,6 +2486,7 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
                  : 0;
     a.S = S;
     a.s_rows = s_rows;
+    a.s_floats = series ? (int64_t)p->host.kid.size() * s_rows * a.nf : 0;
     const size_t lds = (size_t)(series ? p->series_lds : p->lds_bytes);
     const bool big = big_group;
     const int sel = (big ? 1 : 0) | (p->clamp ? 2 : 0) | (p->mpv ? 4 : 0) | (p->C > 1 ? 8 : 0);

@@ -7,13 +7,18 @@ is missing, calls raise instead of computing anything elsewhere.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "librocket.so")
+PRODUCT_LIB_PATH = os.path.join(HERE, "librocket.so")
+# the checked build (device-side bounds checks, for debugging): used when the
+# environment sets ROCKET_DEBUG=1
+CHECKED_LIB_PATH = os.path.join(HERE, "librocket_checked.so")
+LIB_PATH = CHECKED_LIB_PATH if os.environ.get("ROCKET_DEBUG") == "1" else PRODUCT_LIB_PATH
 
 ROCKET_OK = 0
 ROCKET_ERR_INVALID_ARG = -1
@@ -49,6 +54,8 @@ EXPORTED = (
     "rocket_minirocket_fit",
     "rocket_minirocket_free",
     "rocket_minirocket_plan_create",
+    "rocket_checked_build",
+    "rocket_check_flags",
 )
 
 
@@ -136,6 +143,8 @@ def _signatures() -> dict:
         "rocket_plan_tables_build": ([kp, i32, ctypes.POINTER(CPlanTables)], st),
         "rocket_plan_tables_free": ([ctypes.POINTER(CPlanTables)], None),
         "rocket_status_string": ([ctypes.c_int], ctypes.c_char_p),
+        "rocket_checked_build": ([], ctypes.c_int32),
+        "rocket_check_flags": ([ctypes.POINTER(ctypes.c_uint32)], ctypes.c_int),
         "rocket_minirocket_fit": ([vp, i64, i32, i32, ctypes.c_uint64, mp], st),
         "rocket_minirocket_free": ([mp], None),
         "rocket_minirocket_plan_create": ([mp, ctypes.c_uint32, ctypes.POINTER(vp)], st),
@@ -175,6 +184,35 @@ def library() -> ctypes.CDLL:
         raise RuntimeError("librocket.so is not built (run paper_2601_17091_amd.build_lib.build())")
     _lib = bind(ctypes.CDLL(LIB_PATH))
     return _lib
+
+
+@contextlib.contextmanager
+def library_at(path: str):
+    """Route the binding's calls to the library at `path` inside the block
+    (for example the checked build, CHECKED_LIB_PATH).  A plan keeps the
+    library that made it, so a plan made inside stays valid after the block."""
+    global _lib
+    if not os.path.exists(path):
+        raise RuntimeError("%s is not built (run paper_2601_17091_amd.build_lib.build())" % path)
+    prev = _lib
+    _lib = bind(ctypes.CDLL(path))
+    try:
+        yield _lib
+    finally:
+        _lib = prev
+
+
+def checked_build() -> bool:
+    """Whether the loaded library is the checked build."""
+    return bool(library().rocket_checked_build())
+
+
+def check_flags() -> int:
+    """The device-side checks that failed since the last call (checked
+    builds; waits for the device): bit 0 an LDS read, bit 1 a feature store."""
+    v = ctypes.c_uint32(0)
+    _check(library().rocket_check_flags(ctypes.byref(v)), "rocket_check_flags")
+    return int(v.value)
 
 
 def status_string(status: int) -> str:
@@ -329,6 +367,7 @@ class Plan:
     def __init__(self, kernels: dict, L: int, direct: bool = False, clamped: bool = False,
                  mpv: bool = False, tiled: bool = False, series: bool = False):
         lib = library()
+        self._lib = lib  # every call on this plan goes to the library that made it
         self._c, self._keep = as_c_kernels(kernels)
         self.n_kernels = int(self._c.n_kernels)
         self.L = int(L)
@@ -344,7 +383,7 @@ class Plan:
 
     def info(self) -> dict:
         f = CPlanFacts()
-        _check(library().rocket_plan_info(self._h, ctypes.byref(f)), "rocket_plan_info")
+        _check(self._lib.rocket_plan_info(self._h, ctypes.byref(f)), "rocket_plan_info")
         return dict(n_items=f.n_items, n_buckets=f.n_buckets, mfma_per_row=f.mfma_per_row,
                     lds_bytes=f.lds_bytes, direct=bool(f.direct), clamped=bool(f.clamped),
                     features_per_kernel=f.features_per_kernel, rows_per_block=f.rows_per_block,
@@ -362,7 +401,7 @@ class Plan:
         """F[n, fK] <- features of X[n, L] (f = 2, or 3 with MPV);
         asynchronous on `stream`."""
         self._check_io(X, F)
-        _check(library().rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
+        _check(self._lib.rocket_transform_plan(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
                                                ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
                "rocket_transform_plan")
         return F
@@ -387,7 +426,7 @@ class Plan:
         allocation in the library (the series-lane layout uses its static
         scratch); the caller allocates F."""
         self._check_io(X, F)
-        _check(library().rocket_transform_plan_noalloc(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
+        _check(self._lib.rocket_transform_plan_noalloc(self._h, ctypes.c_void_p(X.data_ptr()), X.shape[0],
                                                        ctypes.c_void_p(F.data_ptr()), _stream_handle(stream)),
                "rocket_transform_plan_noalloc")
         return F
@@ -409,7 +448,7 @@ class Plan:
             raise ValueError("F_host must be a contiguous float32 [%d, %d] array" % (n, self.n_features))
         if stream is None:
             stream = torch.cuda.current_stream()
-        _check(library().rocket_transform_host(self._h, ctypes.c_void_p(X_t.data_ptr()), n,
+        _check(self._lib.rocket_transform_host(self._h, ctypes.c_void_p(X_t.data_ptr()), n,
                                                ctypes.c_void_p(F_t.data_ptr()), int(batch_rows),
                                                ctypes.c_void_p(stream.cuda_stream)),
                "rocket_transform_host")
@@ -417,7 +456,7 @@ class Plan:
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:
-            library().rocket_plan_destroy(self._h)
+            self._lib.rocket_plan_destroy(self._h)
             self._h = ctypes.c_void_p()
 
     def __del__(self):
@@ -465,6 +504,7 @@ class MiniRocketPlan(Plan):
 
     def __init__(self, params: dict, clamped: bool = False):
         lib = library()
+        self._lib = lib
         self._c, self._keep = as_c_minirocket(params)
         self.L = int(params["input_length"])
         h = ctypes.c_void_p()

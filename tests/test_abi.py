@@ -43,6 +43,30 @@ def test_library_exports_every_declared_symbol(lib):
         assert getattr(lib, name) is not None
 
 
+def test_product_build_is_unchecked(lib):
+    v = ctypes.c_uint32(7)
+    assert lib.rocket_checked_build() == 0
+    assert lib.rocket_check_flags(ctypes.byref(v)) == rb.ROCKET_OK
+    assert v.value == 0
+    assert lib.rocket_check_flags(None) == rb.ROCKET_ERR_INVALID_ARG
+
+
+def test_checked_build_exports_the_same_symbols(lib):
+    if not os.path.exists(rb.CHECKED_LIB_PATH):
+        from paper_2601_17091_amd import build_lib
+        build_lib.build()
+    out = subprocess.run(["nm", "-D", "--defined-only", rb.CHECKED_LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    for name in declared_functions():
+        assert name in exported, name
+    with rb.library_at(rb.CHECKED_LIB_PATH) as clib:
+        assert clib.rocket_checked_build() == 1
+        assert clib.rocket_check_flags(None) == rb.ROCKET_ERR_INVALID_ARG
+        assert rk.checked_build()
+    assert not rk.checked_build()
+
+
 def test_status_strings(lib):
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert rk.status_string(code) not in ("", "unknown status")

@@ -28,7 +28,8 @@ HOST_TESTS = ["tests/test_plan_host.py", "tests/test_oracle_examples.py", "tests
 # tests of test_abi.py that load the full HIP library (exports, plan and
 # transform entry points) stay with the regular build
 NEEDS_FULL_LIBRARY = ["test_header_declares", "test_library_exports", "test_plan_validation",
-                      "test_transform_validation", "test_minirocket_plan_rejects"]
+                      "test_transform_validation", "test_minirocket_plan_rejects",
+                      "test_product_build_is_unchecked", "test_checked_build_exports"]
 SAN_FLAGS = ["-O1", "-g", "-fPIC", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
              "-fno-sanitize-recover=undefined"]
 
