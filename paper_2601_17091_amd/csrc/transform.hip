@@ -57,8 +57,8 @@ constexpr uint64_t kNegInfPair = 0xff800000ff800000ull;  // two fp32 -inf
 #ifndef ROCKET_CHECKED
 #define ROCKET_CHECKED 0
 #endif
-constexpr uint32_t kCheckLdsRead = 1u;  // an LDS tile read outside the staged bytes
-constexpr uint32_t kCheckStore = 2u;    // a feature store outside its rows / columns
+[[maybe_unused]] constexpr uint32_t kCheckLdsRead = 1u;  // an LDS tile read outside the staged bytes
+[[maybe_unused]] constexpr uint32_t kCheckStore = 2u;    // a feature store outside its rows / columns
 #if ROCKET_CHECKED
 __device__ unsigned int g_rocket_checks;
 __shared__ uint32_t g_check_lds_lo, g_check_lds_hi;  // staged LDS bytes [lo, hi) of the workgroup
