@@ -2051,6 +2051,8 @@ static const void *series_fn(bool mpv) {
 
 struct rocket_plan {
     rocket::HostPlan host;
+    // code variants in launch order: by total item cost, largest first
+    int32_t variant_order[rocket::kNumVariants] = {};
     int device = 0;
     int n_cu = 0;
     bool direct = false;
@@ -2194,6 +2196,17 @@ static hipError_t allow_lds(int device, int64_t lds) {
 
 // Upload the work tables and allow the kernels the workgroup's LDS.
 static hipError_t upload_tables(rocket_plan *p, int64_t lds) {
+    // A launch runs the workgroups of one variant after another (per XCD),
+    // and a variant's workgroups each hold 1/nsplit of its items, so the
+    // variants with the most work per workgroup go first: the launch then
+    // ends on the short workgroups of the light variants rather than on a
+    // late start of the longest ones.
+    const int nv = p->host.n_variants;
+    int64_t cost[rocket::kNumVariants] = {};
+    for (const ItemDesc &it : p->host.items) cost[it.variant] += it.cost;
+    for (int v = 0; v < nv; ++v) p->variant_order[v] = v;
+    std::stable_sort(p->variant_order, p->variant_order + nv,
+                     [&](int32_t x, int32_t y) { return cost[x] > cost[y]; });
     hipError_t e = upload(p->host.items, &p->d_items);
     if (e == hipSuccess) e = upload(p->host.wpk, &p->d_wpk);
     if (e == hipSuccess) e = upload(p->host.bias, &p->d_bias);
@@ -2472,7 +2485,15 @@ static rocket_status launch_groups(const rocket_plan *p, bool series, const floa
     a.split_begin = p->d_split_begin + p->host.layout_off[li];
     a.nsplit = nsplit;
     a.n_variants = 0;
-    for (int v = 0; v < n_var; ++v) {
+    // The cost order (variant_order) pays where a launch is a few rounds
+    // of workgroups per CU, so that its end is a visible share of it (1,000
+    // series: 2.5-3.5 % faster).  Launches of many rounds keep the index
+    // order, which measured 0.2 % faster on 100,000 series; series-lane
+    // chunks keep it too (their launches overlap the next chunk's on a
+    // second stream, and the cost order measured 1.6 % slower there).
+    const bool cost_order = !series && groups * nsplit * n_present < 128 * (int64_t)std::max(p->n_cu, 1);
+    for (int i = 0; i < n_var; ++i) {
+        const int v = cost_order ? p->variant_order[i] : i;
         const int32_t *sb = p->host.split_begin.data() + p->host.layout_off[li];
         if (sb[(v + 1) * nsplit] > sb[v * nsplit]) a.variants[a.n_variants++] = v;
     }
