@@ -31,6 +31,7 @@ CLAMP_MARGIN = 512
 N_VARIANTS = 18      # 0..5 MFMA items, 6..11 VALU items, 12..17 Toeplitz items
 TOEP0 = 12
 SERIES_MAX_L = 128   # VALU items only for longer series
+SERIES_MARGIN = 8    # series-lane layout: zero positions staged on each side of a series
 
 
 def variant_info(v):
@@ -527,3 +528,39 @@ def test_toeplitz_hand_built_dilations(oracle):
     assert ((v >= 12) & (v % 2 == 0)).sum() >= 2 and ((v >= 12) & (v % 2 == 1)).sum() >= 2
     X = rng.standard_normal((4, L)).astype(np.float32)
     check_tables(ks, L, X, oracle)
+
+
+def series_block_reads(b0j, n, L):
+    """Positions read by a series-lane block of n positions under a tap whose
+    first position is b0j, [tap, position]: the start is clamped into
+    [-SERIES_MARGIN, L] (a block moved by the clamp lies wholly outside the
+    series and reads margin zeros)."""
+    b = np.clip(b0j, -SERIES_MARGIN, L)
+    return b[:, None] + np.arange(n)[None, :]
+
+
+@pytest.mark.parametrize("seed,K,L", [(21, 500, 11), (22, 800, 30), (23, 1000, 64), (24, 1000, 100),
+                                      (25, 1000, 128)] + [(30 + i, 600, 11 + 13 * i) for i in range(9)])
+def test_series_lane_reads_stay_staged(seed, K, L):
+    """The series-lane kernel walks an item's O positions in blocks of NT
+    (8 for 4-kernel items, 4 for 8-kernel items; the last block holds the
+    rest), and for tap j a block starting at output t0 reads positions
+    t0 - p + j*d onwards.  Every read stays inside the staged positions
+    [-SERIES_MARGIN, L + SERIES_MARGIN), reads the series position itself
+    where that lies inside the series, and a margin zero where not."""
+    t = rk.plan_tables(rk.generate_kernels(seed, K, L), L)
+    for row in t["items"]:
+        f = item_fields(row)
+        ell, G, nk = variant_info(f["variant"])
+        assert nk == 0 and f["variant"] < 6  # series this short have MFMA items only
+        NT = TILES_PER_BLOCK[G]
+        assert NT <= SERIES_MARGIN
+        for start in range(0, f["O"], NT):
+            n = min(NT, f["O"] - start)
+            b0j = start - f["p"] + np.arange(ell) * f["d"]
+            pos = series_block_reads(b0j, n, L)
+            assert pos.min() >= -SERIES_MARGIN and pos.max() < L + SERIES_MARGIN
+            true = b0j[:, None] + np.arange(n)[None, :]
+            inside = (true >= 0) & (true < L)
+            assert np.array_equal(pos[inside], true[inside])
+            assert np.all((pos[~inside] < 0) | (pos[~inside] >= L))
