@@ -284,6 +284,85 @@ __device__ __forceinline__ void lds_tiles(uint32_t m, float (&xv)[NT]) {
     lds_tiles_raw<NT>(lds_checked(m, 256u * NT), xv);
 }
 
+// The reads of lds_tiles_raw<NT> (NT <= 4) without the wait: the values
+// arrive in xv once lds_wait<NT, KEEP> has run after them.
+template <int NT>
+__device__ __forceinline__ void lds_issue_raw(uint32_t m, float (&xv)[NT]);
+template <>
+__device__ __forceinline__ void lds_issue_raw<1>(uint32_t m, float (&xv)[1]) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tds_read_addtid_b32 %0" : "=v"(xv[0]) : "s"(m) : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_issue_raw<2>(uint32_t m, float (&xv)[2]) {
+    asm volatile(
+        "s_mov_b32 m0, %2\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256"
+        : "=&v"(xv[0]), "=&v"(xv[1])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_issue_raw<3>(uint32_t m, float (&xv)[3]) {
+    asm volatile(
+        "s_mov_b32 m0, %3\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2])
+        : "s"(m)
+        : "memory");
+}
+template <>
+__device__ __forceinline__ void lds_issue_raw<4>(uint32_t m, float (&xv)[4]) {
+    asm volatile(
+        "s_mov_b32 m0, %4\n\ts_nop 0\n\t"
+        "ds_read_addtid_b32 %0\n\tds_read_addtid_b32 %1 offset:256\n\t"
+        "ds_read_addtid_b32 %2 offset:512\n\tds_read_addtid_b32 %3 offset:768"
+        : "=&v"(xv[0]), "=&v"(xv[1]), "=&v"(xv[2]), "=&v"(xv[3])
+        : "s"(m)
+        : "memory");
+}
+template <int NT>
+__device__ __forceinline__ void lds_issue(uint32_t m, float (&xv)[NT]) {
+    lds_issue_raw<NT>(lds_checked(m, 256u * NT), xv);
+}
+
+// Waits until at most KEEP LDS reads are in flight.  LDS reads complete in
+// order, so the reads issued before the last KEEP (xv among them) have
+// arrived; xv passes through the statement, so nothing reads it earlier.
+template <int KEEP, int NT>
+struct LdsWait;
+template <int KEEP>
+struct LdsWait<KEEP, 1> {
+    __device__ __forceinline__ static void run(float (&xv)[1]) {
+        asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(xv[0]) : "n"(KEEP) : "memory");
+    }
+};
+template <int KEEP>
+struct LdsWait<KEEP, 2> {
+    __device__ __forceinline__ static void run(float (&xv)[2]) {
+        asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(xv[0]), "+v"(xv[1]) : "n"(KEEP) : "memory");
+    }
+};
+template <int KEEP>
+struct LdsWait<KEEP, 3> {
+    __device__ __forceinline__ static void run(float (&xv)[3]) {
+        asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(xv[0]), "+v"(xv[1]), "+v"(xv[2]) : "n"(KEEP) : "memory");
+    }
+};
+template <int KEEP>
+struct LdsWait<KEEP, 4> {
+    __device__ __forceinline__ static void run(float (&xv)[4]) {
+        asm volatile("s_waitcnt lgkmcnt(%4)"
+                     : "+v"(xv[0]), "+v"(xv[1]), "+v"(xv[2]), "+v"(xv[3])
+                     : "n"(KEEP)
+                     : "memory");
+    }
+};
+template <int NT, int KEEP>
+__device__ __forceinline__ void lds_wait(float (&xv)[NT]) {
+    LdsWait<KEEP, NT>::run(xv);
+}
+
 // NC tiles (256 bytes apart) at each of P bases sb bytes apart, the first at
 // m: P runs of reads under one M0 each, M0 advanced by sb between runs (one
 // wait state after every M0 write).  Tiles are numbered base-major.  As for
@@ -494,6 +573,16 @@ template <int NT, typename Src>
 __device__ __forceinline__ void read_tiles(const Src &src, int j, float (&xv)[NT]) {
     lds_tiles<NT>(src.m0(j), xv);
 }
+
+// Sources whose next tap's reads tile_mfma issues before the current tap's
+// MFMAs (blocks of up to 4 tiles).  Only the series-lane reads: in the
+// fused kernel the second set of tile registers lowers the occupancy from 5
+// to 4 wavefronts per SIMD (100-thousand-series calls 2.2 % slower), while
+// the series-lane kernel keeps its register count (Many-short 0.4 % faster).
+template <typename Src>
+struct PipelinedReads {
+    static constexpr bool value = false;
+};
 template <int NT, int NC, int P>
 __device__ __forceinline__ void read_tiles(const MultiTiles<NC, P> &src, int j, float (&xv)[NT]) {
     static_assert(NT == NC * P, "one block reads all of its runs");
@@ -541,6 +630,30 @@ template <int ELL, int G, int NT, bool LAST, bool FIRST, typename Src>
 __device__ __forceinline__ void tile_mfma(const Src &src, const float (&wa)[G][ELL],
                                           const v4f (&binit)[G], const v4f (&blast)[G],
                                           v4f (&acc)[NT][G]) {
+    if constexpr (NT <= 4 && PipelinedReads<Src>::value) {
+        // tap j + 1's reads are in flight while tap j's MFMAs issue
+        float xv[2][NT];
+        lds_issue<NT>(src.m0(0), xv[0]);
+#pragma unroll
+        for (int j = 0; j < ELL; ++j) {
+            if (j + 1 < ELL) {
+                lds_issue<NT>(src.m0(j + 1), xv[(j + 1) & 1]);
+                lds_wait<NT, NT>(xv[j & 1]);
+            } else {
+                lds_wait<NT, 0>(xv[j & 1]);
+            }
+#pragma unroll
+            for (int u = 0; u < NT; ++u)
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    const v4f c = (FIRST && j == 0)
+                                      ? ((LAST && run_last(u, NT, TileRuns<Src>::nc)) ? blast[g] : binit[g])
+                                      : acc[u][g];
+                    acc[u][g] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[g][j], xv[j & 1][u], c, 0, 0, 0);
+                }
+        }
+        return;
+    }
 #pragma unroll
     for (int j = 0; j < ELL; ++j) {
         float xv[NT];
@@ -1481,6 +1594,11 @@ struct SeriesTiles {
         const int b = min(max(b0 + j * d, -kSeriesMargin), L);
         return pos0 + 256u * (uint32_t)b;
     }
+};
+
+template <>
+struct PipelinedReads<SeriesTiles> {
+    static constexpr bool value = true;
 };
 
 // Per-lane (per-series) accumulators of one work item.
