@@ -508,15 +508,17 @@ const char *rocket_status_string(rocket_status s);
  * compiled with ROCKET_CHECKED=1; the Python binding loads it when the
  * environment sets ROCKET_DEBUG=1).  Every entry point works as documented
  * above; in addition the device code checks every LDS tile read against the
- * bytes its workgroup staged and every feature store against the rows and
- * columns of its launch.  A failed check sets a flag and the access is
- * redirected inside its buffer (the features are then wrong, but no memory
- * outside the buffers is touched).
+ * bytes its workgroup staged, every feature store of the workgroup kernels
+ * against the rows and columns of its launch, and every slot column the
+ * series-lane permutation reads against the plan's slots.  A failed check
+ * sets a flag and the access is redirected inside its buffer or skipped (the
+ * features are then wrong, but no memory outside the buffers is touched).
  *   rocket_checked_build  1 in a checked build, 0 in the product library.
  *   rocket_check_flags    waits for the current device, stores the checks
  *                         that failed there since the last call in *flags
- *                         (bit 0: an LDS read, bit 1: a feature store;
- *                         0 = none) and clears them.  The product library
+ *                         (bit 0: an LDS read, bit 1: a feature store,
+ *                         bit 2: a slot column read; 0 = none) and clears
+ *                         them.  The product library
  *                         stores 0 and touches no device.
  *                         Errors: ROCKET_ERR_INVALID_ARG (flags NULL);
  *                         ROCKET_ERR_HIP.

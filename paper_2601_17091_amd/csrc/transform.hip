@@ -59,6 +59,7 @@ constexpr uint64_t kNegInfPair = 0xff800000ff800000ull;  // two fp32 -inf
 #endif
 [[maybe_unused]] constexpr uint32_t kCheckLdsRead = 1u;  // an LDS tile read outside the staged bytes
 [[maybe_unused]] constexpr uint32_t kCheckStore = 2u;    // a feature store outside its rows / columns
+[[maybe_unused]] constexpr uint32_t kCheckSlotRead = 4u; // a read of the slot-ordered buffer outside its columns
 #if ROCKET_CHECKED
 __device__ unsigned int g_rocket_checks;
 __shared__ uint32_t g_check_lds_lo, g_check_lds_hi;  // staged LDS bytes [lo, hi) of the workgroup
@@ -1793,7 +1794,8 @@ __global__ __launch_bounds__(kBlock) void rocket_series_kernel(FusedArgs a) {
 template <int NF>
 __global__ __launch_bounds__(kBlock) void rocket_slot_permute_kernel(const float *S, int64_t s_rows,
                                                                      const int32_t *slot_of, int32_t K,
-                                                                     int64_t n_rows, float *F) {
+                                                                     int64_t n_rows, float *F,
+                                                                     int32_t n_slots) {
     constexpr int kRows = 16;
     constexpr int kVec = kRows * NF / 4;  // float4 per lane
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1803,6 +1805,13 @@ __global__ __launch_bounds__(kBlock) void rocket_slot_permute_kernel(const float
         const int64_t k = (t % k_tiles) * 64 + lane;
         const int64_t r0 = (t / k_tiles) * 64 + wave * kRows;
         if (k >= K || r0 >= n_rows) continue;
+#if ROCKET_CHECKED
+        // the slot column this lane reads must be one of the buffer's n_slots
+        if (slot_of[k] < 0 || slot_of[k] >= n_slots) {
+            check_failed(kCheckSlotRead);
+            continue;
+        }
+#endif
         const float4 *src = reinterpret_cast<const float4 *>(S + ((int64_t)slot_of[k] * s_rows + r0) * NF);
         float v[kVec * 4];
 #pragma unroll
@@ -2764,7 +2773,8 @@ static rocket_status enqueue_series(const rocket_plan *p, const float *X, int64_
         int64_t s_rows = chunk;
         float *Fc = F + r0 * K * nf;
         int64_t mm = m;
-        void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&mm, &Fc};
+        int32_t n_slots = (int32_t)p->host.kid.size();
+        void *args[] = {(void *)&S, &s_rows, (void *)&slot_of, &K32, (void *)&mm, &Fc, &n_slots};
         if (hipLaunchKernel(pf, grid, dim3(kBlock), args, 0, p->aux) != hipSuccess ||
             hipGetLastError() != hipSuccess || hipEventRecord(p->half_free[h], p->aux) != hipSuccess) {
             st = ROCKET_ERR_HIP;

@@ -209,7 +209,8 @@ def checked_build() -> bool:
 
 def check_flags() -> int:
     """The device-side checks that failed since the last call (checked
-    builds; waits for the device): bit 0 an LDS read, bit 1 a feature store."""
+    builds; waits for the device): bit 0 an LDS read, bit 1 a feature store,
+    bit 2 a slot column read of the series-lane permutation."""
     v = ctypes.c_uint32(0)
     _check(library().rocket_check_flags(ctypes.byref(v)), "rocket_check_flags")
     return int(v.value)
