@@ -116,6 +116,36 @@ def test_series_lane_hand_built(env, oracle):
     assert_parity(Fs, oracle.transform(X, ks), "series hand-built")
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_series_lane_random_sets(env, oracle, seed):
+    """Generated kernel sets at random sizes (L from 11 to 128, K from 100 to
+    1,200, 1 to 300 series, MPV on or off): the series-lane layout's PPV and
+    MAX equal the tiled layout's, and every feature meets the oracle.  (MPV
+    sums the positive values in a different order in the two layouts: one
+    lane per series there, a wavefront tree here.)"""
+    rng = np.random.default_rng(7000 + seed)
+    L = int(rng.integers(11, 129))
+    K = int(rng.integers(100, 1201))
+    n = int(rng.integers(1, 301))
+    mpv = bool(rng.integers(0, 2))
+    torch, rk = env
+    ks = rk.generate_kernels(7100 + seed, K, L)
+    X = _series(n, L, 7200 + seed)
+    _log("random set seed=%d n=%d L=%d K=%d mpv=%s" % (seed, n, L, K, mpv))
+    Fs, info = _run(env, ks, X, series=True, mpv=mpv)
+    assert info["series_lane"]
+    Ft, info_t = _run(env, ks, X, tiled=True, mpv=mpv)
+    assert not info_t["series_lane"]
+    nf = 3 if mpv else 2
+    for f in (0, 1):
+        assert np.array_equal(Fs[:, f::nf], Ft[:, f::nf]), f
+    ref = oracle.transform(X, ks)
+    if mpv:
+        assert_mpv_parity(Fs, ref, "series random mpv L=%d K=%d" % (L, K))
+    else:
+        assert_parity(Fs, ref, "series random L=%d K=%d" % (L, K))
+
+
 @pytest.mark.parametrize("L", [24, 128])
 def test_series_lane_mpv(env, oracle, L):
     torch, rk = env
