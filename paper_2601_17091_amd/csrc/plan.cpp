@@ -29,8 +29,11 @@ static int popcount64(uint64_t m) { return __builtin_popcountll(m); }
 // most channels and adds, one at a time, the kernel that adds the fewest new
 // channels (ties: the one reading more channels, then list order); then
 // pairwise swaps between groups are applied while they shrink the sum of the
-// two unions.  Deterministic; the swap pass is skipped for lists above 1,024
-// kernels (its cost is quadratic in the group count).
+// two unions, and finally 100 random swaps per kernel are tried, each kept
+// when it does not grow the sum (moves across equal sums let the search
+// leave the plateaus where no single swap shrinks it).  Deterministic (a
+// fixed SplitMix64 sequence); the swap passes are skipped for lists above
+// 1,024 kernels (the first one's cost is quadratic in the group count).
 using KernelSlot = std::pair<int32_t, int32_t>;  // (kernel, first frame tap)
 template <typename MaskOf>
 static std::vector<std::vector<KernelSlot>> group_by_channels(std::vector<KernelSlot> ks,
@@ -92,6 +95,31 @@ static std::vector<std::vector<KernelSlot>> group_by_channels(std::vector<Kernel
                     }
             }
         if (!improved) break;
+    }
+    if (groups.size() < 2) return groups;
+    uint64_t state = 0x243F6A8885A308D3ull ^ (uint64_t)ks.size();
+    auto next = [&state]() {  // SplitMix64
+        uint64_t z = (state += 0x9E3779B97F4A7C15ull);
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        return z ^ (z >> 31);
+    };
+    std::vector<int> cost(groups.size());
+    for (size_t g = 0; g < groups.size(); ++g) cost[g] = uni(groups[g]);
+    const size_t tries = 100 * ks.size();
+    for (size_t t = 0; t < tries; ++t) {
+        const size_t a = next() % groups.size();
+        size_t b = next() % (groups.size() - 1);
+        if (b >= a) ++b;
+        const size_t ia = next() % groups[a].size(), ib = next() % groups[b].size();
+        std::swap(groups[a][ia], groups[b][ib]);
+        const int ca = uni(groups[a]), cb = uni(groups[b]);
+        if (ca + cb <= cost[a] + cost[b]) {
+            cost[a] = ca;
+            cost[b] = cb;
+        } else {
+            std::swap(groups[a][ia], groups[b][ib]);
+        }
     }
     return groups;
 }
