@@ -487,7 +487,16 @@ def test_multichannel_issued_work():
     assert (items[:, 0] % 2 == 0).all()
     valid = (ks["channel_count"].astype(np.int64) * ks["length"] *
              (w.L + 2 * ks["padding"] - (ks["length"] - 1) * ks["dilation"])).sum()
-    assert items[:, 7].sum() * 256 < 1.5 * valid
+    assert items[:, 7].sum() * 256 < 1.42 * valid
+
+
+def test_multichannel_grouping_is_deterministic():
+    """The channel grouping's random swaps follow a fixed sequence: two
+    builds of the same set give the same tables."""
+    ks = rk.generate_kernels_multi(31, 2000, 300, 5)
+    a, b = rk.plan_tables(ks, 300), rk.plan_tables(ks, 300)
+    for key in ("items", "slot_kernel", "chan", "wpk", "order"):
+        assert np.array_equal(a[key], b[key]), key
 
 
 @pytest.mark.parametrize("seed,K,L", [(15, 300, 3000), (16, 400, 1500)])
