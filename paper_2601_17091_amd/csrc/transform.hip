@@ -1667,7 +1667,10 @@ __device__ __forceinline__ void series_block(const SeriesTiles &src, const float
     v4f acc[NT][G];
     tile_mfma<ELL, G, NT, false, true>(src, wa, binit, binit, acc);
     __builtin_amdgcn_sched_barrier(0);
+    // raised wave priority while the fold runs, as in the fused kernel
+    __builtin_amdgcn_s_setprio(1);
     series_reduce<G, NT, MPV>(acc, sa);
+    __builtin_amdgcn_s_setprio(0);
 }
 
 // The last positions of an item, nv (1..N) of them: a code copy per count.
