@@ -452,7 +452,7 @@ def minirocket_compares(params, L):
 
 
 def bench_minirocket(args):
-    """MINIROCKET (Sec. 5 names it): the Manufacturing series, 10,000
+    """MINIROCKET (Sec. 5 names it): the 100,000 series of 1,000 samples of the manufacturing workload, 10,000
     features fitted on the first 1,000 series; one step = one transform pass
     over every series (F [n, n_features] of PPVs)."""
     import torch

@@ -47,12 +47,13 @@ constexpr uint64_t kNegInfPair = 0xff800000ff800000ull;  // two fp32 -inf
 
 // ---------------------------------------------------------------------------
 // Checked build (compiled with ROCKET_CHECKED=1 into librocket_checked.so):
-// every LDS tile read is checked against the bytes its workgroup staged and
-// every feature store against the rows and columns of its launch.  A failed
-// check sets a bit of g_rocket_checks (read and cleared by
-// rocket_check_flags) and the access is redirected inside the buffer, so a
-// wrong index never reads or writes outside it.  The product build compiles
-// none of this.
+// every LDS tile read is checked against the bytes its workgroup staged,
+// every feature store of the workgroup kernels against the rows and columns
+// of its launch, and every slot column the series-lane permutation reads
+// against the plan's slots.  A failed check sets a bit of g_rocket_checks
+// (read and cleared by rocket_check_flags) and the access is redirected
+// inside the buffer or skipped, so a wrong index never reads or writes
+// outside it.  The product build compiles none of this.
 // ---------------------------------------------------------------------------
 #ifndef ROCKET_CHECKED
 #define ROCKET_CHECKED 0
@@ -579,7 +580,8 @@ __device__ __forceinline__ void read_tiles(const Src &src, int j, float (&xv)[NT
 // MFMAs (blocks of up to 4 tiles).  Only the series-lane reads: in the
 // fused kernel the second set of tile registers lowers the occupancy from 5
 // to 4 wavefronts per SIMD (100-thousand-series calls 2.2 % slower), while
-// the series-lane kernel keeps its register count (Many-short 0.4 % faster).
+// the series-lane kernel keeps its register count (a million 64-sample
+// series: 0.4 % faster).
 template <typename Src>
 struct PipelinedReads {
     static constexpr bool value = false;
@@ -760,7 +762,8 @@ __device__ __forceinline__ void tile_block(const Src &src, const float (&wa)[G][
     __builtin_amdgcn_sched_barrier(0);
     // raised wave priority while the reduction runs: a wavefront that has
     // finished its MFMAs gets its vector work issued first (measured: 0.4 %
-    // faster Manufacturing passes, 0.7 % faster long series; same results)
+    // faster passes over 100,000 series of 1,000 samples, 0.7 % faster long
+    // series; same results)
     __builtin_amdgcn_s_setprio(1);
     block_reduce<G, NT, MPV>(acc, ra);
     __builtin_amdgcn_s_setprio(0);
