@@ -452,9 +452,10 @@ def minirocket_compares(params, L):
 
 
 def bench_minirocket(args):
-    """MINIROCKET (Sec. 5 names it): the 100,000 series of 1,000 samples of the manufacturing workload, 10,000
-    features fitted on the first 1,000 series; one step = one transform pass
-    over every series (F [n, n_features] of PPVs)."""
+    """MINIROCKET (Sec. 5 names it): the manufacturing workload's 100,000
+    series of 1,000 samples, 10,000 features fitted on the first 1,000
+    series; one step = one transform pass over every series (F [n,
+    n_features] of PPVs)."""
     import torch
 
     import paper_2601_17091_amd as rk
